@@ -1,0 +1,160 @@
+"""CPU oracle for BEV pooling (BEVFusion, arXiv 2205.13542, Sec. III-B).
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke entry point and the benchmark's
+CPU-baseline leg may use it; the product path never does. It shares no code
+with the GPU library (``paper_2205_13542_amd``) and imports nothing from it.
+
+The arithmetic lives in ``bevpool_oracle.c`` (plain C, double precision,
+built without FMA contraction or fast-math). This module builds it with gcc,
+loads it with ctypes and marshals numpy arrays.
+
+Functions and the passages they follow:
+
+- ``cell_map``: grid index of every frustum point, -1 when dropped
+  (Sec. III-B: lifting pixels to D points along the camera ray, quantising
+  x and y at step r, one z slab; "Precomputation": the 3-D coordinate and
+  grid index of each point).
+- ``sort_by_cell``: points ordered by grid index, ties by point id, and the
+  interval table ("Precomputation": sort by grid index and record ranks;
+  "Interval Reduction": a cell's points are then consecutive).
+- ``pool``: per-cell sums of P * F ("Interval Reduction": sum is one of the
+  symmetric aggregations; "Takeaways": exact, no approximation).
+
+Pins, i.e. what the tests hold this oracle to (none of them re-types its
+formulas): closed-form cell maps of two dyadic rigs, a homogeneous-matrix
+projection through numpy.linalg, numpy's lexsort, a dense 0/1 matrix
+product, the count test, mass conservation, and permutation, linearity and
+boundary cases. Values at the nuScenes-shaped sizes are pinned only by these
+properties: the paper prints no pooled value (parity unpinned by the paper,
+pinned by the invariants).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "bevpool_oracle.c")
+LIB_PATH = os.path.join(_HERE, "liboracle.so")
+
+_lib = None
+
+
+class _Geom(ctypes.Structure):
+    _fields_ = [
+        ("n_cams", ctypes.c_int32), ("feat_h", ctypes.c_int32),
+        ("feat_w", ctypes.c_int32), ("n_depth", ctypes.c_int32),
+        ("depth_min", ctypes.c_double), ("depth_step", ctypes.c_double),
+        ("pixel_offset", ctypes.c_double),
+        ("nx", ctypes.c_int32), ("ny", ctypes.c_int32),
+        ("x_min", ctypes.c_double), ("y_min", ctypes.c_double),
+        ("cell_x", ctypes.c_double), ("cell_y", ctypes.c_double),
+        ("z_min", ctypes.c_double), ("z_cell", ctypes.c_double),
+    ]
+
+
+def build() -> str:
+    """Compile the oracle with gcc (always, so a stale build never survives)."""
+    tmp = LIB_PATH + ".tmp"
+    cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math",
+           "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, LIB_PATH)
+    return LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        build()
+    lib = ctypes.CDLL(LIB_PATH)
+    P = ctypes.c_void_p
+    lib.oracle_cell_map.argtypes = [P, P, ctypes.POINTER(_Geom), P]
+    lib.oracle_cell_map.restype = ctypes.c_int64
+    lib.oracle_sort_by_cell.argtypes = [P, ctypes.c_int64, ctypes.c_int32, P, P]
+    lib.oracle_sort_by_cell.restype = None
+    lib.oracle_pool.argtypes = [P, P, P, ctypes.POINTER(_Geom), ctypes.c_int32,
+                                ctypes.c_int32, P, P, P]
+    lib.oracle_pool.restype = None
+    lib.oracle_max_threads.argtypes = []
+    lib.oracle_max_threads.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _geom(rig) -> _Geom:
+    return _Geom(rig.n_cams, rig.feat_h, rig.feat_w, rig.n_depth,
+                 rig.depth_min, rig.depth_step, rig.pixel_offset,
+                 rig.nx, rig.ny, rig.x_min, rig.y_min, rig.cell_x, rig.cell_y,
+                 rig.z_min, rig.z_cell)
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def cell_map(rig) -> np.ndarray:
+    """int32 [N*D*H*W]: cell id of each point in point-id order, -1 if dropped."""
+    lib = _load()
+    intr = np.ascontiguousarray(rig.intrinsics, dtype=np.float64).reshape(-1)
+    extr = np.ascontiguousarray(rig.extrinsics, dtype=np.float64).reshape(-1)
+    assert intr.size == 4 * rig.n_cams and extr.size == 12 * rig.n_cams
+    out = np.empty(rig.n_points, dtype=np.int32)
+    g = _geom(rig)
+    lib.oracle_cell_map(_ptr(intr), _ptr(extr), ctypes.byref(g), _ptr(out))
+    return out
+
+
+def sort_by_cell(cell_of_point: np.ndarray, n_cells: int):
+    """(sorted_point int32 [K], cell_start int32 [n_cells + 1])."""
+    lib = _load()
+    cop = np.ascontiguousarray(cell_of_point, dtype=np.int32)
+    kept = int((cop >= 0).sum())
+    sorted_point = np.empty(kept, dtype=np.int32)
+    cell_start = np.empty(n_cells + 1, dtype=np.int32)
+    lib.oracle_sort_by_cell(_ptr(cop), cop.size, n_cells, _ptr(sorted_point),
+                            _ptr(cell_start))
+    return sorted_point, cell_start
+
+
+def plan(rig):
+    """The canonical plan: (cell_of_point, sorted_point, cell_start)."""
+    cop = cell_map(rig)
+    sp, cs = sort_by_cell(cop, rig.n_cells)
+    return cop, sp, cs
+
+
+def pool(rig, cell_of_point: np.ndarray, P: np.ndarray, F: np.ndarray,
+         want_f64: bool = False, want_abs: bool = False):
+    """Sum pooling. P float32 [B][N][D][H][W], F float32 [B][N][H][W][C].
+    Returns float32 [B][ny][nx][C]; with want_f64 / want_abs also the
+    double sums and the double sums of |P * F| (in that order)."""
+    lib = _load()
+    P = np.ascontiguousarray(P, dtype=np.float32)
+    F = np.ascontiguousarray(F, dtype=np.float32)
+    B = P.shape[0]
+    C = F.shape[-1]
+    assert P.size == B * rig.n_points and F.size == B * rig.n_pixels * C
+    cop = np.ascontiguousarray(cell_of_point, dtype=np.int32)
+    out = np.empty((B, rig.ny, rig.nx, C), dtype=np.float32)
+    o64 = np.empty(out.shape, dtype=np.float64) if want_f64 else None
+    a64 = np.empty(out.shape, dtype=np.float64) if want_abs else None
+    g = _geom(rig)
+    lib.oracle_pool(_ptr(P), _ptr(F), _ptr(cop), ctypes.byref(g), B, C, _ptr(out),
+                    _ptr(o64) if o64 is not None else None,
+                    _ptr(a64) if a64 is not None else None)
+    res = [out]
+    if want_f64:
+        res.append(o64)
+    if want_abs:
+        res.append(a64)
+    return res[0] if len(res) == 1 else tuple(res)
+
+
+def max_threads() -> int:
+    return int(_load().oracle_max_threads())
