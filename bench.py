@@ -1,0 +1,248 @@
+#!/usr/bin/env python3
+"""Benchmark of the BEV-pooling forward pass on one MI355X.
+
+One step is one bevpool_forward over one batch: the fused lift (P x F) and
+per-cell sum for every BEV cell. This is the whole per-frame hot path. The
+plan is built once beforehand and timed separately.
+
+The default workload is the nuScenes-shaped frame: 6 cameras x 118 depth
+bins x 32x88 features, C = 80 fp32, pooled to a 360x360 grid. Inputs are
+seeded synthetic data already resident in device memory.
+
+Timing: before every timed step a 1 GiB fill evicts the L2s and the
+Infinity Cache, so each forward reads its inputs from HBM. HIP events on the
+stream that runs the kernel bracket the forward alone. The headline `value`
+is algorithmic bytes (P + F read once, the BEV map written once) divided by
+the mean event time. The warm figure (no eviction) is reported beside it.
+
+Prints one JSON line. See `--help` for the knobs.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("BEV-pool forward ms + HBM GB/s, 6cam×118D×32×88×C80"
+          "→360×360 BEV, 1 GPU")
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, AMD published figure
+FLUSH_BYTES = 1 << 30
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "forward_traffic.json")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2205_13542_amd", "csrc", "forward.hip")
+
+WORKLOAD_TEXT = {
+    "nuscenes": "nuScenes-shaped frame: 6 cams x 118 depth bins x 32x88, C=80 fp32 -> 360x360 BEV at 0.3 m",
+    "nuscenes_bf16": "nuScenes-shaped frame, bf16 P and F, fp32 accumulate/output -> 360x360",
+    "nuscenes_f16": "nuScenes-shaped frame, fp16 P and F, fp32 accumulate/output -> 360x360",
+    "nuscenes_b8": "8 nuScenes-shaped frames sharing one plan, C=80 fp32 -> 8 x 360x360",
+    "highres": "6 cams x 236 bins x 64x176, C=128 fp32, 90% one-hot depth -> 720x720 at 0.15 m",
+}
+
+
+def parse_args():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="nuscenes", choices=sorted(WORKLOAD_TEXT))
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip the oracle timing on the host cores")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="approximate CPU time budget of the oracle sample")
+    return ap.parse_args()
+
+
+def algorithmic_bytes(w) -> int:
+    """P and F read once, the BEV map written once (fp32)."""
+    rig = w.rig
+    esize = 4 if w.dtype == "f32" else 2
+    p = w.batch * rig.n_points * esize
+    f = w.batch * rig.n_pixels * w.channels * esize
+    o = w.batch * rig.n_cells * w.channels * 4
+    return p + f + o
+
+
+def kernel_hash() -> str:
+    with open(KERNEL_SOURCE, "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()[:16]
+
+
+def load_traffic(workload: str):
+    """Counter-measured HBM bytes per launch, if they were taken for the
+    current kernel source (else None)."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            rec = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    entry = rec.get("workloads", {}).get(workload)
+    if not entry or rec.get("kernel_sha256_16") != kernel_hash():
+        return None
+    return entry.get("hbm_bytes_per_launch")
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(w, nbytes: int, budget_s: float):
+    """The oracle as it stands, on the host cores: whole frames of the same
+    workload until about budget_s seconds have passed (at least one)."""
+    import oracle
+    t0 = time.perf_counter()
+    cop = oracle.cell_map(w.rig)
+    plan_s = time.perf_counter() - t0
+    frames, spent = 0, 0.0
+    while frames == 0 or (spent < budget_s and frames < 64):
+        b = frames % w.batch
+        t0 = time.perf_counter()
+        oracle.pool(w.rig, cop, w.P[b:b + 1], w.F[b:b + 1])
+        spent += time.perf_counter() - t0
+        frames += 1
+    per_frame_bytes = nbytes / w.batch
+    return {
+        "value": round(per_frame_bytes * frames / spent / 1e9, 4),
+        "unit": "GB/s",
+        "cores": oracle.max_threads(),
+        "kind": "oracle",
+        "sample": f"{frames} whole frame(s) of the same workload, {spent:.1f} s of pooling "
+                  f"({spent / frames * 1e3:.0f} ms/frame); cell map {plan_s * 1e3:.0f} ms; "
+                  f"host CPU {cpu_model()}, os.cpu_count()={os.cpu_count()}",
+    }
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the pooling shards by BEV tiles or frames without a collective; see the design "
+              "notes)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import workloads as wl
+    import paper_2205_13542_amd as bp
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    w = wl.make(args.workload, seed=0)
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[w.dtype]
+    P = torch.from_numpy(w.P).to(dev).to(tdt).contiguous()
+    F = torch.from_numpy(w.F).to(dev).to(tdt).contiguous()
+    out = torch.empty((w.batch, w.rig.ny, w.rig.nx, w.channels), dtype=torch.float32, device=dev)
+    flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    # plan build (one-off, reported separately)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    plan = bp.Plan.from_rig(w.rig, stream=stream)
+    plan_ms = (time.perf_counter() - t0) * 1e3
+    info = plan.info
+
+    for _ in range(args.warmup):
+        flush.zero_()
+        plan.forward(P, F, out=out, stream=stream)
+    torch.cuda.synchronize()
+
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        flush.zero_()
+        starts[k].record(stream)
+        plan.forward(P, F, out=out, stream=stream)
+        ends[k].record(stream)
+    torch.cuda.synchronize()
+    wall_s = time.perf_counter() - t0
+    cold_ms = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
+
+    # warm: back-to-back launches, no eviction (the whole working set fits
+    # the 256 MB Infinity Cache); secondary figure
+    warm_steps = max(10, args.steps)
+    ws = torch.cuda.Event(enable_timing=True)
+    we = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ws.record(stream)
+    for _ in range(warm_steps):
+        plan.forward(P, F, out=out, stream=stream)
+    we.record(stream)
+    torch.cuda.synchronize()
+    warm_ms = ws.elapsed_time(we) / warm_steps
+
+    nbytes = algorithmic_bytes(w)
+    mean_ms = float(cold_ms.mean())
+    gbs = nbytes / (mean_ms * 1e-3) / 1e9
+    traffic = load_traffic(args.workload)
+    rec = {
+        "metric": METRIC,
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(mean_ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": WORKLOAD_TEXT[args.workload],
+            "name": args.workload,
+            "batch": w.batch,
+            "cameras": w.rig.n_cams, "depth_bins": w.rig.n_depth,
+            "feat_hw": [w.rig.feat_h, w.rig.feat_w], "channels": w.channels,
+            "bev": [w.rig.ny, w.rig.nx],
+            "points": info.n_points, "kept": info.n_kept,
+            "nonempty_cells": info.n_nonempty, "max_per_cell": info.max_per_cell,
+            "tiles": info.n_tiles,
+        },
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(gbs, 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(gbs / HBM_PEAK_GBS, 4),
+            "traffic": traffic,
+        },
+        "forward_us": {"mean": round(mean_ms * 1e3, 2),
+                       "median": round(float(np.median(cold_ms)) * 1e3, 2),
+                       "min": round(float(cold_ms.min()) * 1e3, 2),
+                       "p90": round(float(np.percentile(cold_ms, 90)) * 1e3, 2),
+                       "warm_mean": round(warm_ms * 1e3, 2)},
+        "algorithmic_bytes": nbytes,
+        "plan_bytes": 4 * (info.n_kept + info.n_cells + 1 + info.n_tiles + 1),
+        "plan_build_ms": round(plan_ms, 2),
+        "wall_s_timed_loop": round(wall_s, 4),
+        "kernel_sha256_16": kernel_hash(),
+        "device": torch.cuda.get_device_name(dev),
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(w, nbytes, args.cpu_seconds)
+    plan.close()
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,183 @@
+/*
+ * bevpool.h -- C ABI of libbevpool.so: camera-to-BEV pooling on MI355X (gfx950).
+ *
+ * The operation is the BEV pooling step of BEVFusion (arXiv 2205.13542,
+ * Sec. III-B). Each camera feature pixel is lifted to D points along its
+ * camera ray, and each point carries its depth probability times the pixel's
+ * feature vector. The points are quantised to an r x r BEV grid and flattened
+ * along z (first paragraph). All points of a cell are summed (the "Interval
+ * Reduction" paragraph allows sum, mean or max; this library sums).
+ *
+ * The point-to-cell association depends only on the calibration, so it is
+ * computed once per rig ("Precomputation" paragraph). That is bevpool_plan.
+ * Every frame then runs bevpool_forward.
+ *
+ * Conventions that hold for every call:
+ *  - Return value: BEVPOOL_OK (0) on success, a negative BEVPOOL_ERR_* code
+ *    otherwise. bevpool_last_error() then gives a message. No C++ exception
+ *    and no abort crosses this boundary.
+ *  - Pointers marked "host" are ordinary CPU memory. Pointers marked "device"
+ *    are HIP device memory on the current device.
+ *  - The caller owns every input and output buffer. The library owns the
+ *    plan and its device buffers until bevpool_plan_destroy.
+ *  - hip_stream is a hipStream_t passed as void*; NULL is the null stream.
+ */
+#ifndef BEVPOOL_H
+#define BEVPOOL_H
+
+#include <stdint.h>
+
+/* Exported symbols stay visible when the library is built with hidden
+ * default visibility. */
+#ifndef BEVPOOL_API
+#if defined(__GNUC__)
+#define BEVPOOL_API __attribute__((visibility("default")))
+#else
+#define BEVPOOL_API
+#endif
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes. */
+#define BEVPOOL_OK 0
+#define BEVPOOL_ERR_INVALID_ARG (-1)       /* null pointer, non-positive size, non-finite or zero parameter */
+#define BEVPOOL_ERR_SHAPE_MISMATCH (-2)    /* a size does not agree with the plan */
+#define BEVPOOL_ERR_UNSUPPORTED_DTYPE (-3) /* dtype not one of bevpool_dtype */
+#define BEVPOOL_ERR_OVERFLOW (-4)          /* a point, pixel or output index would not fit in int32 */
+#define BEVPOOL_ERR_OOM (-5)               /* device allocation failed */
+#define BEVPOOL_ERR_HIP (-6)               /* a HIP runtime call failed (message has the HIP error) */
+
+/* Element type of depth_prob and cam_feat. Accumulation and output are fp32. */
+typedef enum { BEVPOOL_F32 = 0, BEVPOOL_BF16 = 1, BEVPOOL_F16 = 2 } bevpool_dtype;
+
+/*
+ * Frustum and BEV grid (Sec. III-B, first paragraph: N cameras, an H x W
+ * feature map, D depth bins, grid step r, z flattened).
+ *  - Depth bin k lies at camera-frame depth depth_min + k * depth_step,
+ *    k in [0, n_depth). The paper's typical workload uses 1 m + 0.5 m * k,
+ *    118 bins (Sec. III-B footnote).
+ *  - Feature pixel (h, w) sits at image point (w + pixel_offset, h + pixel_offset)
+ *    in feature-grid pixels.
+ *  - Cells: ix = floor((x - x_min) / cell_x) in [0, nx) and
+ *    iy = floor((y - y_min) / cell_y) in [0, ny), in the ego frame. One z slab:
+ *    a point is kept only if floor((z - z_min) / z_cell) == 0.
+ *  - Cell id = iy * nx + ix. Points outside the grid or the slab are dropped.
+ */
+typedef struct {
+    int32_t n_cams, feat_h, feat_w, n_depth; /* N, H, W, D */
+    double depth_min, depth_step;            /* depth of bin k = depth_min + k * depth_step */
+    double pixel_offset;                     /* usually 0.5 (pixel centres) */
+    int32_t nx, ny;                          /* cells along ego x and ego y */
+    double x_min, y_min, cell_x, cell_y;     /* grid origin and cell sides, metres */
+    double z_min, z_cell;                    /* the single z slab [z_min, z_min + z_cell) */
+} bevpool_geometry;
+
+/* Opaque plan: the camera-fixed point-to-cell association on the device. */
+typedef struct bevpool_plan_s bevpool_plan_t;
+
+/*
+ * Build the plan ("Precomputation" paragraph of Sec. III-B).
+ *  intrinsics: host double[n_cams][4] = {fx, fy, cx, cy}, in feature-grid pixels.
+ *  extrinsics: host double[n_cams][12] = row-major [R | t], camera to ego:
+ *              p_ego = R p_cam + t. Camera axes are x right, y down, z forward.
+ *  geom:       host; copied.
+ *  hip_stream: stream on which the plan kernels run.
+ *  out_plan:   receives the new plan; on failure *out_plan is set to NULL.
+ *
+ * The frustum point with camera n, depth bin d and pixel (h, w) has id
+ * p = ((n * D + d) * H + h) * W + w. Its camera-frame position is
+ * depth * ((u - cx) / fx, (v - cy) / fy, 1). That position is mapped to the
+ * ego frame and quantised. Everything is evaluated in IEEE double in a fixed
+ * order with no fused multiply-add. The resulting cell ids match a plain CPU
+ * evaluation of the same expressions bit for bit.
+ *
+ * The plan holds four things:
+ *  - cell_of_point: each point's cell, or -1 if dropped;
+ *  - sorted_point: the kept points ordered by cell, ties broken by point id;
+ *  - cell_start: the interval table, so cell c owns
+ *    sorted_point[cell_start[c] .. cell_start[c+1]);
+ *  - a work partition used by bevpool_forward.
+ *
+ * Allocates device memory and synchronises hip_stream before returning.
+ * The calibration arrays may be freed as soon as the call returns.
+ * Errors: INVALID_ARG (null pointer, a size < 1, a non-finite value, a zero
+ * focal length, a non-positive step or cell side), OVERFLOW (N*D*H*W or
+ * nx*ny + 1 does not fit in int32), OOM, HIP.
+ */
+BEVPOOL_API int bevpool_plan(const double *intrinsics, const double *extrinsics,
+                 const bevpool_geometry *geom, void *hip_stream,
+                 bevpool_plan_t **out_plan);
+
+/*
+ * Pool one batch of frames with a plan (Sec. III-B: lift P x F, sum each
+ * cell's points; "Interval Reduction": the result is written per cell,
+ * without partial sums in memory).
+ *
+ *  depth_prob: device [batch][N][D][H][W] of dtype.
+ *  cam_feat:   device [batch][N][H][W][channels] of dtype.
+ *  bev_out:    device float [batch][ny][nx][channels]. Every element is
+ *              overwritten, and cells with no kept point are set to 0.
+ *  batch, channels >= 1. N, D, H, W, nx and ny come from the plan; the
+ *  caller's buffers must have those sizes (the library cannot see them).
+ *
+ * out[b][cell][c] = sum over kept points p of cell of
+ * depth_prob[b][p] * cam_feat[b][pixel(p)][c]. The sum is accumulated in fp32
+ * in an order fixed by the plan, so repeated calls give bitwise equal
+ * results. bev_out is written with plain stores, no atomics.
+ *
+ * Inputs must be finite; non-finite inputs give unspecified output.
+ * Asynchronous on hip_stream: no host synchronisation, no allocation.
+ * Inputs must not overlap bev_out.
+ * The fast path needs channels % 4 == 0 and 16-byte aligned cam_feat and
+ * bev_out (8-byte aligned cam_feat for 16-bit dtypes); other cases take a
+ * slower path with the same results.
+ * A plan may be used from several streams at once.
+ * Errors: INVALID_ARG (null pointer or a bad plan handle, batch or
+ * channels < 1), UNSUPPORTED_DTYPE, OVERFLOW (N*H*W*channels or
+ * nx*ny*channels does not fit in int32), HIP (launch failure).
+ */
+BEVPOOL_API int bevpool_forward(const void *depth_prob, const void *cam_feat,
+                    const bevpool_plan_t *plan, float *bev_out,
+                    int32_t batch, int32_t channels, int32_t dtype,
+                    void *hip_stream);
+
+/* Sizes of a plan. All counts are per frame. */
+typedef struct {
+    int64_t n_points;     /* N*D*H*W */
+    int64_t n_kept;       /* points inside the grid and the z slab */
+    int32_t n_cells;      /* nx*ny */
+    int32_t n_nonempty;   /* cells with at least one point */
+    int32_t max_per_cell; /* largest interval */
+    int32_t n_tiles;      /* work items of bevpool_forward (one workgroup each) */
+    int32_t n_cams, n_depth, feat_h, feat_w, nx, ny;
+} bevpool_plan_info;
+
+/* Fill *info. Host only, no device work. Errors: INVALID_ARG. */
+BEVPOOL_API int bevpool_plan_info_get(const bevpool_plan_t *plan, bevpool_plan_info *info);
+
+/*
+ * Copy the plan's association to host arrays: cell_of_point [n_points],
+ * sorted_point [n_kept] and cell_start [n_cells + 1]. Any of them may be
+ * NULL to skip it. Synchronous. Errors: INVALID_ARG, HIP.
+ */
+BEVPOOL_API int bevpool_plan_export(const bevpool_plan_t *plan, int32_t *cell_of_point,
+                        int32_t *sorted_point, int32_t *cell_start);
+
+/* Free a plan and its device memory. NULL-safe. The plan must not be in use
+ * by work still queued on a stream. */
+BEVPOOL_API void bevpool_plan_destroy(bevpool_plan_t *plan);
+
+/* Message for the last nonzero return on the calling thread ("" if none). */
+BEVPOOL_API const char *bevpool_last_error(void);
+
+/* Library version as major * 10000 + minor * 100 + patch. */
+BEVPOOL_API int32_t bevpool_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BEVPOOL_H */

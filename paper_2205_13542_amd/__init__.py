@@ -1,0 +1,125 @@
+"""BEV pooling on MI355X: camera-fixed plan + per-frame fused lift-and-sum.
+
+The camera-to-BEV transform of BEVFusion (arXiv 2205.13542, Sec. III-B):
+each camera feature pixel is lifted to D points along its ray, each carrying
+P[n,d,h,w] * F[n,h,w,:]. Every point is quantised to an r x r BEV cell, and
+the points of each cell are summed. The work runs in libbevpool.so
+(hand-written HIP for gfx950) behind the C ABI of include/bevpool.h. This
+package is the thin binding: ``_binding`` mirrors the C calls one to one, and
+``Plan`` adds torch tensor plumbing (device memory and the current stream
+only). There is no CPU fallback. A missing library raises ImportError.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import _binding
+from ._binding import (BEVPOOL_BF16, BEVPOOL_F16, BEVPOOL_F32, BevpoolError,
+                       bevpool_forward, bevpool_geometry, bevpool_last_error,
+                       bevpool_plan, bevpool_plan_destroy, bevpool_plan_export,
+                       bevpool_plan_info_get, bevpool_version)
+
+__all__ = [
+    "Plan", "BevpoolError", "bevpool_plan", "bevpool_forward", "bevpool_plan_info_get",
+    "bevpool_plan_export", "bevpool_plan_destroy", "bevpool_last_error", "bevpool_version",
+    "bevpool_geometry", "geometry_of", "BEVPOOL_F32", "BEVPOOL_BF16", "BEVPOOL_F16",
+]
+
+_GEOM_FIELDS = [f for f, _ in bevpool_geometry._fields_]
+
+
+def geometry_of(rig) -> bevpool_geometry:
+    """bevpool_geometry from any object (or mapping) with the same field names."""
+    get = rig.__getitem__ if isinstance(rig, dict) else (lambda k: getattr(rig, k))
+    return bevpool_geometry(*[get(f) for f in _GEOM_FIELDS])
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    codes = {torch.float32: BEVPOOL_F32, torch.bfloat16: BEVPOOL_BF16, torch.float16: BEVPOOL_F16}
+    if t.dtype not in codes:
+        raise BevpoolError(_binding.BEVPOOL_ERR_UNSUPPORTED_DTYPE, f"dtype {t.dtype}")
+    return codes[t.dtype]
+
+
+class Plan:
+    """A plan on the current HIP device (see bevpool_plan in bevpool.h).
+
+    ``Plan(intrinsics, extrinsics, geometry)``: intrinsics [N][4] and
+    extrinsics [N][12] float64 host arrays; geometry has the
+    bevpool_geometry fields (e.g. a rig object or a dict).
+    """
+
+    def __init__(self, intrinsics, extrinsics, geometry, stream=None):
+        torch = _torch()
+        _binding.load()
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        self.geometry = geometry_of(geometry)
+        self.handle = bevpool_plan(np.asarray(intrinsics, dtype=np.float64),
+                                   np.asarray(extrinsics, dtype=np.float64),
+                                   self.geometry, stream.cuda_stream)
+        self.info = bevpool_plan_info_get(self.handle)
+
+    @classmethod
+    def from_rig(cls, rig, stream=None) -> "Plan":
+        return cls(rig.intrinsics, rig.extrinsics, rig, stream)
+
+    def close(self) -> None:
+        if getattr(self, "handle", None):
+            bevpool_plan_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def export(self):
+        """(cell_of_point, sorted_point, cell_start) as host int32 arrays."""
+        i = self.info
+        cop = np.empty(i.n_points, dtype=np.int32)
+        sp = np.empty(i.n_kept, dtype=np.int32)
+        cs = np.empty(i.n_cells + 1, dtype=np.int32)
+        bevpool_plan_export(self.handle, cop, sp, cs)
+        return cop, sp, cs
+
+    def forward(self, depth_prob, cam_feat, out=None, stream=None):
+        """depth_prob [B][N][D][H][W], cam_feat [B][N][H][W][C] device tensors
+        of one dtype (fp32, bf16 or fp16); returns fp32 [B][ny][nx][C]."""
+        torch = _torch()
+        i = self.info
+        if depth_prob.dim() != 5 or cam_feat.dim() != 5:
+            raise BevpoolError(_binding.BEVPOOL_ERR_SHAPE_MISMATCH,
+                               "depth_prob and cam_feat must be 5-D")
+        B, C = depth_prob.shape[0], cam_feat.shape[-1]
+        if tuple(depth_prob.shape) != (B, i.n_cams, i.n_depth, i.feat_h, i.feat_w):
+            raise BevpoolError(_binding.BEVPOOL_ERR_SHAPE_MISMATCH,
+                               f"depth_prob shape {tuple(depth_prob.shape)} does not match the plan")
+        if tuple(cam_feat.shape) != (B, i.n_cams, i.feat_h, i.feat_w, C):
+            raise BevpoolError(_binding.BEVPOOL_ERR_SHAPE_MISMATCH,
+                               f"cam_feat shape {tuple(cam_feat.shape)} does not match the plan")
+        if cam_feat.dtype != depth_prob.dtype:
+            raise BevpoolError(_binding.BEVPOOL_ERR_UNSUPPORTED_DTYPE,
+                               "depth_prob and cam_feat must share a dtype")
+        if not (depth_prob.is_cuda and cam_feat.is_cuda):
+            raise BevpoolError(_binding.BEVPOOL_ERR_INVALID_ARG, "inputs must be device tensors")
+        if not (depth_prob.is_contiguous() and cam_feat.is_contiguous()):
+            raise BevpoolError(_binding.BEVPOOL_ERR_INVALID_ARG, "inputs must be contiguous")
+        if out is None:
+            out = torch.empty((B, i.ny, i.nx, C), dtype=torch.float32, device=cam_feat.device)
+        elif (tuple(out.shape) != (B, i.ny, i.nx, C) or out.dtype != torch.float32
+              or not out.is_contiguous() or not out.is_cuda):
+            raise BevpoolError(_binding.BEVPOOL_ERR_SHAPE_MISMATCH,
+                               "out must be a contiguous fp32 device tensor [B][ny][nx][C]")
+        if stream is None:
+            stream = torch.cuda.current_stream(cam_feat.device)
+        bevpool_forward(depth_prob.data_ptr(), cam_feat.data_ptr(), self.handle, out.data_ptr(),
+                        B, C, _dtype_code(cam_feat), stream.cuda_stream)
+        return out

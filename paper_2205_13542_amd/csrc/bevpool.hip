@@ -1,0 +1,164 @@
+// C ABI of libbevpool.so (declared in include/bevpool.h): argument checks,
+// error reporting and plan ownership. Device work is in plan.hip and
+// forward.hip.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <new>
+
+#include "internal.h"
+
+namespace {
+thread_local char g_last_error[512] = "";
+
+bool finite_all(const double *v, size_t n) {
+    for (size_t i = 0; i < n; ++i)
+        if (!isfinite(v[i])) return false;
+    return true;
+}
+
+bool valid_plan(const bevpool_plan_t *plan) { return plan != nullptr && plan->magic == kPlanMagic; }
+
+void free_plan(bevpool_plan_s *plan) {
+    if (!plan) return;
+    int prev = -1;
+    (void)hipGetDevice(&prev);
+    if (prev != plan->device) (void)hipSetDevice(plan->device);
+    (void)hipFree(plan->cell_of_point);
+    (void)hipFree(plan->sorted_point);
+    (void)hipFree(plan->cell_start);
+    (void)hipFree(plan->tile_cell);
+    if (prev >= 0 && prev != plan->device) (void)hipSetDevice(prev);
+    plan->magic = 0;
+    delete plan;
+}
+}  // namespace
+
+int bevpool_fail(int code, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int bevpool_hip_fail(hipError_t err, const char *what) {
+    return bevpool_fail(BEVPOOL_ERR_HIP, "HIP error %d (%s) in %s", int(err), hipGetErrorString(err),
+                        what);
+}
+
+extern "C" {
+
+const char *bevpool_last_error(void) { return g_last_error; }
+
+int32_t bevpool_version(void) { return 100; }  // 0.1.0
+
+int bevpool_plan(const double *intrinsics, const double *extrinsics, const bevpool_geometry *geom,
+                 void *hip_stream, bevpool_plan_t **out_plan) {
+    g_last_error[0] = '\0';
+    if (!out_plan) return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "out_plan is NULL");
+    *out_plan = nullptr;
+    if (!intrinsics || !extrinsics || !geom)
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "intrinsics, extrinsics and geom must be non-NULL");
+    const bevpool_geometry &g = *geom;
+    if (g.n_cams < 1 || g.feat_h < 1 || g.feat_w < 1 || g.n_depth < 1 || g.nx < 1 || g.ny < 1)
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG,
+                            "sizes must be >= 1 (n_cams=%d feat_h=%d feat_w=%d n_depth=%d nx=%d ny=%d)",
+                            g.n_cams, g.feat_h, g.feat_w, g.n_depth, g.nx, g.ny);
+    const double params[] = {g.depth_min, g.depth_step, g.pixel_offset, g.x_min, g.y_min,
+                             g.cell_x,    g.cell_y,     g.z_min,        g.z_cell};
+    if (!finite_all(params, sizeof(params) / sizeof(params[0])))
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "geometry parameters must be finite");
+    if (!(g.depth_step > 0.0) || !(g.cell_x > 0.0) || !(g.cell_y > 0.0) || !(g.z_cell > 0.0))
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG,
+                            "depth_step, cell_x, cell_y and z_cell must be positive");
+    const int64_t np = int64_t(g.n_cams) * g.n_depth * g.feat_h * g.feat_w;
+    if (np > int64_t(INT32_MAX))
+        return bevpool_fail(BEVPOOL_ERR_OVERFLOW, "N*D*H*W = %lld points exceeds int32",
+                            (long long)np);
+    if (int64_t(g.nx) * g.ny + 1 > int64_t(INT32_MAX))
+        return bevpool_fail(BEVPOOL_ERR_OVERFLOW, "nx*ny = %lld cells exceeds int32",
+                            (long long)(int64_t(g.nx) * g.ny));
+    if (!finite_all(intrinsics, size_t(4) * g.n_cams) || !finite_all(extrinsics, size_t(12) * g.n_cams))
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "calibration values must be finite");
+    for (int n = 0; n < g.n_cams; ++n)
+        if (intrinsics[4 * n] == 0.0 || intrinsics[4 * n + 1] == 0.0)
+            return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "camera %d has a zero focal length", n);
+
+    bevpool_plan_s *plan = new (std::nothrow) bevpool_plan_s();
+    if (!plan) return bevpool_fail(BEVPOOL_ERR_OOM, "host allocation of the plan failed");
+    memset(plan, 0, sizeof(*plan));
+    plan->magic = kPlanMagic;
+    plan->geom = g;
+    hipError_t e = hipGetDevice(&plan->device);
+    if (e != hipSuccess) {
+        delete plan;
+        return bevpool_hip_fail(e, "hipGetDevice");
+    }
+    const int rc = bevpool_build_plan(intrinsics, extrinsics, g, hipStream_t(hip_stream), plan);
+    if (rc != BEVPOOL_OK) {
+        free_plan(plan);
+        return rc;
+    }
+    *out_plan = plan;
+    return BEVPOOL_OK;
+}
+
+int bevpool_forward(const void *depth_prob, const void *cam_feat, const bevpool_plan_t *plan,
+                    float *bev_out, int32_t batch, int32_t channels, int32_t dtype,
+                    void *hip_stream) {
+    if (!valid_plan(plan)) return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "invalid plan handle");
+    if (!depth_prob || !cam_feat || !bev_out)
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG,
+                            "depth_prob, cam_feat and bev_out must be non-NULL");
+    if (batch < 1 || channels < 1)
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "batch=%d and channels=%d must be >= 1", batch,
+                            channels);
+    if (dtype != BEVPOOL_F32 && dtype != BEVPOOL_BF16 && dtype != BEVPOOL_F16)
+        return bevpool_fail(BEVPOOL_ERR_UNSUPPORTED_DTYPE, "dtype %d is not F32, BF16 or F16", dtype);
+    return bevpool_launch_forward(depth_prob, cam_feat, plan, bev_out, batch, channels, dtype,
+                                  hipStream_t(hip_stream));
+}
+
+int bevpool_plan_info_get(const bevpool_plan_t *plan, bevpool_plan_info *info) {
+    if (!valid_plan(plan)) return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "invalid plan handle");
+    if (!info) return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "info is NULL");
+    info->n_points = plan->n_points;
+    info->n_kept = plan->n_kept;
+    info->n_cells = plan->n_cells;
+    info->n_nonempty = plan->n_nonempty;
+    info->max_per_cell = plan->max_per_cell;
+    info->n_tiles = plan->n_tiles;
+    info->n_cams = plan->geom.n_cams;
+    info->n_depth = plan->geom.n_depth;
+    info->feat_h = plan->geom.feat_h;
+    info->feat_w = plan->geom.feat_w;
+    info->nx = plan->geom.nx;
+    info->ny = plan->geom.ny;
+    return BEVPOOL_OK;
+}
+
+int bevpool_plan_export(const bevpool_plan_t *plan, int32_t *cell_of_point, int32_t *sorted_point,
+                        int32_t *cell_start) {
+    if (!valid_plan(plan)) return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "invalid plan handle");
+    if (cell_of_point)
+        BEVPOOL_HIP(hipMemcpy(cell_of_point, plan->cell_of_point,
+                              sizeof(int32_t) * size_t(plan->n_points), hipMemcpyDeviceToHost));
+    if (sorted_point)
+        BEVPOOL_HIP(hipMemcpy(sorted_point, plan->sorted_point,
+                              sizeof(int32_t) * size_t(plan->n_kept), hipMemcpyDeviceToHost));
+    if (cell_start)
+        BEVPOOL_HIP(hipMemcpy(cell_start, plan->cell_start,
+                              sizeof(int32_t) * (size_t(plan->n_cells) + 1), hipMemcpyDeviceToHost));
+    return BEVPOOL_OK;
+}
+
+void bevpool_plan_destroy(bevpool_plan_t *plan) {
+    if (!valid_plan(plan)) return;
+    free_plan(plan);
+}
+
+}  // extern "C"

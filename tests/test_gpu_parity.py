@@ -1,0 +1,262 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+- Plan: cell_of_point, sorted_point and cell_start must match bit for bit.
+- fp32 forward: every element within 1e-4 * sqrt(points in its cell), and
+  cells with no kept point exactly 0.
+- bf16 / fp16 inputs: both sides read the same rounded values. The bound is
+  2e-2 * sum |P * F| + 1e-6 per element, and the fp32 bound above must hold too.
+"""
+import dataclasses
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+@pytest.fixture(scope="module")
+def pkg(torch_cuda):
+    import paper_2205_13542_amd as pkg
+    pkg._binding.load()
+    return pkg
+
+
+def _coarse_rig():
+    """The nuScenes rig on a 3 m grid: cells with thousands of points (heavy
+    single-cell tiles staged in several rounds)."""
+    return dataclasses.replace(wl.ring_rig(), nx=36, ny=36, cell_x=3.0, cell_y=3.0)
+
+
+def _anisotropic_rig():
+    base = wl.tilt_rig(wl.ring_rig(), 3.0, -4.0)
+    intr = np.array([[35.0, 47.0, 21.5, 7.25], [41.0, 29.0, 24.0, 9.5]])
+    return dataclasses.replace(base, n_cams=2, feat_h=16, feat_w=44, n_depth=40,
+                               depth_min=0.75, depth_step=1.3, nx=150, ny=90,
+                               x_min=-40.0, y_min=-20.0, cell_x=0.55, cell_y=0.45,
+                               z_min=-1.0, z_cell=3.5, intrinsics=intr,
+                               extrinsics=base.extrinsics[[1, 4]].copy())
+
+
+def _empty_rig():
+    return dataclasses.replace(wl.tiny_rig(), x_min=100.0)      # grid far from the camera
+
+
+def _one_cell_rig():
+    return dataclasses.replace(wl.tiny_rig(), nx=1, ny=1, x_min=0.0, y_min=-8.0,
+                               cell_x=16.0, cell_y=16.0)
+
+
+RIGS = {
+    "tiny": wl.tiny_rig, "tiny_identity": wl.identity_rig, "nuscenes": wl.ring_rig,
+    "nuscenes_tilted": lambda: wl.tilt_rig(wl.ring_rig()), "highres": lambda: wl.ring_rig(2),
+    "anisotropic": _anisotropic_rig, "coarse": _coarse_rig, "empty": _empty_rig,
+    "one_cell": _one_cell_rig,
+}
+
+
+@pytest.fixture(scope="module")
+def oracle_plans(oracle_lib):
+    cache = {}
+
+    def get(name):
+        if name not in cache:
+            cache[name] = oracle_lib.plan(RIGS[name]())
+        return cache[name]
+    return get
+
+
+@pytest.mark.parametrize("name", list(RIGS))
+def test_plan_bit_exact(pkg, oracle_plans, name):
+    _say(f"[plan] {name}")
+    rig = RIGS[name]()
+    plan = pkg.Plan.from_rig(rig)
+    cop, sp, cs = plan.export()
+    rcop, rsp, rcs = oracle_plans(name)
+    assert np.array_equal(cop, rcop)
+    assert np.array_equal(sp, rsp)
+    assert np.array_equal(cs, rcs)
+    counts = np.diff(rcs)
+    assert plan.info.n_kept == rsp.size
+    assert plan.info.n_nonempty == int((counts > 0).sum())
+    assert plan.info.max_per_cell == int(counts.max(initial=0))
+    assert plan.info.n_points == rig.n_points and plan.info.n_cells == rig.n_cells
+    plan.close()
+
+
+def _to_device(torch, arr, dtype):
+    t = torch.from_numpy(np.ascontiguousarray(arr)).cuda()
+    return t.to({"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dtype])
+
+
+def _check_fp32(got, ref, counts):
+    """|got - ref| <= 1e-4 sqrt(count) per element; empty cells exactly 0."""
+    B = got.shape[0]
+    g = got.reshape(B, counts.size, -1)
+    r = ref.reshape(B, counts.size, -1)
+    bound = 1e-4 * np.sqrt(np.maximum(counts, 1))[None, :, None]
+    err = np.abs(g.astype(np.float64) - r.astype(np.float64))
+    worst = float((err / bound).max()) if err.size else 0.0
+    assert (err <= bound).all(), f"max err/bound {worst:.3g}"
+    assert (g[:, counts == 0] == 0).all()
+    return worst
+
+
+def _run(torch, pkg, plan, w):
+    P = _to_device(torch, w.P, w.dtype)
+    F = _to_device(torch, w.F, w.dtype)
+    out = plan.forward(P, F)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+@pytest.mark.parametrize("name,seed", [("tiny", 0), ("tiny_identity", 1), ("nuscenes", 0),
+                                       ("nuscenes_tilted", 2)])
+def test_forward_fp32(torch_cuda, pkg, oracle_lib, oracle_plans, name, seed):
+    _say(f"[forward fp32] {name} seed={seed}")
+    w = wl.make(name, seed=seed)
+    cop, _, cs = oracle_plans(name)
+    ref = oracle_lib.pool(w.rig, cop, w.P, w.F)
+    plan = pkg.Plan.from_rig(w.rig)
+    got = _run(torch_cuda, pkg, plan, w)
+    worst = _check_fp32(got, ref, np.diff(cs))
+    _say(f"  worst err/bound {worst:.3g}")
+
+
+@pytest.mark.parametrize("name", ["nuscenes_bf16", "nuscenes_f16"])
+def test_forward_reduced_precision(torch_cuda, pkg, oracle_lib, oracle_plans, name):
+    _say(f"[forward {name}]")
+    w = wl.make(name, seed=0)
+    cop, _, cs = oracle_plans("nuscenes")
+    ref, ref64, abs64 = oracle_lib.pool(w.rig, cop, w.P, w.F, want_f64=True, want_abs=True)
+    plan = pkg.Plan.from_rig(w.rig)
+    got = _run(torch_cuda, pkg, plan, w)
+    err = np.abs(got.astype(np.float64) - ref64)
+    assert (err <= 2e-2 * abs64 + 1e-6).all()
+    _check_fp32(got, ref, np.diff(cs))
+    rel = np.linalg.norm(got - ref64) / np.linalg.norm(ref64)
+    _say(f"  global relative L2 error {rel:.3g}")
+
+
+def test_forward_batched_matches_single_frames(torch_cuda, pkg, oracle_lib, oracle_plans):
+    _say("[forward batched] nuscenes_b8")
+    torch = torch_cuda
+    w = wl.make("nuscenes_b8", seed=0)
+    cop, _, cs = oracle_plans("nuscenes")
+    plan = pkg.Plan.from_rig(w.rig)
+    P = _to_device(torch, w.P, "f32")
+    F = _to_device(torch, w.F, "f32")
+    batched = plan.forward(P, F).cpu().numpy()
+    for b in range(w.batch):
+        single = plan.forward(P[b:b + 1].contiguous(), F[b:b + 1].contiguous()).cpu().numpy()
+        assert np.array_equal(batched[b:b + 1], single)
+    ref = oracle_lib.pool(w.rig, cop, w.P, w.F)
+    _check_fp32(batched, ref, np.diff(cs))
+
+
+def test_forward_highres(torch_cuda, pkg, oracle_lib, oracle_plans):
+    _say("[forward highres] 6x236x64x176 C=128 -> 720x720")
+    w = wl.make("highres", seed=0)
+    cop, _, cs = oracle_plans("highres")
+    ref = oracle_lib.pool(w.rig, cop, w.P, w.F)
+    plan = pkg.Plan.from_rig(w.rig)
+    got = _run(torch_cuda, pkg, plan, w)
+    _check_fp32(got, ref, np.diff(cs))
+
+
+@pytest.mark.parametrize("name", ["coarse", "anisotropic", "empty", "one_cell"])
+def test_forward_edge_rigs(torch_cuda, pkg, oracle_lib, oracle_plans, name):
+    _say(f"[forward edge] {name}")
+    rig = RIGS[name]()
+    P, F = wl.frames(rig, 16, 1, "normal", seed=5)
+    w = wl.Workload(name, rig, 16, 1, "f32", P, F)
+    cop, _, cs = oracle_plans(name)
+    ref = oracle_lib.pool(rig, cop, P, F)
+    plan = pkg.Plan.from_rig(rig)
+    got = _run(torch_cuda, pkg, plan, w)
+    _check_fp32(got, ref, np.diff(cs))
+    if name == "coarse":
+        assert plan.info.max_per_cell > 1536      # exercises the multi-round path
+    if name == "empty":
+        assert plan.info.n_kept == 0 and (got == 0).all()
+
+
+@pytest.mark.parametrize("channels", [1, 3, 5, 12, 64, 260])
+def test_forward_channel_counts(torch_cuda, pkg, oracle_lib, oracle_plans, channels):
+    """C not a multiple of 4 takes the scalar path; C > 256 takes two
+    channel passes on the vector path."""
+    _say(f"[forward channels] C={channels}")
+    rig = wl.tilt_rig(wl.ring_rig())
+    P, F = wl.frames(rig, channels, 1, "peaked", seed=channels)
+    w = wl.Workload("c", rig, channels, 1, "f32", P, F)
+    cop, _, cs = oracle_plans("nuscenes_tilted")
+    ref = oracle_lib.pool(rig, cop, P, F)
+    plan = pkg.Plan.from_rig(rig)
+    _check_fp32(_run(torch_cuda, pkg, plan, w), ref, np.diff(cs))
+
+
+def test_count_test_on_gpu(torch_cuda, pkg, oracle_plans):
+    """P = 1, F = 1, C = 1: each cell holds its point count exactly."""
+    torch = torch_cuda
+    rig = wl.ring_rig()
+    _, _, cs = oracle_plans("nuscenes")
+    plan = pkg.Plan.from_rig(rig)
+    P = torch.ones((1, rig.n_cams, rig.n_depth, rig.feat_h, rig.feat_w), device="cuda")
+    F = torch.ones((1, rig.n_cams, rig.feat_h, rig.feat_w, 1), device="cuda")
+    out = plan.forward(P, F).cpu().numpy().reshape(-1)
+    assert np.array_equal(out, np.diff(cs).astype(np.float32))
+
+
+def test_unaligned_inputs_take_the_scalar_path(torch_cuda, pkg, oracle_lib, oracle_plans):
+    torch = torch_cuda
+    w = wl.make("nuscenes", seed=3)
+    cop, _, cs = oracle_plans("nuscenes")
+    ref = oracle_lib.pool(w.rig, cop, w.P, w.F)
+    plan = pkg.Plan.from_rig(w.rig)
+    P = _to_device(torch, w.P, "f32")
+    flat = torch.empty(w.F.size + 1, device="cuda")
+    flat[1:] = torch.from_numpy(w.F.reshape(-1)).cuda()
+    F = flat[1:].view(w.F.shape)                  # 4-byte aligned only
+    out = plan.forward(P, F)
+    torch.cuda.synchronize()
+    _check_fp32(out.cpu().numpy(), ref, np.diff(cs))
+
+
+def test_deterministic(torch_cuda, pkg):
+    torch = torch_cuda
+    w = wl.make("nuscenes_tilted", seed=6)
+    plan = pkg.Plan.from_rig(w.rig)
+    P = _to_device(torch, w.P, "f32")
+    F = _to_device(torch, w.F, "f32")
+    a = plan.forward(P, F).cpu().numpy()
+    b = plan.forward(P, F).cpu().numpy()
+    assert np.array_equal(a, b)
+
+
+def test_plan_reuse_and_shape_checks(torch_cuda, pkg):
+    torch = torch_cuda
+    rig = wl.tiny_rig()
+    plan = pkg.Plan.from_rig(rig)
+    P = torch.zeros((1, 1, 8, 4, 8), device="cuda")
+    F = torch.zeros((1, 1, 4, 8, 8), device="cuda")
+    with pytest.raises(pkg.BevpoolError):
+        plan.forward(P[:, :, :7].contiguous(), F)
+    with pytest.raises(pkg.BevpoolError):
+        plan.forward(P, F.to(torch.float16))
+    assert (plan.forward(P, F) == 0).all()
