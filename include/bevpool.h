@@ -153,6 +153,7 @@ typedef struct {
     int32_t max_per_cell; /* largest interval */
     int32_t n_tiles;      /* work items of bevpool_forward (one workgroup each) */
     int32_t n_cams, n_depth, feat_h, feat_w, nx, ny;
+    int32_t n_rows;       /* feature rows staged per frame, summed over tiles */
 } bevpool_plan_info;
 
 /* Fill *info. Host only, no device work. Errors: INVALID_ARG. */

@@ -52,6 +52,7 @@ class bevpool_plan_info(ctypes.Structure):
         ("n_cams", ctypes.c_int32), ("n_depth", ctypes.c_int32),
         ("feat_h", ctypes.c_int32), ("feat_w", ctypes.c_int32),
         ("nx", ctypes.c_int32), ("ny", ctypes.c_int32),
+        ("n_rows", ctypes.c_int32),
     ]
 
 

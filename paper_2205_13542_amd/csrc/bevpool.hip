@@ -30,7 +30,17 @@ void free_plan(bevpool_plan_s *plan) {
     (void)hipFree(plan->cell_of_point);
     (void)hipFree(plan->sorted_point);
     (void)hipFree(plan->cell_start);
-    (void)hipFree(plan->tile_cell);
+    (void)hipFree(plan->tile_cell_begin);
+    (void)hipFree(plan->tile_row_begin);
+    (void)hipFree(plan->tile_cells);
+    (void)hipFree(plan->comp_cell_start);
+    (void)hipFree(plan->comp_point);
+    (void)hipFree(plan->comp_row);
+    (void)hipFree(plan->row_pix);
+    (void)hipFree(plan->empty_cells);
+    (void)hipFree(plan->tile_hdr);
+    (void)hipFree(plan->heavy_tiles);
+    (void)hipFree(plan->group_tile_begin);
     if (prev >= 0 && prev != plan->device) (void)hipSetDevice(prev);
     plan->magic = 0;
     delete plan;
@@ -138,6 +148,7 @@ int bevpool_plan_info_get(const bevpool_plan_t *plan, bevpool_plan_info *info) {
     info->feat_w = plan->geom.feat_w;
     info->nx = plan->geom.nx;
     info->ny = plan->geom.ny;
+    info->n_rows = plan->n_rows;
     return BEVPOOL_OK;
 }
 

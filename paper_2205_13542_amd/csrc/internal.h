@@ -8,23 +8,38 @@
 
 namespace bevpool {
 
-// Work partition of the forward pass. The cells are cut into tiles of
-// consecutive cell ids, one workgroup per tile. A tile's "path length" is
-// kCellWeight * cells + points. A new tile starts whenever that length
-// crosses a multiple of kTilePath. A cell with more than kHeavyPoints points
-// gets a tile of its own. A multi-cell tile therefore holds fewer than
-// kTilePath + kHeavyPoints points, all staged in LDS at once. Heavier
-// single-cell tiles are staged in rounds of kStagePoints.
+// Work partition of the forward pass.
+//
+// Cells with points are grouped into tiles along the camera rays. A cell's
+// key is (camera, feature column / kKeyCols, depth bin / kKeyBins) of its
+// lowest-id point. Cells with one key lie along a short bundle of
+// neighbouring rays, so their points share few distinct feature rows; each
+// row is reused about once per depth bin the bundle spends in the tile. A
+// key group becomes one tile, unless it has more than kPointBudget points or
+// kMaxTileCells cells. Then it is cut where its running point count crosses
+// a multiple of kPointBudget / 2, around every cell with more than
+// kPointBudget / 2 points, and every kMaxTileCells cells. So a tile holds
+// at most kPointBudget points, except a tile that is one heavier cell.
+// One workgroup serves each tile. It stages the tile's distinct feature
+// rows in LDS once, and every point reads its row from there.
+//
+// The forward kernel runs kPersistentGroups workgroups of kPersistentWaves
+// waves, one per CU. Each owns a contiguous run of tiles of about equal cost
+// and a share of the cells without points, which it zeroes. A tile heavier
+// than kPointBudget (one cell) gets an extra workgroup of its own.
 constexpr int kWaveSize = 64;
-constexpr int kWaves = 4;
+constexpr int kWaves = 4;                                  // plan kernels, heavy tiles
 constexpr int kBlock = kWaves * kWaveSize;
-constexpr int kTilePath = 1024;
-constexpr int kCellWeight = 1;
-constexpr int kHeavyPoints = 512;
-constexpr int kStagePoints = kTilePath + kHeavyPoints;        // 1536
-constexpr int kMaxTileCells = kTilePath / kCellWeight + 1;    // 1025
-constexpr int kStagePerThread = kStagePoints / kBlock;        // 6
-static_assert(kStagePoints % kBlock == 0, "staging loop assumes whole rounds");
+constexpr int kPersistentGroups = 256;
+constexpr int kPersistentWaves = 8;
+constexpr int kPersistentBlock = kPersistentWaves * kWaveSize;
+constexpr int kKeyCols = 4;
+constexpr int kKeyBins = 8;
+constexpr int kPointBudget = 2048;
+constexpr int kMaxTileCells = 256;
+constexpr int kStagePerThread = kPointBudget / kBlock;     // 8
+constexpr int kFeatureLdsBytes = 56 * 1024;                // staged feature slab
+static_assert(kPointBudget % kBlock == 0, "staging loop assumes whole rounds");
 
 // Unsigned division by a run-time constant through a multiply-high, after
 // Granlund and Montgomery, "Division by invariant integers using
@@ -53,11 +68,23 @@ struct bevpool_plan_s {
     int device;
     bevpool_geometry geom;
     int64_t n_points, n_kept;
-    int32_t n_cells, n_nonempty, max_per_cell, n_tiles;
+    int32_t n_cells, n_nonempty, max_per_cell, n_tiles, n_rows, n_empty, n_heavy;
+    // canonical association (exported)
     int32_t *cell_of_point;  // [n_points]
     int32_t *sorted_point;   // [n_points]: kept ids by (cell, id), then dropped ids
     int32_t *cell_start;     // [n_cells + 1]
-    int32_t *tile_cell;      // [n_tiles + 1]
+    // forward work partition, all in tile order
+    int32_t *tile_cell_begin;  // [n_tiles + 1] into tile_cells / comp_cell_start
+    int32_t *tile_row_begin;   // [n_tiles + 1] into row_pix
+    int32_t *tile_cells;       // [n_nonempty] cells with points, tile by tile, id order inside
+    int32_t *comp_cell_start;  // [n_nonempty + 1] first point (in comp order) of each listed cell
+    int32_t *empty_cells;      // [n_empty] cells without points, in id order
+    int32_t *tile_hdr;         // [n_tiles][8]: cell begin, cells, point begin, points, row begin, rows
+    int32_t *heavy_tiles;      // [n_heavy] tiles with more than kPointBudget points
+    int32_t *group_tile_begin; // [kPersistentGroups + 1] tile run of each persistent workgroup
+    int32_t *comp_point;       // [n_kept] point ids, tile by tile, cell by cell, id order
+    int32_t *comp_row;         // [n_kept] the point's feature row, relative to its tile
+    int32_t *row_pix;          // [n_rows] pixel (n*H*W + h*W + w) of each staged row
 };
 
 constexpr uint32_t kPlanMagic = 0xB3F9001Du;

@@ -10,7 +10,7 @@
 //   k_radix_scatter}
 //   k_cell_start   interval table from the sorted keys
 //   k_cell_stats   non-empty cells and the largest interval
-//   k_tile_flags / k_scan / k_tile_emit   work partition of the forward pass
+//   k_cell_keys ... k_rows   ray-aligned work partition of the forward pass
 //
 // The geometry is evaluated in IEEE double with the file built without
 // floating-point contraction, in one fixed expression order, so the cell ids
@@ -253,28 +253,225 @@ __global__ __launch_bounds__(kBlock) void k_cell_stats(const int32_t *cell_start
 }
 
 // ---------------------------------------------------------------- work partition
+//
+// Ray-aligned tiles (see the constants in internal.h). Rows: a point starts
+// a new staged row of its tile when the previous depth bin of its pixel is
+// dropped or lies in another tile. Every later point of the same run reads
+// that row. If a ray leaves a tile and comes back, the pixel is staged twice;
+// that wastes one LDS row and changes nothing else.
 
-__device__ __forceinline__ bool tile_starts_at(const int32_t *cs, int32_t c) {
-    if (c == 0) return true;
-    const int64_t here = int64_t(kCellWeight) * c + cs[c];
-    const int64_t prev = int64_t(kCellWeight) * (c - 1) + cs[c - 1];
-    const int32_t n_here = cs[c + 1] - cs[c];
-    const int32_t n_prev = cs[c] - cs[c - 1];
-    return (here / kTilePath != prev / kTilePath) || n_here > kHeavyPoints || n_prev > kHeavyPoints;
+struct KeyArgs {
+    const int32_t *cell_start, *sorted_point;
+    int32_t n_cells, HW, W, D, key_cols, key_bins;
+    uint32_t *key;            // [n_cells]
+    int32_t *nonempty_flag;   // [n_cells + 1]
+    int32_t *empty_flag;      // [n_cells + 1]
+};
+
+__global__ __launch_bounds__(kBlock) void k_cell_keys(KeyArgs a) {
+    const int32_t c = blockIdx.x * kBlock + threadIdx.x;
+    if (c >= a.n_cells) return;
+    const int32_t cnt = a.cell_start[c + 1] - a.cell_start[c];
+    a.nonempty_flag[c] = cnt > 0 ? 1 : 0;
+    a.empty_flag[c] = cnt > 0 ? 0 : 1;
+    if (cnt == 0) return;
+    const int32_t p0 = a.sorted_point[a.cell_start[c]];  // the cell's lowest point id
+    const int32_t q = p0 / a.HW;                          // n * D + d
+    const int32_t n = q / a.D, d = q - n * a.D;
+    const int32_t w = p0 % a.W;
+    a.key[c] = uint32_t((n * a.key_cols + w / kKeyCols) * a.key_bins + d / kKeyBins);
 }
 
-__global__ __launch_bounds__(kBlock) void k_tile_flags(const int32_t *cs, int32_t n_cells,
-                                                       int32_t *flags) {
+__global__ __launch_bounds__(kBlock) void k_compact_cells(const int32_t *cell_start, int32_t n_cells,
+                                                          const uint32_t *key,
+                                                          const int32_t *nonempty_pos,
+                                                          const int32_t *empty_pos,
+                                                          uint32_t *ne_key, int32_t *ne_cell,
+                                                          int32_t *empty_cells) {
     const int32_t c = blockIdx.x * kBlock + threadIdx.x;
-    if (c < n_cells) flags[c] = tile_starts_at(cs, c) ? 1 : 0;
+    if (c >= n_cells) return;
+    if (cell_start[c + 1] > cell_start[c]) {
+        ne_key[nonempty_pos[c]] = key[c];
+        ne_cell[nonempty_pos[c]] = c;
+    } else {
+        empty_cells[empty_pos[c]] = c;
+    }
 }
 
-__global__ __launch_bounds__(kBlock) void k_tile_emit(const int32_t *cs, int32_t n_cells,
-                                                      const int32_t *slot, const int32_t *n_tiles,
-                                                      int32_t *tile_cell) {
-    const int32_t c = blockIdx.x * kBlock + threadIdx.x;
-    if (c < n_cells && tile_starts_at(cs, c)) tile_cell[slot[c]] = c;
-    if (c == 0) tile_cell[*n_tiles] = n_cells;
+// point count of each listed cell, and each cell's position in tile order
+__global__ __launch_bounds__(kBlock) void k_listed_counts(const int32_t *listed_cell, int32_t n,
+                                                          const int32_t *cell_start,
+                                                          int32_t *count_at, int32_t *pos_of_cell) {
+    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+    if (i >= n) return;
+    const int32_t c = listed_cell[i];
+    count_at[i] = cell_start[c + 1] - cell_start[c];
+    pos_of_cell[c] = i;
+}
+
+__global__ __launch_bounds__(kBlock) void k_group_flags(const uint32_t *key, int32_t n,
+                                                        int32_t *flag) {
+    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+    if (i < n) flag[i] = (i == 0 || key[i] != key[i - 1]) ? 1 : 0;
+}
+
+// first listed position of each group (scan = exclusive scan of the flags)
+__global__ __launch_bounds__(kBlock) void k_group_first(const int32_t *scan, int32_t n,
+                                                        int32_t *group_first) {
+    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+    if (i > n) return;
+    if (i == n) group_first[scan[n]] = n;
+    else if (scan[i + 1] != scan[i]) group_first[scan[i]] = i;
+}
+
+struct TileFlagArgs {
+    const int32_t *group_scan, *group_first, *X;  // X: exclusive scan of the counts
+    int32_t n;
+    int32_t *flag;
+};
+
+__global__ __launch_bounds__(kBlock) void k_tile_flags(TileFlagArgs a) {
+    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+    if (i >= a.n) return;
+    const int32_t g = a.group_scan[i + 1] - 1;
+    const int32_t gf = a.group_first[g];
+    const int32_t total = a.X[a.group_first[g + 1]] - a.X[gf];
+    constexpr int32_t S = kPointBudget / 2;
+    bool start = (i == gf) || ((i - gf) % kMaxTileCells == 0);
+    if (!start && total > kPointBudget) {
+        const int32_t here = a.X[i] - a.X[gf], prev = a.X[i - 1] - a.X[gf];
+        const int32_t n_here = a.X[i + 1] - a.X[i], n_prev = a.X[i] - a.X[i - 1];
+        start = (here / S != prev / S) || n_here > S || n_prev > S;
+    }
+    a.flag[i] = start ? 1 : 0;
+}
+
+// tile_cell_begin[t] = first listed position of tile t; tile_of_cell per cell
+__global__ __launch_bounds__(kBlock) void k_tile_emit(const int32_t *tile_scan, int32_t n,
+                                                      const int32_t *listed_cell,
+                                                      int32_t *tile_cell_begin,
+                                                      int32_t *tile_of_cell) {
+    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+    if (i > n) return;
+    if (i == n) {
+        tile_cell_begin[tile_scan[n]] = n;
+        return;
+    }
+    if (tile_scan[i + 1] != tile_scan[i]) tile_cell_begin[tile_scan[i]] = i;
+    tile_of_cell[listed_cell[i]] = tile_scan[i + 1] - 1;
+}
+
+// Points in tile order: a cell's run of the canonical order moves as a block.
+__global__ __launch_bounds__(kBlock) void k_comp_points(const int32_t *sorted_point, int32_t n_kept,
+                                                        const int32_t *cell_of_point,
+                                                        const int32_t *cell_start,
+                                                        const int32_t *pos_of_cell,
+                                                        const int32_t *comp_cell_start,
+                                                        int32_t *comp_point, int32_t *pos_of_point) {
+    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+    if (i >= n_kept) return;
+    const int32_t p = sorted_point[i];
+    const int32_t c = cell_of_point[p];
+    const int32_t ci = comp_cell_start[pos_of_cell[c]] + (i - cell_start[c]);
+    comp_point[ci] = p;
+    pos_of_point[p] = ci;
+}
+
+// 1 where a point starts a run of its pixel inside its tile
+__global__ __launch_bounds__(kBlock) void k_run_flags(const int32_t *comp_point, int32_t n_kept,
+                                                      const int32_t *cell_of_point,
+                                                      const int32_t *tile_of_cell, int32_t HW,
+                                                      FastDiv div_hw, FastDiv div_d, int32_t D,
+                                                      int32_t *flag) {
+    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+    if (i >= n_kept) return;
+    const int32_t p = comp_point[i];
+    const uint32_t q = fdiv(uint32_t(p), div_hw);
+    const int32_t d = int32_t(q) - int32_t(fdiv(q, div_d)) * D;
+    const int32_t prev = d > 0 ? cell_of_point[p - HW] : -1;
+    flag[i] = (prev < 0 || tile_of_cell[prev] != tile_of_cell[cell_of_point[p]]) ? 1 : 0;
+}
+
+__global__ __launch_bounds__(kBlock) void k_tile_row_begin(const int32_t *tile_cell_begin,
+                                                           const int32_t *comp_cell_start,
+                                                           const int32_t *row_scan, int32_t n_tiles,
+                                                           int32_t *tile_row_begin) {
+    const int32_t t = blockIdx.x * kBlock + threadIdx.x;
+    if (t <= n_tiles) tile_row_begin[t] = row_scan[comp_cell_start[tile_cell_begin[t]]];
+}
+
+// One thread per pixel walks its depth bins in order, names the staged row
+// of each run and gives every point its row relative to its tile.
+__global__ __launch_bounds__(kBlock) void k_rows(const int32_t *cell_of_point,
+                                                 const int32_t *pos_of_point,
+                                                 const int32_t *tile_of_cell,
+                                                 const int32_t *row_scan,
+                                                 const int32_t *tile_row_begin, int32_t n_pix,
+                                                 int32_t HW, int32_t D, int32_t *row_pix,
+                                                 int32_t *comp_row) {
+    const int32_t pixel = blockIdx.x * kBlock + threadIdx.x;
+    if (pixel >= n_pix) return;
+    const int32_t n = pixel / HW, hw = pixel - n * HW;
+    int32_t row = 0;
+    for (int32_t d = 0; d < D; ++d) {
+        const int32_t p = (n * D + d) * HW + hw;
+        const int32_t c = cell_of_point[p];
+        if (c < 0) continue;
+        const int32_t i = pos_of_point[p];
+        if (row_scan[i + 1] != row_scan[i]) {
+            row = row_scan[i];
+            row_pix[row] = pixel;
+        }
+        comp_row[i] = row - tile_row_begin[tile_of_cell[c]];
+    }
+}
+
+// Per-tile header, heavy flag and cost (for splitting tiles over the
+// persistent workgroups): points, plus rows and cells, which also cost time.
+__global__ __launch_bounds__(kBlock) void k_tile_headers(const int32_t *tile_cell_begin,
+                                                         const int32_t *tile_row_begin,
+                                                         const int32_t *comp_cell_start,
+                                                         int32_t n_tiles, int32_t *hdr,
+                                                         int32_t *heavy_flag, int32_t *cost) {
+    const int32_t t = blockIdx.x * kBlock + threadIdx.x;
+    if (t >= n_tiles) return;
+    const int32_t tcb = tile_cell_begin[t], ncell = tile_cell_begin[t + 1] - tcb;
+    const int32_t tpb = comp_cell_start[tcb], npts = comp_cell_start[tcb + ncell] - tpb;
+    const int32_t trb = tile_row_begin[t], nrows = tile_row_begin[t + 1] - trb;
+    int32_t *h = hdr + 8 * int64_t(t);
+    h[0] = tcb;
+    h[1] = ncell;
+    h[2] = tpb;
+    h[3] = npts;
+    h[4] = trb;
+    h[5] = nrows;
+    h[6] = 0;
+    h[7] = 0;
+    const bool heavy = npts > kPointBudget;
+    heavy_flag[t] = heavy ? 1 : 0;
+    cost[t] = heavy ? 0 : npts + 2 * nrows + 4 * ncell + 64;
+}
+
+__global__ __launch_bounds__(kBlock) void k_heavy_list(const int32_t *heavy_scan, int32_t n_tiles,
+                                                       int32_t *heavy_tiles) {
+    const int32_t t = blockIdx.x * kBlock + threadIdx.x;
+    if (t < n_tiles && heavy_scan[t + 1] != heavy_scan[t]) heavy_tiles[heavy_scan[t]] = t;
+}
+
+// group_tile_begin[w] = first tile whose running cost reaches w/G of the total
+__global__ __launch_bounds__(kBlock) void k_group_ranges(const int32_t *cost_scan, int32_t n_tiles,
+                                                         int32_t *group_tile_begin) {
+    const int32_t w = blockIdx.x * kBlock + threadIdx.x;
+    if (w > kPersistentGroups) return;
+    const int64_t total = cost_scan[n_tiles];
+    const int64_t target = total * w / kPersistentGroups;
+    int32_t lo = 0, hi = n_tiles;  // first t with cost_scan[t] >= target
+    while (lo < hi) {
+        const int32_t mid = (lo + hi) >> 1;
+        if (cost_scan[mid] < target) lo = mid + 1;
+        else hi = mid;
+    }
+    group_tile_begin[w] = (w == kPersistentGroups) ? n_tiles : lo;
 }
 
 int blocks_for(int64_t n) { return int((n + kBlock - 1) / kBlock); }
@@ -292,6 +489,12 @@ int dev_alloc(T **p, size_t count, const char *what) {
     return BEVPOOL_OK;
 }
 
+// Exclusive scan of data[0..n] in place; data[n] must be 0 on entry and
+// holds the total afterwards.
+void scan_with_total(int32_t *data, int64_t n, int32_t *scratch_total, hipStream_t stream) {
+    hipLaunchKernelGGL(k_scan, dim3(1), dim3(kScanBlock), 0, stream, data, n + 1, scratch_total);
+}
+
 }  // namespace
 }  // namespace bevpool
 
@@ -302,6 +505,8 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
     const int64_t np64 = int64_t(g.n_cams) * g.n_depth * g.feat_h * g.feat_w;
     const int32_t np = int32_t(np64);
     const int32_t n_cells = g.nx * g.ny;
+    const int32_t HW = g.feat_h * g.feat_w;
+    const int32_t n_pix = g.n_cams * HW;
     plan->n_points = np64;
     plan->n_cells = n_cells;
 
@@ -309,34 +514,82 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
     if ((rc = dev_alloc(&plan->cell_of_point, size_t(np), "cell_of_point"))) return rc;
     if ((rc = dev_alloc(&plan->sorted_point, size_t(np), "sorted_point"))) return rc;
     if ((rc = dev_alloc(&plan->cell_start, size_t(n_cells) + 1, "cell_start"))) return rc;
-    if ((rc = dev_alloc(&plan->tile_cell, size_t(n_cells) + 1, "tile_cell"))) return rc;
 
     // temporaries, freed on every exit path below
-    const int sort_tiles = int((np64 + kSortTile - 1) / kSortTile);
-    int bits = 1;
-    while ((int64_t(1) << bits) <= int64_t(n_cells)) ++bits;  // keys are 0..n_cells
-    const int passes = (bits + 7) / 8;
+    const int64_t sort_cap = np64 > n_cells ? np64 : int64_t(n_cells);
+    const int sort_tiles_cap = int((sort_cap + kSortTile - 1) / kSortTile);
     double *d_calib = nullptr;
-    uint32_t *keys_a = nullptr, *keys_b = nullptr;
-    int32_t *vals_b = nullptr, *hist = nullptr, *small = nullptr, *flags = nullptr;
+    uint32_t *keys_a = nullptr, *keys_b = nullptr, *cell_key = nullptr;
+    int32_t *vals_b = nullptr, *hist = nullptr, *small = nullptr;
+    int32_t *flag_a = nullptr, *flag_b = nullptr, *group_first = nullptr;
+    int32_t *tile_of_cell = nullptr, *pos_of_cell = nullptr, *pos_of_point = nullptr;
+    int32_t *row_scan = nullptr;
     auto cleanup = [&]() {
         (void)hipFree(d_calib);
         (void)hipFree(keys_a);
         (void)hipFree(keys_b);
+        (void)hipFree(cell_key);
         (void)hipFree(vals_b);
         (void)hipFree(hist);
         (void)hipFree(small);
-        (void)hipFree(flags);
+        (void)hipFree(flag_a);
+        (void)hipFree(flag_b);
+        (void)hipFree(group_first);
+        (void)hipFree(tile_of_cell);
+        (void)hipFree(pos_of_cell);
+        (void)hipFree(pos_of_point);
+        (void)hipFree(row_scan);
     };
+    auto launch_ok = [](int64_t n) { return n > 0; };
+
+    // stable LSD radix sort of (keys, vals)[0, n) on the low `bits` bits; the
+    // result ends in (keys, vals)
+    auto radix_sort = [&](uint32_t *keys, int32_t *vals, int32_t n, int bits) -> int {
+        if (n <= 0) return BEVPOOL_OK;
+        const int tiles = int((int64_t(n) + kSortTile - 1) / kSortTile);
+        const int passes = (bits + 7) / 8;
+        uint32_t *kin = keys, *kout = keys == keys_a ? keys_b : keys_a;
+        int32_t *vin = vals, *vout = vals_b;
+        for (int pass = 0; pass < passes; ++pass) {
+            const int shift = 8 * pass;
+            hipLaunchKernelGGL(k_radix_hist, dim3(tiles), dim3(kBlock), 0, stream, kin, n, shift, hist);
+            hipLaunchKernelGGL(k_scan, dim3(1), dim3(kScanBlock), 0, stream, hist,
+                               int64_t(tiles) * 256, small + 3);
+            hipLaunchKernelGGL(k_radix_scatter, dim3(tiles), dim3(kBlock), 0, stream, kin, vin, n,
+                               shift, hist, kout, vout);
+            BEVPOOL_HIP(hipGetLastError());
+            std::swap(kin, kout);
+            std::swap(vin, vout);
+        }
+        if (kin != keys)
+            BEVPOOL_HIP(hipMemcpyAsync(keys, kin, sizeof(uint32_t) * size_t(n),
+                                       hipMemcpyDeviceToDevice, stream));
+        if (vin != vals)
+            BEVPOOL_HIP(hipMemcpyAsync(vals, vin, sizeof(int32_t) * size_t(n),
+                                       hipMemcpyDeviceToDevice, stream));
+        return BEVPOOL_OK;
+    };
+    auto bits_for = [](int64_t max_key) {
+        int b = 1;
+        while ((int64_t(1) << b) <= max_key) ++b;
+        return b;
+    };
+
     auto run = [&]() -> int {
         int rc2;
         if ((rc2 = dev_alloc(&d_calib, size_t(g.n_cams) * 16, "calibration"))) return rc2;
-        if ((rc2 = dev_alloc(&keys_a, size_t(np), "sort keys"))) return rc2;
-        if ((rc2 = dev_alloc(&keys_b, size_t(np), "sort keys"))) return rc2;
-        if ((rc2 = dev_alloc(&vals_b, size_t(np), "sort values"))) return rc2;
-        if ((rc2 = dev_alloc(&hist, size_t(sort_tiles) * 256, "radix histogram"))) return rc2;
+        if ((rc2 = dev_alloc(&keys_a, size_t(sort_cap), "sort keys"))) return rc2;
+        if ((rc2 = dev_alloc(&keys_b, size_t(sort_cap), "sort keys"))) return rc2;
+        if ((rc2 = dev_alloc(&vals_b, size_t(sort_cap), "sort values"))) return rc2;
+        if ((rc2 = dev_alloc(&cell_key, size_t(n_cells), "cell keys"))) return rc2;
+        if ((rc2 = dev_alloc(&hist, size_t(sort_tiles_cap) * 256, "radix histogram"))) return rc2;
         if ((rc2 = dev_alloc(&small, 4, "plan counters"))) return rc2;
-        if ((rc2 = dev_alloc(&flags, size_t(n_cells) + 1, "tile flags"))) return rc2;
+        if ((rc2 = dev_alloc(&flag_a, size_t(n_cells) + 1, "flags"))) return rc2;
+        if ((rc2 = dev_alloc(&flag_b, size_t(n_cells) + 1, "flags"))) return rc2;
+        if ((rc2 = dev_alloc(&group_first, size_t(n_cells) + 1, "group starts"))) return rc2;
+        if ((rc2 = dev_alloc(&tile_of_cell, size_t(n_cells), "tile of cell"))) return rc2;
+        if ((rc2 = dev_alloc(&pos_of_cell, size_t(n_cells), "cell positions"))) return rc2;
+        if ((rc2 = dev_alloc(&pos_of_point, size_t(np), "point positions"))) return rc2;
 
         BEVPOOL_HIP(hipMemcpyAsync(d_calib, intrinsics, sizeof(double) * 4 * g.n_cams,
                                    hipMemcpyHostToDevice, stream));
@@ -359,48 +612,156 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         hipLaunchKernelGGL(k_project, dim3(blocks_for(np)), dim3(kBlock), 0, stream, pa);
         BEVPOOL_HIP(hipGetLastError());
 
-        // LSD radix sort; buffers alternate so the last pass lands in
-        // plan->sorted_point (values) whatever the number of passes
-        uint32_t *kin = keys_a, *kout = keys_b;
-        int32_t *vin = plan->sorted_point, *vout = vals_b;
-        for (int pass = 0; pass < passes; ++pass) {
-            const int shift = 8 * pass;
-            hipLaunchKernelGGL(k_radix_hist, dim3(sort_tiles), dim3(kBlock), 0, stream, kin, np,
-                               shift, hist);
-            hipLaunchKernelGGL(k_scan, dim3(1), dim3(kScanBlock), 0, stream, hist,
-                               int64_t(sort_tiles) * 256, small + 3);
-            hipLaunchKernelGGL(k_radix_scatter, dim3(sort_tiles), dim3(kBlock), 0, stream, kin,
-                               vin, np, shift, hist, kout, vout);
-            BEVPOOL_HIP(hipGetLastError());
-            std::swap(kin, kout);
-            std::swap(vin, vout);
-        }
-        if (vin != plan->sorted_point)
-            BEVPOOL_HIP(hipMemcpyAsync(plan->sorted_point, vin, sizeof(int32_t) * size_t(np),
-                                       hipMemcpyDeviceToDevice, stream));
-
+        // canonical order: points by (cell, id); dropped points last
+        if ((rc2 = radix_sort(keys_a, plan->sorted_point, np, bits_for(n_cells)))) return rc2;
         hipLaunchKernelGGL(k_cell_start, dim3(blocks_for(int64_t(np) + 1)), dim3(kBlock), 0,
-                           stream, kin, np, n_cells, plan->cell_start);
+                           stream, keys_a, np, n_cells, plan->cell_start);
         hipLaunchKernelGGL(k_cell_stats, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream,
                            plan->cell_start, n_cells, small);
-        hipLaunchKernelGGL(k_tile_flags, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream,
-                           plan->cell_start, n_cells, flags);
-        hipLaunchKernelGGL(k_scan, dim3(1), dim3(kScanBlock), 0, stream, flags, int64_t(n_cells),
-                           small + 2);
-        hipLaunchKernelGGL(k_tile_emit, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream,
-                           plan->cell_start, n_cells, flags, small + 2, plan->tile_cell);
-        BEVPOOL_HIP(hipGetLastError());
 
-        int32_t stats[4];
+        // cells with points, keyed along the rays; cells without points listed
+        const int32_t key_cols = (g.feat_w + kKeyCols - 1) / kKeyCols;
+        const int32_t key_bins = (g.n_depth + kKeyBins - 1) / kKeyBins;
+        KeyArgs ka;
+        ka.cell_start = plan->cell_start;
+        ka.sorted_point = plan->sorted_point;
+        ka.n_cells = n_cells;
+        ka.HW = HW;
+        ka.W = g.feat_w;
+        ka.D = g.n_depth;
+        ka.key_cols = key_cols;
+        ka.key_bins = key_bins;
+        ka.key = cell_key;
+        ka.nonempty_flag = flag_a;
+        ka.empty_flag = flag_b;
+        BEVPOOL_HIP(hipMemsetAsync(flag_a, 0, sizeof(int32_t) * (size_t(n_cells) + 1), stream));
+        BEVPOOL_HIP(hipMemsetAsync(flag_b, 0, sizeof(int32_t) * (size_t(n_cells) + 1), stream));
+        hipLaunchKernelGGL(k_cell_keys, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream, ka);
+        scan_with_total(flag_a, n_cells, small + 3, stream);
+        scan_with_total(flag_b, n_cells, small + 3, stream);
+        BEVPOOL_HIP(hipGetLastError());
+        int32_t host[2], counts2[2];
+        BEVPOOL_HIP(hipMemcpyAsync(host, small, sizeof(host), hipMemcpyDeviceToHost, stream));
+        BEVPOOL_HIP(hipMemcpyAsync(&counts2[0], flag_a + n_cells, sizeof(int32_t),
+                                   hipMemcpyDeviceToHost, stream));
+        BEVPOOL_HIP(hipMemcpyAsync(&counts2[1], flag_b + n_cells, sizeof(int32_t),
+                                   hipMemcpyDeviceToHost, stream));
         int32_t kept;
-        BEVPOOL_HIP(hipMemcpyAsync(stats, small, sizeof(stats), hipMemcpyDeviceToHost, stream));
         BEVPOOL_HIP(hipMemcpyAsync(&kept, plan->cell_start + n_cells, sizeof(kept),
                                    hipMemcpyDeviceToHost, stream));
         BEVPOOL_HIP(hipStreamSynchronize(stream));
-        plan->n_nonempty = stats[0];
-        plan->max_per_cell = stats[1];
-        plan->n_tiles = stats[2];
+        plan->n_nonempty = host[0];
+        plan->max_per_cell = host[1];
         plan->n_kept = kept;
+        const int32_t n_ne = counts2[0];
+        plan->n_empty = counts2[1];
+
+        if ((rc2 = dev_alloc(&plan->tile_cells, size_t(n_ne), "tile_cells"))) return rc2;
+        if ((rc2 = dev_alloc(&plan->comp_cell_start, size_t(n_ne) + 1, "comp_cell_start"))) return rc2;
+        if ((rc2 = dev_alloc(&plan->empty_cells, size_t(plan->n_empty), "empty_cells"))) return rc2;
+        // compact into (key, cell) pairs in keys_b / vals_b's partner buffers
+        uint32_t *ne_key = keys_a;     // free again after k_cell_start
+        int32_t *ne_cell = plan->tile_cells;
+        hipLaunchKernelGGL(k_compact_cells, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream,
+                           plan->cell_start, n_cells, cell_key, flag_a, flag_b, ne_key, ne_cell,
+                           plan->empty_cells);
+        BEVPOOL_HIP(hipGetLastError());
+        const int64_t max_key = int64_t(g.n_cams) * key_cols * key_bins;
+        if ((rc2 = radix_sort(ne_key, ne_cell, n_ne, bits_for(max_key)))) return rc2;
+
+        // point counts in tile order and their running sum
+        BEVPOOL_HIP(hipMemsetAsync(plan->comp_cell_start, 0, sizeof(int32_t) * (size_t(n_ne) + 1),
+                                   stream));
+        if (launch_ok(n_ne)) {
+            hipLaunchKernelGGL(k_listed_counts, dim3(blocks_for(n_ne)), dim3(kBlock), 0, stream,
+                               plan->tile_cells, n_ne, plan->cell_start, plan->comp_cell_start,
+                               pos_of_cell);
+        }
+        scan_with_total(plan->comp_cell_start, n_ne, small + 3, stream);
+
+        // key groups, then tiles
+        BEVPOOL_HIP(hipMemsetAsync(flag_a, 0, sizeof(int32_t) * (size_t(n_ne) + 1), stream));
+        BEVPOOL_HIP(hipMemsetAsync(flag_b, 0, sizeof(int32_t) * (size_t(n_ne) + 1), stream));
+        if (launch_ok(n_ne))
+            hipLaunchKernelGGL(k_group_flags, dim3(blocks_for(n_ne)), dim3(kBlock), 0, stream,
+                               ne_key, n_ne, flag_a);
+        scan_with_total(flag_a, n_ne, small + 3, stream);
+        hipLaunchKernelGGL(k_group_first, dim3(blocks_for(int64_t(n_ne) + 1)), dim3(kBlock), 0,
+                           stream, flag_a, n_ne, group_first);
+        TileFlagArgs ta;
+        ta.group_scan = flag_a;
+        ta.group_first = group_first;
+        ta.X = plan->comp_cell_start;
+        ta.n = n_ne;
+        ta.flag = flag_b;
+        if (launch_ok(n_ne))
+            hipLaunchKernelGGL(k_tile_flags, dim3(blocks_for(n_ne)), dim3(kBlock), 0, stream, ta);
+        scan_with_total(flag_b, n_ne, small + 3, stream);
+        BEVPOOL_HIP(hipGetLastError());
+        BEVPOOL_HIP(hipMemcpyAsync(&plan->n_tiles, flag_b + n_ne, sizeof(int32_t),
+                                   hipMemcpyDeviceToHost, stream));
+        BEVPOOL_HIP(hipStreamSynchronize(stream));
+        const int32_t n_tiles = plan->n_tiles;
+        if ((rc2 = dev_alloc(&plan->tile_cell_begin, size_t(n_tiles) + 1, "tile_cell_begin"))) return rc2;
+        if ((rc2 = dev_alloc(&plan->tile_row_begin, size_t(n_tiles) + 1, "tile_row_begin"))) return rc2;
+        hipLaunchKernelGGL(k_tile_emit, dim3(blocks_for(int64_t(n_ne) + 1)), dim3(kBlock), 0,
+                           stream, flag_b, n_ne, plan->tile_cells, plan->tile_cell_begin,
+                           tile_of_cell);
+        BEVPOOL_HIP(hipGetLastError());
+
+        // points in tile order, staged rows and each point's row
+        if ((rc2 = dev_alloc(&plan->comp_point, size_t(kept), "comp_point"))) return rc2;
+        if ((rc2 = dev_alloc(&plan->comp_row, size_t(kept), "comp_row"))) return rc2;
+        if ((rc2 = dev_alloc(&row_scan, size_t(kept) + 1, "row scan"))) return rc2;
+        BEVPOOL_HIP(hipMemsetAsync(row_scan, 0, sizeof(int32_t) * (size_t(kept) + 1), stream));
+        if (launch_ok(kept)) {
+            hipLaunchKernelGGL(k_comp_points, dim3(blocks_for(kept)), dim3(kBlock), 0, stream,
+                               plan->sorted_point, kept, plan->cell_of_point, plan->cell_start,
+                               pos_of_cell, plan->comp_cell_start, plan->comp_point, pos_of_point);
+            hipLaunchKernelGGL(k_run_flags, dim3(blocks_for(kept)), dim3(kBlock), 0, stream,
+                               plan->comp_point, kept, plan->cell_of_point, tile_of_cell, HW,
+                               make_fastdiv(uint32_t(HW)), make_fastdiv(uint32_t(g.n_depth)),
+                               g.n_depth, row_scan);
+        }
+        scan_with_total(row_scan, kept, small + 3, stream);
+        hipLaunchKernelGGL(k_tile_row_begin, dim3(blocks_for(int64_t(n_tiles) + 1)), dim3(kBlock), 0,
+                           stream, plan->tile_cell_begin, plan->comp_cell_start, row_scan, n_tiles,
+                           plan->tile_row_begin);
+        BEVPOOL_HIP(hipGetLastError());
+        int32_t n_rows;
+        BEVPOOL_HIP(hipMemcpyAsync(&n_rows, row_scan + kept, sizeof(n_rows), hipMemcpyDeviceToHost,
+                                   stream));
+        BEVPOOL_HIP(hipStreamSynchronize(stream));
+        plan->n_rows = n_rows;
+        if ((rc2 = dev_alloc(&plan->row_pix, size_t(n_rows), "row_pix"))) return rc2;
+        hipLaunchKernelGGL(k_rows, dim3(blocks_for(n_pix)), dim3(kBlock), 0, stream,
+                           plan->cell_of_point, pos_of_point, tile_of_cell, row_scan,
+                           plan->tile_row_begin, n_pix, HW, g.n_depth, plan->row_pix,
+                           plan->comp_row);
+        BEVPOOL_HIP(hipGetLastError());
+
+        // headers, heavy tiles and the persistent workgroups' tile runs
+        if ((rc2 = dev_alloc(&plan->tile_hdr, size_t(n_tiles) * 8, "tile_hdr"))) return rc2;
+        if ((rc2 = dev_alloc(&plan->group_tile_begin, size_t(kPersistentGroups) + 1, "tile runs"))) return rc2;
+        BEVPOOL_HIP(hipMemsetAsync(flag_a, 0, sizeof(int32_t) * (size_t(n_tiles) + 1), stream));
+        BEVPOOL_HIP(hipMemsetAsync(flag_b, 0, sizeof(int32_t) * (size_t(n_tiles) + 1), stream));
+        if (launch_ok(n_tiles))
+            hipLaunchKernelGGL(k_tile_headers, dim3(blocks_for(n_tiles)), dim3(kBlock), 0, stream,
+                               plan->tile_cell_begin, plan->tile_row_begin, plan->comp_cell_start,
+                               n_tiles, plan->tile_hdr, flag_a, flag_b);
+        scan_with_total(flag_a, n_tiles, small + 3, stream);
+        scan_with_total(flag_b, n_tiles, small + 3, stream);
+        hipLaunchKernelGGL(k_group_ranges, dim3(blocks_for(kPersistentGroups + 1)), dim3(kBlock), 0,
+                           stream, flag_b, n_tiles, plan->group_tile_begin);
+        BEVPOOL_HIP(hipMemcpyAsync(&plan->n_heavy, flag_a + n_tiles, sizeof(int32_t),
+                                   hipMemcpyDeviceToHost, stream));
+        BEVPOOL_HIP(hipStreamSynchronize(stream));
+        if ((rc2 = dev_alloc(&plan->heavy_tiles, size_t(plan->n_heavy), "heavy_tiles"))) return rc2;
+        if (launch_ok(n_tiles))
+            hipLaunchKernelGGL(k_heavy_list, dim3(blocks_for(n_tiles)), dim3(kBlock), 0, stream,
+                               flag_a, n_tiles, plan->heavy_tiles);
+        BEVPOOL_HIP(hipGetLastError());
+        BEVPOOL_HIP(hipStreamSynchronize(stream));
         return BEVPOOL_OK;
     };
     rc = run();
