@@ -58,7 +58,29 @@ def parse_args():
                     help="skip the oracle timing on the host cores")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU time budget of the oracle sample")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain device-to-device copy of 256 MiB five times (the "
+                         "reference kernel for scaling the FETCH_SIZE / WRITE_SIZE counters)")
     return ap.parse_args()
+
+
+COPY_BYTES = 256 << 20
+
+
+def copy_calibration():
+    """A plain copy of COPY_BYTES, five times. Under rocprofv3 --pmc its
+    FETCH_SIZE and WRITE_SIZE per dispatch give the counter's reading for a
+    known number of HBM bytes."""
+    import torch
+    dev = torch.device("cuda:0")
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration": True, "bytes_read": COPY_BYTES,
+                      "bytes_written": COPY_BYTES, "launches": 5}), flush=True)
 
 
 def algorithmic_bytes(w) -> int:
@@ -134,6 +156,9 @@ def main():
               "(the pooling shards by BEV tiles or frames without a collective; see the design "
               "notes)", file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
 
     import numpy as np
     import torch
