@@ -247,7 +247,8 @@ def main():
             "bev": [w.rig.ny, w.rig.nx],
             "points": info.n_points, "kept": info.n_kept,
             "nonempty_cells": info.n_nonempty, "max_per_cell": info.max_per_cell,
-            "tiles": info.n_tiles,
+            "column_cells": info.n_column, "generic_cells": info.n_generic,
+            "generic_runs": info.n_runs, "empty_cells": info.n_empty,
         },
         "roofline": {
             "bound": "hbm",
@@ -263,7 +264,8 @@ def main():
                        "p90": round(float(np.percentile(cold_ms, 90)) * 1e3, 2),
                        "warm_mean": round(warm_ms * 1e3, 2)},
         "algorithmic_bytes": nbytes,
-        "plan_bytes": 4 * (info.n_kept + info.n_cells + 1 + info.n_tiles + 1),
+        "plan_bytes_read": 8 * info.n_cams * info.n_depth * info.feat_w + 16 * info.n_generic
+                           + 16 * info.n_runs + 4 * info.n_empty,
         "plan_build_ms": round(plan_ms, 2),
         "wall_s_timed_loop": round(wall_s, 4),
         "kernel_sha256_16": kernel_hash(),

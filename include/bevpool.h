@@ -151,9 +151,11 @@ typedef struct {
     int32_t n_cells;      /* nx*ny */
     int32_t n_nonempty;   /* cells with at least one point */
     int32_t max_per_cell; /* largest interval */
-    int32_t n_tiles;      /* work items of bevpool_forward (one workgroup each) */
     int32_t n_cams, n_depth, feat_h, feat_w, nx, ny;
-    int32_t n_rows;       /* feature rows staged per frame, summed over tiles */
+    int32_t n_column;     /* cells fed by one (camera, depth bin, pixel column) */
+    int32_t n_generic;    /* other cells with points */
+    int32_t n_empty;      /* cells without points */
+    int32_t n_runs;       /* gather runs of the generic cells */
 } bevpool_plan_info;
 
 /* Fill *info. Host only, no device work. Errors: INVALID_ARG. */

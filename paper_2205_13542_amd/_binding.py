@@ -48,11 +48,12 @@ class bevpool_plan_info(ctypes.Structure):
     _fields_ = [
         ("n_points", ctypes.c_int64), ("n_kept", ctypes.c_int64),
         ("n_cells", ctypes.c_int32), ("n_nonempty", ctypes.c_int32),
-        ("max_per_cell", ctypes.c_int32), ("n_tiles", ctypes.c_int32),
+        ("max_per_cell", ctypes.c_int32),
         ("n_cams", ctypes.c_int32), ("n_depth", ctypes.c_int32),
         ("feat_h", ctypes.c_int32), ("feat_w", ctypes.c_int32),
         ("nx", ctypes.c_int32), ("ny", ctypes.c_int32),
-        ("n_rows", ctypes.c_int32),
+        ("n_column", ctypes.c_int32), ("n_generic", ctypes.c_int32),
+        ("n_empty", ctypes.c_int32), ("n_runs", ctypes.c_int32),
     ]
 
 

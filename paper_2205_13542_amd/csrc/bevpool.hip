@@ -30,17 +30,10 @@ void free_plan(bevpool_plan_s *plan) {
     (void)hipFree(plan->cell_of_point);
     (void)hipFree(plan->sorted_point);
     (void)hipFree(plan->cell_start);
-    (void)hipFree(plan->tile_cell_begin);
-    (void)hipFree(plan->tile_row_begin);
-    (void)hipFree(plan->tile_cells);
-    (void)hipFree(plan->comp_cell_start);
-    (void)hipFree(plan->comp_point);
-    (void)hipFree(plan->comp_row);
-    (void)hipFree(plan->row_pix);
+    (void)hipFree(plan->column_table);
+    (void)hipFree(plan->generic_hdr);
+    (void)hipFree(plan->generic_runs);
     (void)hipFree(plan->empty_cells);
-    (void)hipFree(plan->tile_hdr);
-    (void)hipFree(plan->heavy_tiles);
-    (void)hipFree(plan->group_tile_begin);
     if (prev >= 0 && prev != plan->device) (void)hipSetDevice(prev);
     plan->magic = 0;
     delete plan;
@@ -141,14 +134,16 @@ int bevpool_plan_info_get(const bevpool_plan_t *plan, bevpool_plan_info *info) {
     info->n_cells = plan->n_cells;
     info->n_nonempty = plan->n_nonempty;
     info->max_per_cell = plan->max_per_cell;
-    info->n_tiles = plan->n_tiles;
+    info->n_column = plan->n_column;
+    info->n_generic = plan->n_generic;
+    info->n_empty = plan->n_empty;
+    info->n_runs = plan->n_runs;
     info->n_cams = plan->geom.n_cams;
     info->n_depth = plan->geom.n_depth;
     info->feat_h = plan->geom.feat_h;
     info->feat_w = plan->geom.feat_w;
     info->nx = plan->geom.nx;
     info->ny = plan->geom.ny;
-    info->n_rows = plan->n_rows;
     return BEVPOOL_OK;
 }
 

@@ -1,30 +1,41 @@
 // Per-frame BEV pooling: fused lift (depth probability x feature) and
 // per-cell sum (BEVFusion, arXiv 2205.13542, Sec. III-B, first paragraph and
-// "Interval Reduction"). The paper gives each cell one GPU thread. Here a
-// workgroup owns a tile of cells along a bundle of camera rays (from the
-// plan), and lanes run across channels.
+// "Interval Reduction"). The paper gives each cell one GPU thread that walks
+// the cell's interval. Here the work follows the camera geometry instead
+// (see the partition in internal.h): one launch, four workgroup roles.
 //
-// One persistent workgroup of 8 waves per CU walks its run of tiles as a
-// software pipeline. While tile k is reduced from LDS, the loads for tile
-// k+1 (its distinct feature rows and depth probabilities) and tile k+2 (its
-// point records, cell list and row pixels) are in flight into registers.
-// After the reduction, tile k+1 is written into LDS. A tile's reduction:
-//   - its points are split into G equal contiguous chunks, one per lane
-//     group (L lanes x NCH chunks of CH channels);
-//   - each group walks its chunk cell by cell, reading feature slices from
-//     LDS (one staged copy per distinct row of the tile) and accumulating
-//     P * F in fp32 registers;
-//   - a cell that lies wholly inside one chunk is stored at once. Cells cut
-//     by chunk edges leave partial sums in LDS, and the chunk holding the
-//     cell's start adds them in chunk order and stores the row.
-// A tile whose rows do not fit in LDS reads its features from memory
-// instead. A single cell with more points than a tile may stage has an
-// extra workgroup of its own, which stages it in rounds. Each workgroup
-// also zeroes its share of the cells without points.
+//   column items   kColDepth depth bins x kColWidth pixel columns of one
+//                  camera. A group of 16 lanes (one DPP row) owns a column
+//                  and holds kColDepth fp32 accumulators per channel. Each
+//                  feature row (n, h, w) is read once and applied to every
+//                  depth bin of the item; the depth probabilities are read
+//                  one per lane and broadcast inside the row with DPP.
+//                  Single-combo cells are stored from registers; the
+//                  combos of a multi-combo cell meet in LDS and the cell's
+//                  first combo adds them in slot order.
+//   light generic  one wave per generic cell. Its runs (consecutive depth
+//                  bins of one pixel) are taken 64 at a time: each lane loads
+//                  one run record and sums the run's depth probabilities,
+//                  then the four lane groups share the runs out, each run
+//                  costing one feature row. Groups are combined by shuffles.
+//   heavy generic  one workgroup per generic cell with more than kGenHeavy
+//                  points; its waves take the 64-run chunks in turn, and the
+//                  16 groups are combined through LDS.
+//   zero rows      cells without points, kZeroCells per workgroup, as one
+//                  flat run of 16-byte stores over their rows.
 //
-// Every output row is written exactly once, with plain stores. The
-// summation order depends only on the plan, so results are deterministic.
-// There is no MFMA: this is a gather and a sum, not a contraction.
+// Channels go across the 16 lanes of a group (channel j + 16k in lane j), so
+// every load and store of a row is contiguous across the group. Rows wider
+// than kSliceChannels are done in slices (grid z).
+//
+// All reads and writes of P, F and the BEV map go through buffer resources
+// of one frame each. An access that must not happen gets an offset past the
+// end of its buffer: the hardware range check then returns 0 for a load and
+// drops a store, so the hot loops carry no branches for bounds or masks.
+//
+// Every output row is written exactly once with plain stores, and every sum
+// runs in an order fixed by the plan, so results are deterministic. There is
+// no MFMA: each feature row meets only a handful of depth bins.
 #include <math.h>
 #include <stdint.h>
 
@@ -33,545 +44,422 @@
 namespace bevpool {
 namespace {
 
-// Input access per dtype and chunk width CH (4 elements, or 1 on the
-// unaligned path), widened exactly to fp32.
-template <int DT, int CH>
-struct In;
+constexpr uint32_t kOff = 0x80000000u;   // past every buffer (sizes stay below 2^31)
+constexpr int kRsrcWord3 = 0x00020000;   // gfx9 raw buffer: 32-bit data format
 
-template <>
-struct In<BEVPOOL_F32, 4> {
-    using T = float;
-    using Raw = uint4;
-    static __device__ __forceinline__ void widen(const Raw &r, float *f) {
-        f[0] = __uint_as_float(r.x);
-        f[1] = __uint_as_float(r.y);
-        f[2] = __uint_as_float(r.z);
-        f[3] = __uint_as_float(r.w);
-    }
-};
+using Rsrc = __amdgpu_buffer_rsrc_t;
 
-template <>
-struct In<BEVPOOL_BF16, 4> {
-    using T = uint16_t;
-    using Raw = uint2;
-    static __device__ __forceinline__ void widen(const Raw &r, float *f) {
-        f[0] = __uint_as_float(r.x << 16);
-        f[1] = __uint_as_float(r.x & 0xFFFF0000u);
-        f[2] = __uint_as_float(r.y << 16);
-        f[3] = __uint_as_float(r.y & 0xFFFF0000u);
-    }
-};
-
-template <>
-struct In<BEVPOOL_F16, 4> {
-    using T = _Float16;
-    using Raw = uint2;
-    typedef _Float16 half4 __attribute__((ext_vector_type(4)));
-    static __device__ __forceinline__ void widen(const Raw &r, float *f) {
-        const half4 h = __builtin_bit_cast(half4, r);
-        f[0] = float(h.x);
-        f[1] = float(h.y);
-        f[2] = float(h.z);
-        f[3] = float(h.w);
-    }
-};
-
-__device__ __forceinline__ float widen1(const float &v) { return v; }
-__device__ __forceinline__ float widen1(const uint16_t &v) { return __uint_as_float(uint32_t(v) << 16); }
-__device__ __forceinline__ float widen1(const _Float16 &v) { return float(v); }
-
-template <int DT>
-struct In<DT, 1> {
-    using T = typename In<DT, 4>::T;
-    using Raw = T;
-    static __device__ __forceinline__ void widen(const Raw &r, float *f) { f[0] = widen1(r); }
-};
-
-template <int DT>
-__device__ __forceinline__ float load_scalar(const typename In<DT, 4>::T *p) {
-    return widen1(*p);
+__device__ __forceinline__ Rsrc make_rsrc(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, int(bytes), kRsrcWord3);
 }
 
-template <int DT, int CH>
-__device__ __forceinline__ typename In<DT, CH>::Raw load_raw(const typename In<DT, CH>::T *p) {
-    return *reinterpret_cast<const typename In<DT, CH>::Raw *>(p);
-}
-
-// fp32 accumulator of one lane: NCH chunks of CH channels
-template <int CH, int NCH>
-struct Acc {
-    float v[CH * NCH];
-    __device__ __forceinline__ void zero() {
-#pragma unroll
-        for (int k = 0; k < CH * NCH; ++k) v[k] = 0.f;
-    }
-    __device__ __forceinline__ void add(const float *s) {
-#pragma unroll
-        for (int k = 0; k < CH * NCH; ++k) v[k] += s[k];
+template <int DT>
+struct Elem;
+template <>
+struct Elem<BEVPOOL_F32> {
+    static constexpr uint32_t kBytes = 4;
+    static __device__ __forceinline__ float load(Rsrc r, uint32_t off) {
+        return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, int(off), 0, 0));
     }
 };
+template <>
+struct Elem<BEVPOOL_BF16> {
+    static constexpr uint32_t kBytes = 2;
+    static __device__ __forceinline__ float load(Rsrc r, uint32_t off) {
+        return __uint_as_float(uint32_t(__builtin_amdgcn_raw_buffer_load_b16(r, int(off), 0, 0)) << 16);
+    }
+};
+template <>
+struct Elem<BEVPOOL_F16> {
+    static constexpr uint32_t kBytes = 2;
+    static __device__ __forceinline__ float load(Rsrc r, uint32_t off) {
+        return float(__builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(r, int(off), 0, 0)));
+    }
+};
+
+__device__ __forceinline__ void store_f32(Rsrc r, uint32_t off, float v) {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, int(off), 0, 0);
+}
 
 struct FwdArgs {
-    const void *P;   // [B][n_points]
-    const void *F;   // [B][n_pix][C]
-    float *out;      // [B][n_cells][C]
-    const int32_t *tile_hdr, *tile_cells, *comp_cell_start, *comp_point, *comp_row, *row_pix;
-    const int32_t *empty_cells, *heavy_tiles, *group_tile_begin;
-    int32_t batch, C, n_cells, n_points, n_pix, n_tiles, n_empty, n_heavy;
-    FastDiv div_cpr;  // division by chunks per row, ceil(C / CH)
+    const char *P, *F;
+    float *out;
+    const int2 *table;
+    const int4 *gen_hdr;
+    const int4 *gen_runs;
+    const int32_t *empty_cells;
+    int32_t N, D, H, W, HW;
+    int32_t n_cells, C, slice_c;
+    uint32_t p_bytes, f_bytes, o_bytes, run_bytes;   // per frame (runs: whole table)
+    int32_t items_d, items_w, n_items;
+    int32_t n_heavy, n_light, n_empty;
+    int32_t base_col, base_zero, base_light;
+    int32_t zero_vec, zero_units;       // empty rows: float4 units (or floats) per row
+    FastDiv div_units;
 };
 
-constexpr int kThreads = kPersistentBlock;                    // 512
-constexpr int kUnroll = 8;
-constexpr int kRecPerThread = kPointBudget / kThreads;        // 4
-constexpr int kFChunkPerThread = 8;
-constexpr int kFChunks = kFChunkPerThread * kThreads;         // feature chunks a tile may stage
-static_assert(kPointBudget % kThreads == 0, "records split evenly over the threads");
-static_assert(kMaxTileCells + 1 <= kThreads, "one cell entry per thread");
-
-// Lane groups: L lanes per group, S groups per wave, G per workgroup.
-struct Groups {
-    int L, S, G, sg, lsg, g;
-    bool in_group;
-    __device__ __forceinline__ Groups(int lanes, int tid, int waves) {
-        L = lanes;
-        S = kWaveSize / L;
-        G = waves * S;
-        const int lane = tid % kWaveSize, wave = tid / kWaveSize;
-        sg = lane / L;
-        lsg = lane - sg * L;
-        in_group = sg < S;
-        g = wave * S + sg;
-    }
+// The three buffers of frame b.
+struct Frame {
+    Rsrc P, F, O;
+    __device__ __forceinline__ Frame(const FwdArgs &a, int b)
+        : P(make_rsrc(a.P + int64_t(b) * a.p_bytes, a.p_bytes)),
+          F(make_rsrc(a.F + int64_t(b) * a.f_bytes, a.f_bytes)),
+          O(make_rsrc(reinterpret_cast<const char *>(a.out) + int64_t(b) * a.o_bytes, a.o_bytes)) {}
 };
 
-// Sum P * F over records [lo, hi) into acc. LDS mode: rec.x is the byte
-// offset of the point's row in s_F (which the caller has advanced to the
-// channel block); global mode: rec.x is its pixel. Lane lsg reads chunks
-// lsg and lsg + L, so each read of a group covers one contiguous run.
-template <int DT, int CH, int NCH, bool LDS>
-__device__ __forceinline__ void gather_sum(const unsigned char *s_F, const typename In<DT, CH>::T *Fc,
-                                           int C, int Crem, int L, int lsg, const int2 *s_rec,
-                                           int lo, int hi, Acc<CH, NCH> &acc) {
-    using R = typename In<DT, CH>::Raw;
-    using T = typename In<DT, CH>::T;
-    // element offset of each chunk in the row; a chunk past the row's end
-    // (last, partial channel block) reads the row's first chunk instead,
-    // and its sums are never stored
-    int goff[NCH];
-#pragma unroll
-    for (int k = 0; k < NCH; ++k) {
-        goff[k] = (lsg + k * L) * CH;
-        if (goff[k] >= Crem) goff[k] = 0;
-    }
-    auto fetch = [&](int2 e, R *r) {
-#pragma unroll
-        for (int k = 0; k < NCH; ++k) {
-            if (LDS) r[k] = *reinterpret_cast<const R *>(s_F + e.x + goff[k] * int(sizeof(T)));
-            else r[k] = load_raw<DT, CH>(Fc + int64_t(e.x) * C + goff[k]);
-        }
-    };
-    auto fma_in = [&](float p, const R *r) {
-#pragma unroll
-        for (int k = 0; k < NCH; ++k) {
-            float f[CH];
-            In<DT, CH>::widen(r[k], f);
-#pragma unroll
-            for (int q = 0; q < CH; ++q) acc.v[k * CH + q] = fmaf(p, f[q], acc.v[k * CH + q]);
-        }
-    };
-    int i = lo;
-    for (; i + kUnroll <= hi; i += kUnroll) {
-        int2 e[kUnroll];
-        R r[kUnroll][NCH];
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) e[u] = s_rec[i + u];
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) fetch(e[u], r[u]);
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) fma_in(__int_as_float(e[u].y), r[u]);
-    }
-    for (; i < hi; ++i) {
-        const int2 e = s_rec[i];
-        R r[NCH];
-        fetch(e, r);
-        fma_in(__int_as_float(e.y), r);
-    }
+constexpr int kSlots = kColDepth * kColWidth;   // 128 combos per item
+constexpr int kStages = 6;                      // row-pair stages in flight per wave
+constexpr int kZeroCells = kSlots;              // empty rows per zeroing workgroup
+
+// LDS row stride of a slot: 16*NCH floats, padded so that the four groups
+// of a wave start on different bank quarters.
+template <int NCH>
+constexpr int slot_stride() { return 16 * NCH + ((NCH % 2 == 0) ? 16 : 0); }
+
+// Value of lane J of this lane's DPP row (row_newbcast).
+template <int J>
+__device__ __forceinline__ int row_bcast(int v) {
+    return __builtin_amdgcn_mov_dpp(v, 0x150 + J, 0xF, 0xF, false);
+}
+template <int J>
+__device__ __forceinline__ float row_bcast(float v) {
+    return __int_as_float(row_bcast<J>(__float_as_int(v)));
 }
 
-// store a lane's chunks of one output row; Crem = channels left in the row
-template <int CH, int NCH>
-__device__ __forceinline__ void store_acc(float *row, int Crem, int L, int lsg, const Acc<CH, NCH> &acc) {
-#pragma unroll
-    for (int k = 0; k < NCH; ++k) {
-        const int ch = (lsg + k * L) * CH;
-        if (ch < Crem) {
-            if (CH == 4) {
-                *reinterpret_cast<float4 *>(row + ch) =
-                    make_float4(acc.v[k * CH], acc.v[k * CH + 1], acc.v[k * CH + 2], acc.v[k * CH + 3]);
-            } else {
-                row[ch] = acc.v[k * CH];
-            }
-        }
-    }
+// Item order with consecutive depth blocks of one column block adjacent,
+// and adjacent items placed on the same XCD (workgroups are dealt to the 8
+// XCDs round-robin), so the feature rows they share meet in one L2.
+__device__ __forceinline__ int xcd_remap(int b, int G) {
+    const int q = G >> 3, r = G & 7, x = b & 7, k = b >> 3;
+    return x < r ? x * (q + 1) + k : r * (q + 1) + (x - r) * q + k;
 }
 
-// partial sums in LDS: slot s holds L lanes x (CH * NCH) floats
-template <int CH, int NCH>
-__device__ __forceinline__ float *part_slot(float *s_part, int slot, int L, int lsg) {
-    return s_part + (slot * L + lsg) * (CH * NCH);
-}
-
-// A tile header: cell list, points and staged rows of one work item.
-struct Hdr {
-    int tcb, ncell, tpb, npts, trb, nrows, frame;
-    bool direct;
+template <int NCH>
+struct Row {
+    float v[NCH];
 };
 
-// A header is fetched raw and decoded later: reading its fields at once
-// would make the wave wait for every load issued before it.
-struct RawHdr {
-    int4 x, y;
-    int item;
-};
-
-__device__ __forceinline__ RawHdr fetch_hdr(const FwdArgs &a, int item, int t_begin, int n_items) {
-    RawHdr r{make_int4(0, 0, 0, 0), make_int4(0, 0, 0, 0), item};
-    if (item < n_items) {
-        // through the scalar cache: the wave does not wait on vector loads
-        typedef __attribute__((address_space(4))) const int const_int;
-        const int t = t_begin + item / a.batch;
-        const const_int *p = (const const_int *)(a.tile_hdr + 8 * int64_t(t));
-        r.x = make_int4(p[0], p[1], p[2], p[3]);
-        r.y = make_int4(p[4], p[5], p[6], p[7]);
-    }
-    return r;
-}
-
-__device__ __forceinline__ Hdr decode_hdr(const FwdArgs &a, const RawHdr &r, int cpr) {
-    Hdr h{0, 0, 0, 0, 0, 0, 0, false};
-    h.frame = r.item - (r.item / a.batch) * a.batch;
-    if (r.x.w <= kPointBudget) {  // heavier tiles have workgroups of their own
-        h.tcb = r.x.x;
-        h.ncell = r.x.y;
-        h.tpb = r.x.z;
-        h.npts = r.x.w;
-        h.trb = r.y.x;
-        h.nrows = r.y.y;
-    }
-    h.direct = int64_t(h.nrows) * cpr > kFChunks;
-    return h;
-}
-
-// Loads of a work item that need only its header: point ids, rows, cell
-// entries, and the pixel of every feature chunk this thread will stage.
-struct Rec {
-    int pid[kRecPerThread], row[kRecPerThread], fpix[kFChunkPerThread], cs, cid;
-};
-
-__device__ __forceinline__ void load_records(const FwdArgs &a, const Hdr &h, int cpr, int tid, Rec &r) {
-#pragma unroll
-    for (int i = 0; i < kRecPerThread; ++i) {
-        const int j = tid + i * kThreads;
-        r.pid[i] = 0;
-        r.row[i] = 0;
-        if (j < h.npts) {
-            r.pid[i] = a.comp_point[h.tpb + j];
-            r.row[i] = a.comp_row[h.tpb + j];
-        }
-    }
-    const int nchunks = h.direct ? 0 : h.nrows * cpr;
-#pragma unroll
-    for (int i = 0; i < kFChunkPerThread; ++i) {
-        const int j = tid + i * kThreads;
-        r.fpix[i] = 0;
-        if (j < nchunks) r.fpix[i] = a.row_pix[h.trb + int(fdiv(uint32_t(j), a.div_cpr))];
-    }
-    r.cs = (tid <= h.ncell && h.npts > 0) ? a.comp_cell_start[h.tcb + tid] : 0;
-    r.cid = (tid < h.ncell && h.npts > 0) ? a.tile_cells[h.tcb + tid] : 0;
-}
-
-// Loads that need the records: feature chunks, depth probabilities and,
-// for a tile read from memory, each point's pixel.
-template <int DT, int CH>
+// Two feature rows of a column and the lane's depth probability for them.
+template <int NCH>
 struct Stage {
-    typename In<DT, CH>::Raw v[kFChunkPerThread];
-    float pv[kRecPerThread];
-    int x[kRecPerThread];
+    float pv;
+    Row<NCH> f0, f1;
 };
 
-template <int DT, int CH>
-__device__ __forceinline__ void load_stage(const FwdArgs &a, const Hdr &h, int cpr, int tid,
-                                           const Rec &r, Stage<DT, CH> &st) {
-    using T = typename In<DT, CH>::T;
-    const T *Pb = static_cast<const T *>(a.P) + int64_t(h.frame) * a.n_points;
-    const T *Fb = static_cast<const T *>(a.F) + int64_t(h.frame) * a.n_pix * a.C;
-    const int nchunks = h.direct ? 0 : h.nrows * cpr;
+// Chunks k = 0..NCH-1 of a row slice (element offset of chunk 0 in bytes,
+// or kOff). Lanes past the slice's last channel read bytes that are never
+// stored.
+template <int DT, int NCH>
+__device__ __forceinline__ void load_row(Row<NCH> &r, Rsrc src, uint32_t off) {
 #pragma unroll
-    for (int i = 0; i < kFChunkPerThread; ++i) {
-        const int j = tid + i * kThreads;
-        if (j < nchunks) {
-            const int q = j - int(fdiv(uint32_t(j), a.div_cpr)) * cpr;
-            st.v[i] = load_raw<DT, CH>(Fb + int64_t(r.fpix[i]) * a.C + q * CH);
-        }
+    for (int k = 0; k < NCH; ++k) r.v[k] = Elem<DT>::load(src, off + uint32_t(k) * 16 * Elem<DT>::kBytes);
+}
+
+// Store chunks of a row slice at byte offset off (or kOff). Only the last
+// chunk can run past the slice: tail_ok says whether it does not.
+template <int NCH>
+__device__ __forceinline__ void store_row(Rsrc dst, uint32_t off, const float *v, bool tail_ok) {
+#pragma unroll
+    for (int k = 0; k < NCH - 1; ++k) store_f32(dst, off + uint32_t(k) * 64, v[k]);
+    store_f32(dst, tail_ok ? off + uint32_t(NCH - 1) * 64 : kOff, v[NCH - 1]);
+}
+
+// acc[J] += P(depth bin J, this row) * f for every depth bin J of the item;
+// the probabilities sit in lanes OFF..OFF+7 of the row (0 where a bin has
+// no point in this row). Branch-free: skipping absent bins saves little.
+template <int OFF, int J, int NCH>
+struct Apply {
+    static __device__ __forceinline__ void run(float (&acc)[kColDepth][NCH], float pv,
+                                               const Row<NCH> &f) {
+        const float pb = row_bcast<OFF + J>(pv);
+#pragma unroll
+        for (int k = 0; k < NCH; ++k) acc[J][k] = __builtin_fmaf(pb, f.v[k], acc[J][k]);
+        Apply<OFF, J + 1, NCH>::run(acc, pv, f);
     }
+};
+template <int OFF, int NCH>
+struct Apply<OFF, kColDepth, NCH> {
+    static __device__ __forceinline__ void run(float (&)[kColDepth][NCH], float, const Row<NCH> &) {}
+};
+
+// After the row loop: single-combo cells are stored, multi-combo partials
+// go to their LDS slot. Lane J of the group holds the entry of depth bin J.
+template <int J, int NCH>
+struct Emit {
+    static __device__ __forceinline__ void run(const float (&acc)[kColDepth][NCH], int ecell, int ey,
+                                               uint32_t dm, Rsrc out, uint32_t ch_off, int C,
+                                               float *s_part, int wl, bool tail_ok) {
+        if (dm & (1u << J)) {
+            const int cell = row_bcast<J>(ecell);
+            const uint32_t y = uint32_t(row_bcast<J>(ey));
+            const bool single = cell >= 0 && !(y & kComboMulti);
+            store_row<NCH>(out, single ? uint32_t(cell) * uint32_t(C) * 4u + ch_off : kOff, acc[J],
+                           tail_ok);
+            if (cell >= 0 && (y & kComboMulti)) {
+                float *dst = s_part + (J * kColWidth + wl) * slot_stride<NCH>() + (threadIdx.x & 15);
 #pragma unroll
-    for (int i = 0; i < kRecPerThread; ++i) {
-        const int j = tid + i * kThreads;
-        st.pv[i] = 0.f;
-        st.x[i] = 0;
-        if (j < h.npts) {
-            st.pv[i] = load_scalar<DT>(Pb + r.pid[i]);
-            if (h.direct) st.x[i] = a.row_pix[h.trb + r.row[i]];
+                for (int k = 0; k < NCH; ++k) dst[16 * k] = acc[J][k];
+            }
+        }
+        Emit<J + 1, NCH>::run(acc, ecell, ey, dm, out, ch_off, C, s_part, wl, tail_ok);
+    }
+};
+template <int NCH>
+struct Emit<kColDepth, NCH> {
+    static __device__ __forceinline__ void run(const float (&)[kColDepth][NCH], int, int, uint32_t,
+                                               Rsrc, uint32_t, int, float *, int, bool) {}
+};
+
+// Rows of kZeroCells listed empty cells of frame b (in slice 0 only),
+// written as one flat sequence of 16-byte (or 4-byte) units: unit f is unit
+// f % U of row f / U. Rows of consecutive cells are adjacent in memory, so
+// runs of empty cells become contiguous stores. The cell ids are staged in
+// LDS first, so no store waits on a load.
+__device__ void zero_rows(const FwdArgs &a, int zb, int b, int *s_cell) {
+    const int e0 = zb * kZeroCells;
+    const int ne = min(kZeroCells, a.n_empty - e0);
+    if (int(threadIdx.x) < ne) s_cell[threadIdx.x] = a.empty_cells[e0 + threadIdx.x];
+    __syncthreads();
+    const int U = a.zero_units;
+    const int total = ne * U;
+    if (a.zero_vec) {
+        float4 *o = reinterpret_cast<float4 *>(a.out + int64_t(b) * a.n_cells * a.C);
+        for (int f = threadIdx.x; f < total; f += kBlock) {
+            const int r = int(fdiv(uint32_t(f), a.div_units));
+            o[int64_t(s_cell[r]) * U + (f - r * U)] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    } else {
+        float *o = a.out + int64_t(b) * a.n_cells * a.C;
+        for (int f = threadIdx.x; f < total; f += kBlock) {
+            const int r = int(fdiv(uint32_t(f), a.div_units));
+            o[int64_t(s_cell[r]) * U + (f - r * U)] = 0.f;
         }
     }
 }
 
-template <int DT, int CH, int NCH>
-__device__ __forceinline__ void reduce_tile(const FwdArgs &a, const Hdr &h, int tid,
-                                            unsigned char *s_F, const int2 *s_rec, const int *s_cs,
-                                            const int *s_cid, int *s_pcell, float *s_part) {
-    using T = typename In<DT, CH>::T;
-    using A = Acc<CH, NCH>;
-    constexpr int W = CH * NCH;
-    const int C = a.C;
-    const int npts = h.npts, ncell = h.ncell, tpb = h.tpb;
-    if (npts == 0) return;  // uniform across the workgroup
-    const T *Fb = static_cast<const T *>(a.F) + int64_t(h.frame) * a.n_pix * C;
-    float *ob = a.out + int64_t(h.frame) * a.n_cells * C;
-    const Groups gr(min(kWaveSize, (C + W - 1) / W), tid, kPersistentWaves);
-    const int cblock = gr.L * W;
-    const int ca = npts * gr.g / gr.G, cb = npts * (gr.g + 1) / gr.G;  // this group's chunk
+template <int DT, int NCH>
+__device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0, int cn,
+                            float *s_part, int *s_cell) {
+    constexpr uint32_t ES = Elem<DT>::kBytes;
+    const int db = item % a.items_d;
+    const int t = item / a.items_d;
+    const int wb = t % a.items_w, n = t / a.items_w;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int j = lane & 15;
+    const int wl = wave * 4 + (lane >> 4);        // column within the item
+    const int w = wb * kColWidth + wl;
+    const int jd = j & 7;
+    const int d = db * kColDepth + jd;
+    const bool in_w = w < a.W;
+    const bool tail_ok = j + 16 * (NCH - 1) < cn;
 
-    for (int ch0 = 0; ch0 < C; ch0 += cblock) {
-        A head, tail;
-        head.zero();
-        tail.zero();
-        int head_cell = -1, tail_cell = -1;
-        const bool lane_live = gr.in_group && ch0 + gr.lsg * CH < C;
-        if (gr.in_group && ca < cb) {
-            int lo = 0, hi = ncell - 1;  // last j with s_cs[j] - tpb <= ca
-            while (lo < hi) {
-                const int mid = (lo + hi + 1) >> 1;
-                if (s_cs[mid] - tpb <= ca) lo = mid;
-                else hi = mid - 1;
-            }
-            for (int j = lo;; ++j) {
-                const int cs = s_cs[j] - tpb, ce = s_cs[j + 1] - tpb;
-                A acc;
-                acc.zero();
-                if (lane_live) {
-                    if (h.direct)
-                        gather_sum<DT, CH, NCH, false>(s_F, Fb + ch0, C, C - ch0, gr.L, gr.lsg, s_rec,
-                                                       max(ca, cs), min(cb, ce), acc);
-                    else
-                        gather_sum<DT, CH, NCH, true>(s_F + ch0 * int(sizeof(T)), Fb, C, C - ch0, gr.L,
-                                                      gr.lsg, s_rec, max(ca, cs), min(cb, ce), acc);
-                }
-                if (cs < ca) {
-                    head = acc;
-                    head_cell = j;
-                } else if (ce > cb) {
-                    tail = acc;
-                    tail_cell = j;
-                } else if (lane_live) {
-                    store_acc<CH, NCH>(ob + int64_t(s_cid[j]) * C + ch0, C - ch0, gr.L, gr.lsg, acc);
-                }
-                if (ce >= cb) break;
-            }
-        }
-        if (gr.in_group) {
-            if (gr.lsg == 0) {
-                s_pcell[2 * gr.g] = head_cell;
-                s_pcell[2 * gr.g + 1] = tail_cell;
-            }
-            float *hp = part_slot<CH, NCH>(s_part, 2 * gr.g, gr.L, gr.lsg);
-            float *tp = part_slot<CH, NCH>(s_part, 2 * gr.g + 1, gr.L, gr.lsg);
-#pragma unroll
-            for (int k = 0; k < W; ++k) {
-                hp[k] = head.v[k];
-                tp[k] = tail.v[k];
-            }
-        }
-        __syncthreads();
-        // the chunk holding the start of a cut cell adds the later chunks'
-        // partial sums of that cell, in chunk order, and stores the row
-        if (lane_live) {
-            const int j = s_pcell[2 * gr.g + 1];
-            if (j >= 0) {
-                A sum;
-                sum.zero();
-                sum.add(part_slot<CH, NCH>(s_part, 2 * gr.g + 1, gr.L, gr.lsg));
-                for (int g2 = gr.g + 1; g2 < gr.G; ++g2) {
-                    if (npts * g2 / gr.G == npts * (g2 + 1) / gr.G) continue;  // empty chunk
-                    if (s_pcell[2 * g2] != j) break;
-                    sum.add(part_slot<CH, NCH>(s_part, 2 * g2, gr.L, gr.lsg));
-                }
-                store_acc<CH, NCH>(ob + int64_t(s_cid[j]) * C + ch0, C - ch0, gr.L, gr.lsg, sum);
-            }
-        }
-        __syncthreads();  // partial slots free for the next channel block
-    }
-}
-
-// One cell with more points than a tile may stage: rounds of kPointBudget
-// points, features read from memory, every group accumulating the cell,
-// partials combined in group order.
-template <int DT, int CH, int NCH>
-__device__ void heavy_cell(const FwdArgs &a, int tile, int tid, int2 *s_rec, float *s_part) {
-    using T = typename In<DT, CH>::T;
-    using A = Acc<CH, NCH>;
-    constexpr int W = CH * NCH;
-    const int C = a.C;
-    const int *hd = a.tile_hdr + 8 * int64_t(tile);
-    const int tcb = hd[0], tpb = hd[2], npts = hd[3], trb = hd[4];
-    const int cid = a.tile_cells[tcb];
-    const Groups gr(min(kWaveSize, (C + W - 1) / W), tid, kPersistentWaves);
-    for (int fb = 0; fb < a.batch; ++fb) {
-        const T *Pb = static_cast<const T *>(a.P) + int64_t(fb) * a.n_points;
-        const T *Fb = static_cast<const T *>(a.F) + int64_t(fb) * a.n_pix * C;
-        float *orow = a.out + (int64_t(fb) * a.n_cells + cid) * C;
-        for (int ch0 = 0; ch0 < C; ch0 += gr.L * W) {
-            A acc;
-            acc.zero();
-            for (int r0 = 0; r0 < npts; r0 += kPointBudget) {
-                const int nr = min(kPointBudget, npts - r0);
-                __syncthreads();
-                for (int i = tid; i < nr; i += kThreads) {
-                    const int q = tpb + r0 + i;
-                    const int pix = a.row_pix[trb + a.comp_row[q]];
-                    s_rec[i] = make_int2(pix, __float_as_int(load_scalar<DT>(Pb + a.comp_point[q])));
-                }
-                __syncthreads();
-                if (gr.in_group && ch0 + gr.lsg * CH < C)
-                    gather_sum<DT, CH, NCH, false>(nullptr, Fb + ch0, C, C - ch0, gr.L, gr.lsg, s_rec,
-                                                   nr * gr.g / gr.G, nr * (gr.g + 1) / gr.G, acc);
-            }
-            if (gr.in_group) {
-                float *slot = part_slot<CH, NCH>(s_part, gr.g, gr.L, gr.lsg);
-#pragma unroll
-                for (int k = 0; k < W; ++k) slot[k] = acc.v[k];
-            }
-            __syncthreads();
-            if (gr.in_group && gr.g == 0) {
-                A sum;
-                sum.zero();
-                for (int g2 = 0; g2 < gr.G; ++g2) sum.add(part_slot<CH, NCH>(s_part, g2, gr.L, gr.lsg));
-                store_acc<CH, NCH>(orow + ch0, C - ch0, gr.L, gr.lsg, sum);
-            }
-            __syncthreads();
-        }
-    }
-}
-
-__device__ __forceinline__ void wait_all_loads() {
-    __builtin_amdgcn_s_waitcnt(0);  // vmcnt, expcnt and lgkmcnt all zero
-}
-
-template <int DT, int CH, int NCH>
-__global__ __launch_bounds__(kThreads) void k_forward(FwdArgs a) {
-    using T = typename In<DT, CH>::T;
-    using R = typename In<DT, CH>::Raw;
-    constexpr int W = CH * NCH;
-    __shared__ __align__(16) unsigned char s_F[kFChunks * CH * sizeof(T)];  // staged rows
-    __shared__ int2 s_rec[kPointBudget];                                    // row offset (or pixel), P
-    __shared__ int s_cs[kMaxTileCells + 1];                                 // interval table slice
-    __shared__ int s_cid[kMaxTileCells];                                    // cell ids
-    __shared__ int s_pcell[2 * kThreads];                                   // cut cells per chunk
-    __shared__ __align__(16) float s_part[2 * kThreads * W];                // their partial sums
-
-    const int tid = threadIdx.x;
-    const int C = a.C;
-    if (int(blockIdx.x) >= kPersistentGroups) {
-        heavy_cell<DT, CH, NCH>(a, a.heavy_tiles[blockIdx.x - kPersistentGroups], tid, s_rec, s_part);
-        return;
-    }
-    // Workgroups are dealt to the 8 XCDs round-robin. Remap them so that each
-    // XCD walks one contiguous run of tiles: neighbouring tiles share feature
-    // rows, which then stay in that XCD's L2.
-    const int w = (blockIdx.x & 7) * (kPersistentGroups / 8) + (blockIdx.x >> 3);
-    const int t_begin = a.group_tile_begin[w], t_end = a.group_tile_begin[w + 1];
-    const int n_items = (t_end - t_begin) * a.batch;
-    const int cpr = (C + CH - 1) / CH;
-
-    auto write_item = [&](const Hdr &h, const Rec &r, const Stage<DT, CH> &st) {
-        const int row_bytes = cpr * CH * int(sizeof(T));
-        const int nchunks = h.direct ? 0 : h.nrows * cpr;
-#pragma unroll
-        for (int i = 0; i < kFChunkPerThread; ++i) {
-            const int j = tid + i * kThreads;
-            if (j < nchunks) *reinterpret_cast<R *>(s_F + size_t(j) * CH * sizeof(T)) = st.v[i];
-        }
-#pragma unroll
-        for (int i = 0; i < kRecPerThread; ++i) {
-            const int j = tid + i * kThreads;
-            if (j < h.npts)
-                s_rec[j] = make_int2(h.direct ? st.x[i] : r.row[i] * row_bytes, __float_as_int(st.pv[i]));
-        }
-        if (tid <= h.ncell) s_cs[tid] = r.cs;
-        if (tid < h.ncell) s_cid[tid] = r.cid;
+    // The row loop covers all H rows, so its loads need nothing from the
+    // column table and the first stages are issued before the entries
+    // arrive; a lane's probability is masked to its combo's row range when
+    // its stage is applied.
+    const bool dw_ok = in_w && d < a.D;
+    const uint32_t p_col = dw_ok ? uint32_t(((n * a.D + d) * a.H) * a.W + w) * ES : kOff;
+    const uint32_t p_row = uint32_t(a.W) * ES;
+    const uint32_t f_col = in_w ? (uint32_t(n * a.HW + w) * uint32_t(a.C) + uint32_t(c0 + j)) * ES : kOff;
+    const uint32_t f_row = uint32_t(a.W) * uint32_t(a.C) * ES;
+    const int hsel = j >> 3;
+    const int H = a.H;
+    auto load_stage = [&](Stage<NCH> &st, int h) {
+        st.pv = Elem<DT>::load(fr.P, h + hsel < H ? p_col + uint32_t(h + hsel) * p_row : kOff);
+        load_row<DT, NCH>(st.f0, fr.F, h < H ? f_col + uint32_t(h) * f_row : kOff);
+        load_row<DT, NCH>(st.f1, fr.F, h + 1 < H ? f_col + uint32_t(h + 1) * f_row : kOff);
     };
+    int2 e = make_int2(-1, 0);
+    if (dw_ok) e = a.table[(int64_t(n) * a.D + d) * a.W + w];
+    Stage<NCH> st[kStages];
+#pragma unroll
+    for (int u = 0; u < kStages; ++u) load_stage(st[u], 2 * u);
 
-    // prologue: item 0 into LDS, item 1's records in registers
-    Hdr hC = decode_hdr(a, fetch_hdr(a, 0, t_begin, n_items), cpr);
-    Hdr hN = decode_hdr(a, fetch_hdr(a, 1, t_begin, n_items), cpr);
-    Hdr hNN = decode_hdr(a, fetch_hdr(a, 2, t_begin, n_items), cpr);
-    Rec rN, rNN;
-    Stage<DT, CH> st;
-    load_records(a, hC, cpr, tid, rN);
-    wait_all_loads();
-    load_stage<DT, CH>(a, hC, cpr, tid, rN, st);
-    {
-        // this workgroup's share of the cells without points
-        const int z0 = int(int64_t(a.n_empty) * w / kPersistentGroups);
-        const int z1 = int(int64_t(a.n_empty) * (w + 1) / kPersistentGroups);
-        const int n = (z1 - z0) * cpr;
-        for (int fb = 0; fb < a.batch; ++fb) {
-            float *ob = a.out + int64_t(fb) * a.n_cells * C;
-            for (int idx = tid; idx < n; idx += kThreads) {
-                const int cl = int(fdiv(uint32_t(idx), a.div_cpr));
-                const int ch = (idx - cl * cpr) * CH;
-                float *row = ob + int64_t(a.empty_cells[z0 + cl]) * C;
-                if (CH == 4) *reinterpret_cast<float4 *>(row + ch) = make_float4(0.f, 0.f, 0.f, 0.f);
-                else row[ch] = 0.f;
+    const bool act = e.x >= 0;
+    const uint32_t ey = uint32_t(e.y);
+    const int hlo = act ? int(ey & 0xFFFFu) : 0x7FFFFFFF;
+    const int hhi = act ? int((ey >> 16) & 0x3FFFu) : 0;
+    if (j < 8) s_cell[jd * kColWidth + wl] = (act && (ey & kComboMulti)) ? e.x : -1;
+    // depth bins present in the wave (a wave without any skips the loop)
+    const uint64_t bal = __ballot(act);
+    const uint32_t dm = uint32_t((bal | (bal >> 16) | (bal >> 32) | (bal >> 48)) & 0xFFu);
+
+    float acc[kColDepth][NCH];
+#pragma unroll
+    for (int q = 0; q < kColDepth; ++q)
+#pragma unroll
+        for (int k = 0; k < NCH; ++k) acc[q][k] = 0.f;
+
+    if (dm != 0) {
+        // a ring of kStages stages of two rows: while one stage is applied,
+        // the loads of the next kStages - 1 are outstanding
+        for (int h = 0; h < H; h += 2 * kStages) {
+#pragma unroll
+            for (int u = 0; u < kStages; ++u) {
+                const int hs = h + 2 * u;
+                if (hs >= H) break;
+                const int hp = hs + hsel;
+                const float pv = (hp >= hlo && hp < hhi) ? st[u].pv : 0.f;
+                Apply<0, 0, NCH>::run(acc, pv, st[u].f0);
+                Apply<8, 0, NCH>::run(acc, pv, st[u].f1);
+                load_stage(st[u], hs + 2 * kStages);
             }
         }
     }
-    wait_all_loads();
-    write_item(hC, rN, st);
-    load_records(a, hN, cpr, tid, rN);
-    wait_all_loads();
+
+    const uint32_t ch_off = uint32_t(c0 + j) * 4u;
+    Emit<0, NCH>::run(acc, e.x, e.y, dm, fr.O, ch_off, a.C, s_part, wl, tail_ok);
     __syncthreads();
 
-    for (int k = 0; k < n_items; ++k) {
-        // in flight during the reduction of item k: item k+3's header, item
-        // k+1's features and probabilities, item k+2's records
-        const RawHdr rawF = fetch_hdr(a, k + 3, t_begin, n_items);
-        load_stage<DT, CH>(a, hN, cpr, tid, rN, st);
-        load_records(a, hNN, cpr, tid, rNN);
-        reduce_tile<DT, CH, NCH>(a, hC, tid, s_F, s_rec, s_cs, s_cid, s_pcell, s_part);
-        wait_all_loads();
-        __syncthreads();  // item k is no longer read from LDS
-        write_item(hN, rN, st);
-        __syncthreads();
-        hC = hN;
-        hN = hNN;
-        hNN = decode_hdr(a, rawF, cpr);
-        rN = rNN;
+    // Multi-combo cells: the group of the cell's first combo adds the cell's
+    // slots in ascending slot order. A cell's slots all lie in this item, at
+    // or after its first combo.
+    constexpr int SS = slot_stride<NCH>();
+    const int gsh = (lane >> 4) * 16;
+#pragma unroll
+    for (int J = 0; J < kColDepth; ++J) {
+        const int s0 = J * kColWidth + wl;
+        const int cell = s_cell[s0];
+        const bool owner = cell >= 0 && (uint32_t(__shfl(e.y, (lane & 48) | J)) & kComboOwner);
+        if (__ballot(owner) == 0) continue;
+        float sum[NCH];
+#pragma unroll
+        for (int k = 0; k < NCH; ++k) sum[k] = 0.f;
+        for (int r = J; r < kColDepth; ++r) {
+            const int tt = r * kColWidth + j;
+            const bool m = owner && tt >= s0 && s_cell[tt] == cell;
+            uint32_t gm = uint32_t(__ballot(m) >> gsh) & 0xFFFFu;
+            while (gm) {
+                const int k0 = __builtin_ctz(gm);
+                gm &= gm - 1;
+                const float *src = s_part + (r * kColWidth + k0) * SS + j;
+#pragma unroll
+                for (int k = 0; k < NCH; ++k) sum[k] += src[16 * k];
+            }
+        }
+        store_row<NCH>(fr.O, owner ? uint32_t(cell) * uint32_t(a.C) * 4u + ch_off : kOff, sum, tail_ok);
     }
 }
 
-template <int DT, int CH, int NCH>
-void launch(const FwdArgs &a, int grid, hipStream_t stream) {
-    hipLaunchKernelGGL((k_forward<DT, CH, NCH>), dim3(grid), dim3(kThreads), 0, stream, a);
+// A generic cell's runs in chunks of 64: lane i loads run i of the chunk and
+// sums its depth probabilities; then the four lane groups take the runs
+// round-robin, four at a time, each run costing one feature row. A group's
+// runs are added in a fixed order.
+template <int DT, int NCH>
+__device__ __forceinline__ void generic_runs(float (&acc)[NCH], const FwdArgs &a, const Frame &fr,
+                                             int4 hdr, int c0, int first_chunk, int chunk_step) {
+    constexpr uint32_t ES = Elem<DT>::kBytes;
+    const int lane = threadIdx.x & 63;
+    const int j = lane & 15, grp = lane >> 4;
+    const Rsrc runs = make_rsrc(a.gen_runs, a.run_bytes);
+    for (int ch = first_chunk; ch * 64 < hdr.z; ch += chunk_step) {
+        const int nr = min(64, hdr.z - ch * 64);
+        const uint32_t roff = lane < nr ? uint32_t(hdr.y + ch * 64 + lane) * 16u : kOff;
+        const auto rv = __builtin_amdgcn_raw_buffer_load_b128(runs, int(roff), 0, 0);
+        const int p0 = int(rv[0]), pix = int(rv[1]), len = int(rv[2]);
+        float ps = 0.f;
+        for (int q = 0; q < len; ++q) ps += Elem<DT>::load(fr.P, uint32_t(p0 + q * a.HW) * ES);
+        for (int i0 = 0; i0 < nr; i0 += 16) {
+            float pr[4];
+            Row<NCH> f[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int i = i0 + 4 * u + grp;
+                pr[u] = __shfl(ps, i & 63);
+                const int px = __shfl(pix, i & 63);
+                load_row<DT, NCH>(f[u], fr.F,
+                                  i < nr ? (uint32_t(px) * uint32_t(a.C) + uint32_t(c0 + j)) * ES : kOff);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int k = 0; k < NCH; ++k) acc[k] = __builtin_fmaf(pr[u], f[u].v[k], acc[k]);
+        }
+    }
+}
+
+template <int DT, int NCH>
+__device__ void light_generic(const FwdArgs &a, const Frame &fr, int k, int c0, int cn) {
+    const int lane = threadIdx.x & 63;
+    const int j = lane & 15, grp = lane >> 4;
+    const int4 hdr = a.gen_hdr[a.n_heavy + k];
+    float acc[NCH];
+#pragma unroll
+    for (int q = 0; q < NCH; ++q) acc[q] = 0.f;
+    generic_runs<DT, NCH>(acc, a, fr, hdr, c0, 0, 1);
+    // (g0 + g1) + (g2 + g3), the same in every lane of the wave
+#pragma unroll
+    for (int q = 0; q < NCH; ++q) {
+        const float s = acc[q] + __shfl_xor(acc[q], 16);
+        acc[q] = s + __shfl_xor(s, 32);
+    }
+    store_row<NCH>(fr.O, grp == 0 ? (uint32_t(hdr.x) * uint32_t(a.C) + uint32_t(c0 + j)) * 4u : kOff,
+                   acc, j + 16 * (NCH - 1) < cn);
+}
+
+template <int DT, int NCH>
+__device__ void heavy_generic(const FwdArgs &a, const Frame &fr, int k, int c0, int cn,
+                              float *s_part) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int j = lane & 15;
+    const int wl = wave * 4 + (lane >> 4);
+    constexpr int SS = slot_stride<NCH>();
+    const int4 hdr = a.gen_hdr[k];
+    float acc[NCH];
+#pragma unroll
+    for (int q = 0; q < NCH; ++q) acc[q] = 0.f;
+    generic_runs<DT, NCH>(acc, a, fr, hdr, c0, wave, kWaves);
+#pragma unroll
+    for (int q = 0; q < NCH; ++q) s_part[wl * SS + j + 16 * q] = acc[q];
+    __syncthreads();
+    if (wl == 0) {
+        float sum[NCH];
+#pragma unroll
+        for (int q = 0; q < NCH; ++q) sum[q] = 0.f;
+        for (int g = 0; g < kColWidth; ++g)
+#pragma unroll
+            for (int q = 0; q < NCH; ++q) sum[q] += s_part[g * SS + j + 16 * q];
+        store_row<NCH>(fr.O, (uint32_t(hdr.x) * uint32_t(a.C) + uint32_t(c0 + j)) * 4u, sum,
+                       j + 16 * (NCH - 1) < cn);
+    }
+}
+
+template <int DT, int NCH>
+__global__ __launch_bounds__(kBlock) void k_forward(FwdArgs a) {
+    __shared__ float s_part[kSlots * slot_stride<NCH>()];
+    __shared__ int s_cell[kSlots];
+    const int bx = blockIdx.x, b = blockIdx.y;
+    const int c0 = blockIdx.z * a.slice_c;
+    const int cn = min(a.slice_c, a.C - c0);
+    if (bx < a.n_heavy) {
+        heavy_generic<DT, NCH>(a, Frame(a, b), bx, c0, cn, s_part);
+    } else if (bx < a.base_col) {
+        return;  // padding: column items start on a multiple of 8
+    } else if (bx < a.base_col + a.n_items) {
+        column_item<DT, NCH>(a, Frame(a, b), xcd_remap(bx - a.base_col, a.n_items), c0, cn,
+                             s_part, s_cell);
+    } else if (bx < a.base_zero) {
+        return;
+    } else if (bx < a.base_light) {
+        if (blockIdx.z == 0) zero_rows(a, bx - a.base_zero, b, s_cell);   // whole rows
+    } else {
+        const int k = (bx - a.base_light) * kWaves + int(threadIdx.x >> 6);
+        if (k < a.n_light) light_generic<DT, NCH>(a, Frame(a, b), k, c0, cn);
+    }
 }
 
 template <int DT>
-void launch_dtype(const FwdArgs &a, int grid, int mode, hipStream_t stream) {
-    if (mode == 2) launch<DT, 4, 2>(a, grid, stream);
-    else if (mode == 1) launch<DT, 4, 1>(a, grid, stream);
-    else launch<DT, 1, 1>(a, grid, stream);
+void launch_dtype(const FwdArgs &a, dim3 grid, int nch, hipStream_t s) {
+    switch (nch) {
+        case 1: hipLaunchKernelGGL((k_forward<DT, 1>), grid, dim3(kBlock), 0, s, a); break;
+        case 2: hipLaunchKernelGGL((k_forward<DT, 2>), grid, dim3(kBlock), 0, s, a); break;
+        case 3: hipLaunchKernelGGL((k_forward<DT, 3>), grid, dim3(kBlock), 0, s, a); break;
+        case 4: hipLaunchKernelGGL((k_forward<DT, 4>), grid, dim3(kBlock), 0, s, a); break;
+        default: hipLaunchKernelGGL((k_forward<DT, 5>), grid, dim3(kBlock), 0, s, a); break;
+    }
 }
+
+int round8(int x) { return (x + 7) & ~7; }
 
 }  // namespace
 }  // namespace bevpool
@@ -582,45 +470,63 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
                            int32_t batch, int32_t channels, int32_t dtype, hipStream_t stream) {
     const bevpool_geometry &g = plan->geom;
     const int64_t n_pix = int64_t(g.n_cams) * g.feat_h * g.feat_w;
-    if (n_pix * channels > INT32_MAX || int64_t(plan->n_cells) * channels > INT32_MAX)
+    const int64_t esize = dtype == BEVPOOL_F32 ? 4 : 2;
+    const int64_t p_bytes = plan->n_points * esize;
+    const int64_t f_bytes = n_pix * channels * esize;
+    const int64_t o_bytes = int64_t(plan->n_cells) * channels * 4;
+    const int64_t run_bytes = int64_t(plan->n_runs) * 16;
+    constexpr int64_t kLimit = int64_t(1) << 31;
+    if (p_bytes >= kLimit || f_bytes >= kLimit || o_bytes >= kLimit || run_bytes >= kLimit)
         return bevpool_fail(BEVPOOL_ERR_OVERFLOW,
-                            "channels=%d: pixel or cell rows exceed int32 element offsets", channels);
+                            "channels=%d: one frame's depth (%lld B), feature (%lld B) or BEV "
+                            "(%lld B) tensor reaches 2 GiB", channels, (long long)p_bytes,
+                            (long long)f_bytes, (long long)o_bytes);
+    if (batch > 65535)
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "batch=%d exceeds 65535 frames per call", batch);
 
-    const size_t elem = dtype == BEVPOOL_F32 ? 4 : 2;
-    const bool aligned = channels % 4 == 0 && (reinterpret_cast<uintptr_t>(F) % (4 * elem)) == 0 &&
-                         (reinterpret_cast<uintptr_t>(out) % 16) == 0;
-    // 8 channels per lane when the row splits into whole 8-channel lanes
-    const int mode = !aligned ? 0 : (channels % 8 == 0 ? 2 : 1);
-    const int chunk = aligned ? 4 : 1;
+    const int n_slices = (channels + kSliceChannels - 1) / kSliceChannels;
+    const int slice_c = (channels + n_slices - 1) / n_slices;
+    const int nch = (slice_c + 15) / 16;
 
     FwdArgs a;
-    a.P = P;
-    a.F = F;
+    a.P = static_cast<const char *>(P);
+    a.F = static_cast<const char *>(F);
     a.out = out;
-    a.tile_hdr = plan->tile_hdr;
-    a.tile_cells = plan->tile_cells;
-    a.comp_cell_start = plan->comp_cell_start;
-    a.comp_point = plan->comp_point;
-    a.comp_row = plan->comp_row;
-    a.row_pix = plan->row_pix;
+    a.table = plan->column_table;
+    a.gen_hdr = plan->generic_hdr;
+    a.gen_runs = plan->generic_runs;
     a.empty_cells = plan->empty_cells;
-    a.heavy_tiles = plan->heavy_tiles;
-    a.group_tile_begin = plan->group_tile_begin;
-    a.batch = batch;
-    a.C = channels;
+    a.N = g.n_cams;
+    a.D = g.n_depth;
+    a.H = g.feat_h;
+    a.W = g.feat_w;
+    a.HW = g.feat_h * g.feat_w;
     a.n_cells = plan->n_cells;
-    a.n_points = int32_t(plan->n_points);
-    a.n_pix = int32_t(n_pix);
-    a.n_tiles = plan->n_tiles;
+    a.C = channels;
+    a.slice_c = slice_c;
+    a.p_bytes = uint32_t(p_bytes);
+    a.f_bytes = uint32_t(f_bytes);
+    a.o_bytes = uint32_t(o_bytes);
+    a.run_bytes = uint32_t(run_bytes);
+    a.items_d = (g.n_depth + kColDepth - 1) / kColDepth;
+    a.items_w = (g.feat_w + kColWidth - 1) / kColWidth;
+    a.n_items = g.n_cams * a.items_d * a.items_w;
+    a.n_heavy = plan->n_generic_heavy;
+    a.n_light = plan->n_generic - plan->n_generic_heavy;
     a.n_empty = plan->n_empty;
-    a.n_heavy = plan->n_heavy;
-    a.div_cpr = make_fastdiv(uint32_t((channels + chunk - 1) / chunk));
+    a.base_col = round8(a.n_heavy);
+    a.base_zero = round8(a.base_col + a.n_items);
+    a.base_light = a.base_zero + (a.n_empty + kZeroCells - 1) / kZeroCells;
+    a.zero_vec = (channels % 4 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0) ? 1 : 0;
+    a.zero_units = a.zero_vec ? channels / 4 : channels;
+    a.div_units = make_fastdiv(uint32_t(a.zero_units));
+    const int n_blocks = a.base_light + (a.n_light + kWaves - 1) / kWaves;
 
-    const int grid = kPersistentGroups + plan->n_heavy;
+    const dim3 grid(n_blocks, batch, n_slices);
     switch (dtype) {
-        case BEVPOOL_F32: launch_dtype<BEVPOOL_F32>(a, grid, mode, stream); break;
-        case BEVPOOL_BF16: launch_dtype<BEVPOOL_BF16>(a, grid, mode, stream); break;
-        default: launch_dtype<BEVPOOL_F16>(a, grid, mode, stream); break;
+        case BEVPOOL_F32: launch_dtype<BEVPOOL_F32>(a, grid, nch, stream); break;
+        case BEVPOOL_BF16: launch_dtype<BEVPOOL_BF16>(a, grid, nch, stream); break;
+        default: launch_dtype<BEVPOOL_F16>(a, grid, nch, stream); break;
     }
     BEVPOOL_HIP(hipGetLastError());
     return BEVPOOL_OK;

@@ -10,36 +10,36 @@ namespace bevpool {
 
 // Work partition of the forward pass.
 //
-// Cells with points are grouped into tiles along the camera rays. A cell's
-// key is (camera, feature column / kKeyCols, depth bin / kKeyBins) of its
-// lowest-id point. Cells with one key lie along a short bundle of
-// neighbouring rays, so their points share few distinct feature rows; each
-// row is reused about once per depth bin the bundle spends in the tile. A
-// key group becomes one tile, unless it has more than kPointBudget points or
-// kMaxTileCells cells. Then it is cut where its running point count crosses
-// a multiple of kPointBudget / 2, around every cell with more than
-// kPointBudget / 2 points, and every kMaxTileCells cells. So a tile holds
-// at most kPointBudget points, except a tile that is one heavier cell.
-// One workgroup serves each tile. It stages the tile's distinct feature
-// rows in LDS once, and every point reads its row from there.
+// A frustum point is (camera n, depth bin d, pixel row h, pixel column w).
+// A "combo" is one (n, d, w): a column of H points on one depth plane. A
+// combo is clean when all its kept points lie in one cell and their rows
+// form one range h_lo..h_hi-1. A level camera makes almost every combo
+// clean, since its rows then differ only in height.
 //
-// The forward kernel runs kPersistentGroups workgroups of kPersistentWaves
-// waves, one per CU. Each owns a contiguous run of tiles of about equal cost
-// and a share of the cells without points, which it zeroes. A tile heavier
-// than kPointBudget (one cell) gets an extra workgroup of its own.
+// The points are split over column items of kColDepth depth bins x
+// kColWidth pixel columns of one camera. A cell is "column-served" when
+// all its points come from clean combos inside one item. Such a cell is
+// computed by that item's workgroup: the workgroup reads each feature row
+// (n, h, w) of its columns once and applies it to the kColDepth depth bins
+// held in registers. A cell fed by a single combo is stored from
+// registers; a cell fed by several combos of the item is summed through
+// LDS. Every other cell with points is "generic": its points are gathered
+// in runs of consecutive depth bins of one pixel. A generic cell gets one
+// wave, or a whole workgroup when it has more than kGenHeavy points. Cells
+// without points are zeroed by workgroups of their own.
 constexpr int kWaveSize = 64;
-constexpr int kWaves = 4;                                  // plan kernels, heavy tiles
-constexpr int kBlock = kWaves * kWaveSize;
-constexpr int kPersistentGroups = 256;
-constexpr int kPersistentWaves = 8;
-constexpr int kPersistentBlock = kPersistentWaves * kWaveSize;
-constexpr int kKeyCols = 4;
-constexpr int kKeyBins = 8;
-constexpr int kPointBudget = 2048;
-constexpr int kMaxTileCells = 256;
-constexpr int kStagePerThread = kPointBudget / kBlock;     // 8
-constexpr int kFeatureLdsBytes = 56 * 1024;                // staged feature slab
-static_assert(kPointBudget % kBlock == 0, "staging loop assumes whole rounds");
+constexpr int kWaves = 4;
+constexpr int kBlock = kWaves * kWaveSize;      // plan kernels and the forward kernel
+constexpr int kGroupLanes = 16;                 // lanes per pixel column (one DPP row)
+constexpr int kColDepth = 8;
+constexpr int kColWidth = kBlock / kGroupLanes; // 16 columns per item
+constexpr int kGenHeavy = 256;
+constexpr int kSliceChannels = 80;              // channels per pass (LDS partials)
+
+// Column-table entry flags (second word: h_lo | h_hi << 16 | flags).
+constexpr uint32_t kComboMulti = 1u << 31;      // the cell has other combos
+constexpr uint32_t kComboOwner = 1u << 30;      // first combo of a multi cell
+constexpr int kMaxFeatH = 1 << 14;              // rows must fit the 15-bit fields
 
 // Unsigned division by a run-time constant through a multiply-high, after
 // Granlund and Montgomery, "Division by invariant integers using
@@ -68,23 +68,17 @@ struct bevpool_plan_s {
     int device;
     bevpool_geometry geom;
     int64_t n_points, n_kept;
-    int32_t n_cells, n_nonempty, max_per_cell, n_tiles, n_rows, n_empty, n_heavy;
+    int32_t n_cells, n_nonempty, max_per_cell;
+    int32_t n_column, n_generic, n_generic_heavy, n_runs, n_empty;
     // canonical association (exported)
     int32_t *cell_of_point;  // [n_points]
     int32_t *sorted_point;   // [n_points]: kept ids by (cell, id), then dropped ids
     int32_t *cell_start;     // [n_cells + 1]
-    // forward work partition, all in tile order
-    int32_t *tile_cell_begin;  // [n_tiles + 1] into tile_cells / comp_cell_start
-    int32_t *tile_row_begin;   // [n_tiles + 1] into row_pix
-    int32_t *tile_cells;       // [n_nonempty] cells with points, tile by tile, id order inside
-    int32_t *comp_cell_start;  // [n_nonempty + 1] first point (in comp order) of each listed cell
-    int32_t *empty_cells;      // [n_empty] cells without points, in id order
-    int32_t *tile_hdr;         // [n_tiles][8]: cell begin, cells, point begin, points, row begin, rows
-    int32_t *heavy_tiles;      // [n_heavy] tiles with more than kPointBudget points
-    int32_t *group_tile_begin; // [kPersistentGroups + 1] tile run of each persistent workgroup
-    int32_t *comp_point;       // [n_kept] point ids, tile by tile, cell by cell, id order
-    int32_t *comp_row;         // [n_kept] the point's feature row, relative to its tile
-    int32_t *row_pix;          // [n_rows] pixel (n*H*W + h*W + w) of each staged row
+    // forward work partition
+    int2 *column_table;      // [N][D][W]: {cell or -1, h_lo | h_hi << 16 | flags}
+    int4 *generic_hdr;       // [n_generic]: {cell, first run, runs, points}, most points first
+    int4 *generic_runs;      // [n_runs]: {first point id, pixel, depth bins, 0}
+    int32_t *empty_cells;    // [n_empty] cells without points, ascending
 };
 
 constexpr uint32_t kPlanMagic = 0xB3F9001Du;

@@ -10,7 +10,9 @@
 //   k_radix_scatter}
 //   k_cell_start   interval table from the sorted keys
 //   k_cell_stats   non-empty cells and the largest interval
-//   k_cell_keys ... k_rows   ray-aligned work partition of the forward pass
+//   k_combo_walk ... k_generic_runs   work partition of the forward pass:
+//                  clean combos, the column table, generic cells and their
+//                  runs, empty cells
 //
 // The geometry is evaluated in IEEE double with the file built without
 // floating-point contraction, in one fixed expression order, so the cell ids
@@ -254,224 +256,184 @@ __global__ __launch_bounds__(kBlock) void k_cell_stats(const int32_t *cell_start
 
 // ---------------------------------------------------------------- work partition
 //
-// Ray-aligned tiles (see the constants in internal.h). Rows: a point starts
-// a new staged row of its tile when the previous depth bin of its pixel is
-// dropped or lies in another tile. Every later point of the same run reads
-// that row. If a ray leaves a tile and comes back, the pixel is staged twice;
-// that wastes one LDS row and changes nothing else.
+// Combos, items and cell classes as described in internal.h. Every kernel
+// below is a plain per-element pass; ordering comes from scans and the
+// stable radix sort only, so the partition is deterministic.
 
-struct KeyArgs {
-    const int32_t *cell_start, *sorted_point;
-    int32_t n_cells, HW, W, D, key_cols, key_bins;
-    uint32_t *key;            // [n_cells]
-    int32_t *nonempty_flag;   // [n_cells + 1]
-    int32_t *empty_flag;      // [n_cells + 1]
+__global__ __launch_bounds__(kBlock) void k_fill(int32_t *p, int64_t n, int32_t v) {
+    const int64_t i = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+struct ComboArgs {
+    const int32_t *cell_of_point;
+    int32_t N, D, H, W, items_d, items_w;
+    int32_t allow_clean;        // 0 when rows do not fit the packed row range
+    int32_t *combo_cell;        // [N*D*W]: cell of a clean combo, -1 none kept, -2 not clean
+    int32_t *combo_range;       // [N*D*W]: h_lo | h_hi << 16
+    int32_t *cell_generic;      // [n_cells]: 1 if a combo that is not clean touches the cell
+    int32_t *cell_ncombo;       // [n_cells]: clean combos of the cell
+    int32_t *cell_item_min, *cell_item_max, *cell_first;
 };
 
-__global__ __launch_bounds__(kBlock) void k_cell_keys(KeyArgs a) {
-    const int32_t c = blockIdx.x * kBlock + threadIdx.x;
-    if (c >= a.n_cells) return;
-    const int32_t cnt = a.cell_start[c + 1] - a.cell_start[c];
-    a.nonempty_flag[c] = cnt > 0 ? 1 : 0;
-    a.empty_flag[c] = cnt > 0 ? 0 : 1;
-    if (cnt == 0) return;
-    const int32_t p0 = a.sorted_point[a.cell_start[c]];  // the cell's lowest point id
-    const int32_t q = p0 / a.HW;                          // n * D + d
-    const int32_t n = q / a.D, d = q - n * a.D;
-    const int32_t w = p0 % a.W;
-    a.key[c] = uint32_t((n * a.key_cols + w / kKeyCols) * a.key_bins + d / kKeyBins);
-}
-
-__global__ __launch_bounds__(kBlock) void k_compact_cells(const int32_t *cell_start, int32_t n_cells,
-                                                          const uint32_t *key,
-                                                          const int32_t *nonempty_pos,
-                                                          const int32_t *empty_pos,
-                                                          uint32_t *ne_key, int32_t *ne_cell,
-                                                          int32_t *empty_cells) {
-    const int32_t c = blockIdx.x * kBlock + threadIdx.x;
-    if (c >= n_cells) return;
-    if (cell_start[c + 1] > cell_start[c]) {
-        ne_key[nonempty_pos[c]] = key[c];
-        ne_cell[nonempty_pos[c]] = c;
-    } else {
-        empty_cells[empty_pos[c]] = c;
+// One thread per combo walks its H rows.
+__global__ __launch_bounds__(kBlock) void k_combo_walk(ComboArgs a) {
+    const int64_t x = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    const int64_t n_combo = int64_t(a.N) * a.D * a.W;
+    if (x >= n_combo) return;
+    const int32_t X = int32_t(x);
+    const int32_t w = X % a.W, nd = X / a.W;
+    const int32_t d = nd % a.D, n = nd / a.D;
+    const int64_t base = int64_t(nd) * a.H * a.W + w;
+    int32_t c0 = -1, hlo = -1, hlast = -1, kept = 0;
+    bool one_cell = true;
+    for (int32_t h = 0; h < a.H; ++h) {
+        const int32_t c = a.cell_of_point[base + int64_t(h) * a.W];
+        if (c < 0) continue;
+        if (kept == 0) {
+            c0 = c;
+            hlo = h;
+        } else if (c != c0) {
+            one_cell = false;
+        }
+        hlast = h;
+        ++kept;
     }
-}
-
-// point count of each listed cell, and each cell's position in tile order
-__global__ __launch_bounds__(kBlock) void k_listed_counts(const int32_t *listed_cell, int32_t n,
-                                                          const int32_t *cell_start,
-                                                          int32_t *count_at, int32_t *pos_of_cell) {
-    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
-    if (i >= n) return;
-    const int32_t c = listed_cell[i];
-    count_at[i] = cell_start[c + 1] - cell_start[c];
-    pos_of_cell[c] = i;
-}
-
-__global__ __launch_bounds__(kBlock) void k_group_flags(const uint32_t *key, int32_t n,
-                                                        int32_t *flag) {
-    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
-    if (i < n) flag[i] = (i == 0 || key[i] != key[i - 1]) ? 1 : 0;
-}
-
-// first listed position of each group (scan = exclusive scan of the flags)
-__global__ __launch_bounds__(kBlock) void k_group_first(const int32_t *scan, int32_t n,
-                                                        int32_t *group_first) {
-    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
-    if (i > n) return;
-    if (i == n) group_first[scan[n]] = n;
-    else if (scan[i + 1] != scan[i]) group_first[scan[i]] = i;
-}
-
-struct TileFlagArgs {
-    const int32_t *group_scan, *group_first, *X;  // X: exclusive scan of the counts
-    int32_t n;
-    int32_t *flag;
-};
-
-__global__ __launch_bounds__(kBlock) void k_tile_flags(TileFlagArgs a) {
-    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
-    if (i >= a.n) return;
-    const int32_t g = a.group_scan[i + 1] - 1;
-    const int32_t gf = a.group_first[g];
-    const int32_t total = a.X[a.group_first[g + 1]] - a.X[gf];
-    constexpr int32_t S = kPointBudget / 2;
-    bool start = (i == gf) || ((i - gf) % kMaxTileCells == 0);
-    if (!start && total > kPointBudget) {
-        const int32_t here = a.X[i] - a.X[gf], prev = a.X[i - 1] - a.X[gf];
-        const int32_t n_here = a.X[i + 1] - a.X[i], n_prev = a.X[i] - a.X[i - 1];
-        start = (here / S != prev / S) || n_here > S || n_prev > S;
-    }
-    a.flag[i] = start ? 1 : 0;
-}
-
-// tile_cell_begin[t] = first listed position of tile t; tile_of_cell per cell
-__global__ __launch_bounds__(kBlock) void k_tile_emit(const int32_t *tile_scan, int32_t n,
-                                                      const int32_t *listed_cell,
-                                                      int32_t *tile_cell_begin,
-                                                      int32_t *tile_of_cell) {
-    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
-    if (i > n) return;
-    if (i == n) {
-        tile_cell_begin[tile_scan[n]] = n;
+    if (kept == 0) {
+        a.combo_cell[X] = -1;
+        a.combo_range[X] = 0;
         return;
     }
-    if (tile_scan[i + 1] != tile_scan[i]) tile_cell_begin[tile_scan[i]] = i;
-    tile_of_cell[listed_cell[i]] = tile_scan[i + 1] - 1;
+    const bool clean = a.allow_clean && one_cell && kept == hlast - hlo + 1;
+    if (clean) {
+        const int32_t item = (n * a.items_d + d / kColDepth) * a.items_w + w / kColWidth;
+        a.combo_cell[X] = c0;
+        a.combo_range[X] = hlo | ((hlast + 1) << 16);
+        atomicAdd(&a.cell_ncombo[c0], 1);
+        atomicMin(&a.cell_item_min[c0], item);
+        atomicMax(&a.cell_item_max[c0], item);
+        atomicMin(&a.cell_first[c0], X);
+    } else {
+        a.combo_cell[X] = -2;
+        a.combo_range[X] = 0;
+        for (int32_t h = hlo; h <= hlast; ++h) {
+            const int32_t c = a.cell_of_point[base + int64_t(h) * a.W];
+            if (c >= 0) atomicOr(&a.cell_generic[c], 1);
+        }
+    }
 }
 
-// Points in tile order: a cell's run of the canonical order moves as a block.
-__global__ __launch_bounds__(kBlock) void k_comp_points(const int32_t *sorted_point, int32_t n_kept,
-                                                        const int32_t *cell_of_point,
-                                                        const int32_t *cell_start,
-                                                        const int32_t *pos_of_cell,
-                                                        const int32_t *comp_cell_start,
-                                                        int32_t *comp_point, int32_t *pos_of_point) {
-    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
-    if (i >= n_kept) return;
-    const int32_t p = sorted_point[i];
-    const int32_t c = cell_of_point[p];
-    const int32_t ci = comp_cell_start[pos_of_cell[c]] + (i - cell_start[c]);
-    comp_point[ci] = p;
-    pos_of_point[p] = ci;
+__device__ __forceinline__ bool column_served(const ComboArgs &a, int32_t c) {
+    return a.cell_generic[c] == 0 && a.cell_item_min[c] == a.cell_item_max[c];
 }
 
-// 1 where a point starts a run of its pixel inside its tile
-__global__ __launch_bounds__(kBlock) void k_run_flags(const int32_t *comp_point, int32_t n_kept,
+// Per cell: generic flag, empty flag; counters[0] += served, counters[1] +=
+// heavy generic.
+__global__ __launch_bounds__(kBlock) void k_cell_class(ComboArgs a, const int32_t *cell_start,
+                                                       int32_t n_cells, int32_t *generic_flag,
+                                                       int32_t *empty_flag, int32_t *counters) {
+    const int32_t c = blockIdx.x * kBlock + threadIdx.x;
+    if (c >= n_cells) return;
+    const int32_t cnt = cell_start[c + 1] - cell_start[c];
+    const bool served = cnt > 0 && column_served(a, c);
+    generic_flag[c] = (cnt > 0 && !served) ? 1 : 0;
+    empty_flag[c] = cnt == 0 ? 1 : 0;
+    if (served) atomicAdd(&counters[0], 1);
+    if (cnt > kGenHeavy && !served) atomicAdd(&counters[1], 1);
+}
+
+__global__ __launch_bounds__(kBlock) void k_combo_table(ComboArgs a, int2 *table) {
+    const int64_t x = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    if (x >= int64_t(a.N) * a.D * a.W) return;
+    const int32_t X = int32_t(x);
+    const int32_t c = a.combo_cell[X];
+    int2 e = make_int2(-1, 0);
+    if (c >= 0 && column_served(a, c)) {
+        uint32_t y = uint32_t(a.combo_range[X]);
+        if (a.cell_ncombo[c] > 1) y |= kComboMulti;
+        if (a.cell_first[c] == X) y |= kComboOwner;
+        e = make_int2(c, int32_t(y));
+    }
+    table[X] = e;
+}
+
+// Generic cells keyed for a descending sort by point count; empty cells
+// listed in ascending order.
+__global__ __launch_bounds__(kBlock) void k_compact_classes(const int32_t *cell_start, int32_t n_cells,
+                                                            const int32_t *generic_pos,
+                                                            const int32_t *empty_pos,
+                                                            int32_t max_per_cell, uint32_t *gen_key,
+                                                            int32_t *gen_cell, int32_t *empty_cells) {
+    const int32_t c = blockIdx.x * kBlock + threadIdx.x;
+    if (c >= n_cells) return;
+    const int32_t cnt = cell_start[c + 1] - cell_start[c];
+    if (generic_pos[c + 1] != generic_pos[c]) {
+        gen_key[generic_pos[c]] = uint32_t(max_per_cell - cnt);
+        gen_cell[generic_pos[c]] = c;
+    }
+    if (empty_pos[c + 1] != empty_pos[c]) empty_cells[empty_pos[c]] = c;
+}
+
+// 1 where a kept point of a generic cell starts a run: its previous depth
+// bin (same pixel) is not a point of the same cell.
+__global__ __launch_bounds__(kBlock) void k_run_flags(const int32_t *sorted_point, int32_t n_kept,
                                                       const int32_t *cell_of_point,
-                                                      const int32_t *tile_of_cell, int32_t HW,
+                                                      const int32_t *generic_pos, int32_t HW,
                                                       FastDiv div_hw, FastDiv div_d, int32_t D,
                                                       int32_t *flag) {
     const int32_t i = blockIdx.x * kBlock + threadIdx.x;
     if (i >= n_kept) return;
-    const int32_t p = comp_point[i];
+    const int32_t p = sorted_point[i];
+    const int32_t c = cell_of_point[p];
+    const bool generic = generic_pos[c + 1] != generic_pos[c];
     const uint32_t q = fdiv(uint32_t(p), div_hw);
     const int32_t d = int32_t(q) - int32_t(fdiv(q, div_d)) * D;
-    const int32_t prev = d > 0 ? cell_of_point[p - HW] : -1;
-    flag[i] = (prev < 0 || tile_of_cell[prev] != tile_of_cell[cell_of_point[p]]) ? 1 : 0;
+    flag[i] = (generic && (d == 0 || cell_of_point[p - HW] != c)) ? 1 : 0;
 }
 
-__global__ __launch_bounds__(kBlock) void k_tile_row_begin(const int32_t *tile_cell_begin,
-                                                           const int32_t *comp_cell_start,
-                                                           const int32_t *row_scan, int32_t n_tiles,
-                                                           int32_t *tile_row_begin) {
-    const int32_t t = blockIdx.x * kBlock + threadIdx.x;
-    if (t <= n_tiles) tile_row_begin[t] = row_scan[comp_cell_start[tile_cell_begin[t]]];
+// Runs per listed generic cell, and each cell's list position.
+__global__ __launch_bounds__(kBlock) void k_generic_counts(const int32_t *gen_cell, int32_t n_gen,
+                                                           const int32_t *cell_start,
+                                                           const int32_t *run_scan,
+                                                           int32_t *runs_of, int32_t *pos_of_cell) {
+    const int32_t k = blockIdx.x * kBlock + threadIdx.x;
+    if (k >= n_gen) return;
+    const int32_t c = gen_cell[k];
+    runs_of[k] = run_scan[cell_start[c + 1]] - run_scan[cell_start[c]];
+    pos_of_cell[c] = k;
 }
 
-// One thread per pixel walks its depth bins in order, names the staged row
-// of each run and gives every point its row relative to its tile.
-__global__ __launch_bounds__(kBlock) void k_rows(const int32_t *cell_of_point,
-                                                 const int32_t *pos_of_point,
-                                                 const int32_t *tile_of_cell,
-                                                 const int32_t *row_scan,
-                                                 const int32_t *tile_row_begin, int32_t n_pix,
-                                                 int32_t HW, int32_t D, int32_t *row_pix,
-                                                 int32_t *comp_row) {
-    const int32_t pixel = blockIdx.x * kBlock + threadIdx.x;
-    if (pixel >= n_pix) return;
-    const int32_t n = pixel / HW, hw = pixel - n * HW;
-    int32_t row = 0;
-    for (int32_t d = 0; d < D; ++d) {
-        const int32_t p = (n * D + d) * HW + hw;
-        const int32_t c = cell_of_point[p];
-        if (c < 0) continue;
-        const int32_t i = pos_of_point[p];
-        if (row_scan[i + 1] != row_scan[i]) {
-            row = row_scan[i];
-            row_pix[row] = pixel;
-        }
-        comp_row[i] = row - tile_row_begin[tile_of_cell[c]];
-    }
+__global__ __launch_bounds__(kBlock) void k_generic_hdr(const int32_t *gen_cell, int32_t n_gen,
+                                                        const int32_t *cell_start,
+                                                        const int32_t *run_begin, int4 *hdr) {
+    const int32_t k = blockIdx.x * kBlock + threadIdx.x;
+    if (k >= n_gen) return;
+    const int32_t c = gen_cell[k];
+    hdr[k] = make_int4(c, run_begin[k], run_begin[k + 1] - run_begin[k],
+                       cell_start[c + 1] - cell_start[c]);
 }
 
-// Per-tile header, heavy flag and cost (for splitting tiles over the
-// persistent workgroups): points, plus rows and cells, which also cost time.
-__global__ __launch_bounds__(kBlock) void k_tile_headers(const int32_t *tile_cell_begin,
-                                                         const int32_t *tile_row_begin,
-                                                         const int32_t *comp_cell_start,
-                                                         int32_t n_tiles, int32_t *hdr,
-                                                         int32_t *heavy_flag, int32_t *cost) {
-    const int32_t t = blockIdx.x * kBlock + threadIdx.x;
-    if (t >= n_tiles) return;
-    const int32_t tcb = tile_cell_begin[t], ncell = tile_cell_begin[t + 1] - tcb;
-    const int32_t tpb = comp_cell_start[tcb], npts = comp_cell_start[tcb + ncell] - tpb;
-    const int32_t trb = tile_row_begin[t], nrows = tile_row_begin[t + 1] - trb;
-    int32_t *h = hdr + 8 * int64_t(t);
-    h[0] = tcb;
-    h[1] = ncell;
-    h[2] = tpb;
-    h[3] = npts;
-    h[4] = trb;
-    h[5] = nrows;
-    h[6] = 0;
-    h[7] = 0;
-    const bool heavy = npts > kPointBudget;
-    heavy_flag[t] = heavy ? 1 : 0;
-    cost[t] = heavy ? 0 : npts + 2 * nrows + 4 * ncell + 64;
-}
-
-__global__ __launch_bounds__(kBlock) void k_heavy_list(const int32_t *heavy_scan, int32_t n_tiles,
-                                                       int32_t *heavy_tiles) {
-    const int32_t t = blockIdx.x * kBlock + threadIdx.x;
-    if (t < n_tiles && heavy_scan[t + 1] != heavy_scan[t]) heavy_tiles[heavy_scan[t]] = t;
-}
-
-// group_tile_begin[w] = first tile whose running cost reaches w/G of the total
-__global__ __launch_bounds__(kBlock) void k_group_ranges(const int32_t *cost_scan, int32_t n_tiles,
-                                                         int32_t *group_tile_begin) {
-    const int32_t w = blockIdx.x * kBlock + threadIdx.x;
-    if (w > kPersistentGroups) return;
-    const int64_t total = cost_scan[n_tiles];
-    const int64_t target = total * w / kPersistentGroups;
-    int32_t lo = 0, hi = n_tiles;  // first t with cost_scan[t] >= target
-    while (lo < hi) {
-        const int32_t mid = (lo + hi) >> 1;
-        if (cost_scan[mid] < target) lo = mid + 1;
-        else hi = mid;
-    }
-    group_tile_begin[w] = (w == kPersistentGroups) ? n_tiles : lo;
+// One thread per run start: the run's record, at its place in list order.
+__global__ __launch_bounds__(kBlock) void k_generic_runs(const int32_t *sorted_point, int32_t n_kept,
+                                                         const int32_t *cell_of_point,
+                                                         const int32_t *cell_start,
+                                                         const int32_t *run_scan,
+                                                         const int32_t *pos_of_cell,
+                                                         const int32_t *run_begin, int32_t HW,
+                                                         int32_t D, FastDiv div_hw, FastDiv div_d,
+                                                         int4 *runs) {
+    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+    if (i >= n_kept || run_scan[i + 1] == run_scan[i]) return;
+    const int32_t p = sorted_point[i];
+    const int32_t c = cell_of_point[p];
+    const uint32_t q = fdiv(uint32_t(p), div_hw);           // n * D + d
+    const int32_t n = int32_t(fdiv(q, div_d));
+    const int32_t d = int32_t(q) - n * D;
+    const int32_t pixel = n * HW + (p - int32_t(q) * HW);
+    int32_t len = 1;
+    while (d + len < D && cell_of_point[p + len * HW] == c) ++len;
+    const int32_t r = run_begin[pos_of_cell[c]] + (run_scan[i] - run_scan[cell_start[c]]);
+    runs[r] = make_int4(p, pixel, len, 0);
 }
 
 int blocks_for(int64_t n) { return int((n + kBlock - 1) / kBlock); }
@@ -505,8 +467,9 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
     const int64_t np64 = int64_t(g.n_cams) * g.n_depth * g.feat_h * g.feat_w;
     const int32_t np = int32_t(np64);
     const int32_t n_cells = g.nx * g.ny;
-    const int32_t HW = g.feat_h * g.feat_w;
-    const int32_t n_pix = g.n_cams * HW;
+    const int32_t N = g.n_cams, D = g.n_depth, H = g.feat_h, W = g.feat_w;
+    const int32_t HW = H * W;
+    const int64_t n_combo = int64_t(N) * D * W;
     plan->n_points = np64;
     plan->n_cells = n_cells;
 
@@ -514,33 +477,28 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
     if ((rc = dev_alloc(&plan->cell_of_point, size_t(np), "cell_of_point"))) return rc;
     if ((rc = dev_alloc(&plan->sorted_point, size_t(np), "sorted_point"))) return rc;
     if ((rc = dev_alloc(&plan->cell_start, size_t(n_cells) + 1, "cell_start"))) return rc;
+    if ((rc = dev_alloc(&plan->column_table, size_t(n_combo), "column_table"))) return rc;
 
     // temporaries, freed on every exit path below
     const int64_t sort_cap = np64 > n_cells ? np64 : int64_t(n_cells);
     const int sort_tiles_cap = int((sort_cap + kSortTile - 1) / kSortTile);
     double *d_calib = nullptr;
-    uint32_t *keys_a = nullptr, *keys_b = nullptr, *cell_key = nullptr;
-    int32_t *vals_b = nullptr, *hist = nullptr, *small = nullptr;
-    int32_t *flag_a = nullptr, *flag_b = nullptr, *group_first = nullptr;
-    int32_t *tile_of_cell = nullptr, *pos_of_cell = nullptr, *pos_of_point = nullptr;
-    int32_t *row_scan = nullptr;
+    uint32_t *keys_a = nullptr, *keys_b = nullptr;
+    int32_t *vals_a = nullptr, *vals_b = nullptr, *hist = nullptr, *small = nullptr;
+    int32_t *flag_a = nullptr, *flag_b = nullptr;
+    int32_t *combo_cell = nullptr, *combo_range = nullptr, *cell_generic = nullptr;
+    int32_t *cell_ncombo = nullptr, *cell_item_min = nullptr, *cell_item_max = nullptr;
+    int32_t *cell_first = nullptr, *run_scan = nullptr, *run_begin = nullptr;
+    int32_t *pos_of_cell = nullptr;
     auto cleanup = [&]() {
-        (void)hipFree(d_calib);
-        (void)hipFree(keys_a);
-        (void)hipFree(keys_b);
-        (void)hipFree(cell_key);
-        (void)hipFree(vals_b);
-        (void)hipFree(hist);
-        (void)hipFree(small);
-        (void)hipFree(flag_a);
-        (void)hipFree(flag_b);
-        (void)hipFree(group_first);
-        (void)hipFree(tile_of_cell);
-        (void)hipFree(pos_of_cell);
-        (void)hipFree(pos_of_point);
-        (void)hipFree(row_scan);
+        for (void *q : {(void *)d_calib, (void *)keys_a, (void *)keys_b, (void *)vals_a,
+                        (void *)vals_b, (void *)hist, (void *)small, (void *)flag_a,
+                        (void *)flag_b, (void *)combo_cell, (void *)combo_range,
+                        (void *)cell_generic, (void *)cell_ncombo, (void *)cell_item_min,
+                        (void *)cell_item_max, (void *)cell_first, (void *)run_scan,
+                        (void *)run_begin, (void *)pos_of_cell})
+            (void)hipFree(q);
     };
-    auto launch_ok = [](int64_t n) { return n > 0; };
 
     // stable LSD radix sort of (keys, vals)[0, n) on the low `bits` bits; the
     // result ends in (keys, vals)
@@ -549,7 +507,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         const int tiles = int((int64_t(n) + kSortTile - 1) / kSortTile);
         const int passes = (bits + 7) / 8;
         uint32_t *kin = keys, *kout = keys == keys_a ? keys_b : keys_a;
-        int32_t *vin = vals, *vout = vals_b;
+        int32_t *vin = vals, *vout = vals == vals_b ? vals_a : vals_b;
         for (int pass = 0; pass < passes; ++pass) {
             const int shift = 8 * pass;
             hipLaunchKernelGGL(k_radix_hist, dim3(tiles), dim3(kBlock), 0, stream, kin, n, shift, hist);
@@ -574,36 +532,41 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         while ((int64_t(1) << b) <= max_key) ++b;
         return b;
     };
+    auto fill = [&](int32_t *p, int64_t n, int32_t v) {
+        if (n > 0) hipLaunchKernelGGL(k_fill, dim3(blocks_for(n)), dim3(kBlock), 0, stream, p, n, v);
+    };
+    auto to_host = [&](int32_t *dst, const int32_t *src) -> int {
+        BEVPOOL_HIP(hipMemcpyAsync(dst, src, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
+        return BEVPOOL_OK;
+    };
 
     auto run = [&]() -> int {
         int rc2;
         if ((rc2 = dev_alloc(&d_calib, size_t(g.n_cams) * 16, "calibration"))) return rc2;
         if ((rc2 = dev_alloc(&keys_a, size_t(sort_cap), "sort keys"))) return rc2;
         if ((rc2 = dev_alloc(&keys_b, size_t(sort_cap), "sort keys"))) return rc2;
+        if ((rc2 = dev_alloc(&vals_a, size_t(sort_cap), "sort values"))) return rc2;
         if ((rc2 = dev_alloc(&vals_b, size_t(sort_cap), "sort values"))) return rc2;
-        if ((rc2 = dev_alloc(&cell_key, size_t(n_cells), "cell keys"))) return rc2;
         if ((rc2 = dev_alloc(&hist, size_t(sort_tiles_cap) * 256, "radix histogram"))) return rc2;
-        if ((rc2 = dev_alloc(&small, 4, "plan counters"))) return rc2;
+        if ((rc2 = dev_alloc(&small, 8, "plan counters"))) return rc2;
         if ((rc2 = dev_alloc(&flag_a, size_t(n_cells) + 1, "flags"))) return rc2;
         if ((rc2 = dev_alloc(&flag_b, size_t(n_cells) + 1, "flags"))) return rc2;
-        if ((rc2 = dev_alloc(&group_first, size_t(n_cells) + 1, "group starts"))) return rc2;
-        if ((rc2 = dev_alloc(&tile_of_cell, size_t(n_cells), "tile of cell"))) return rc2;
-        if ((rc2 = dev_alloc(&pos_of_cell, size_t(n_cells), "cell positions"))) return rc2;
-        if ((rc2 = dev_alloc(&pos_of_point, size_t(np), "point positions"))) return rc2;
 
         BEVPOOL_HIP(hipMemcpyAsync(d_calib, intrinsics, sizeof(double) * 4 * g.n_cams,
                                    hipMemcpyHostToDevice, stream));
         BEVPOOL_HIP(hipMemcpyAsync(d_calib + 4 * g.n_cams, extrinsics,
                                    sizeof(double) * 12 * g.n_cams, hipMemcpyHostToDevice, stream));
-        BEVPOOL_HIP(hipMemsetAsync(small, 0, 4 * sizeof(int32_t), stream));
+        fill(small, 8, 0);
 
+        // Sec. III-B, precomputation: cell of every point, then the points
+        // sorted by (cell, id) and the interval table.
         ProjectArgs pa;
         pa.intr = d_calib;
         pa.extr = d_calib + 4 * g.n_cams;
         pa.g = g;
-        pa.div_w = make_fastdiv(uint32_t(g.feat_w));
-        pa.div_h = make_fastdiv(uint32_t(g.feat_h));
-        pa.div_d = make_fastdiv(uint32_t(g.n_depth));
+        pa.div_w = make_fastdiv(uint32_t(W));
+        pa.div_h = make_fastdiv(uint32_t(H));
+        pa.div_d = make_fastdiv(uint32_t(D));
         pa.n_points = np;
         pa.n_cells = n_cells;
         pa.cell_of_point = plan->cell_of_point;
@@ -611,155 +574,109 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         pa.vals = plan->sorted_point;
         hipLaunchKernelGGL(k_project, dim3(blocks_for(np)), dim3(kBlock), 0, stream, pa);
         BEVPOOL_HIP(hipGetLastError());
-
-        // canonical order: points by (cell, id); dropped points last
         if ((rc2 = radix_sort(keys_a, plan->sorted_point, np, bits_for(n_cells)))) return rc2;
         hipLaunchKernelGGL(k_cell_start, dim3(blocks_for(int64_t(np) + 1)), dim3(kBlock), 0,
                            stream, keys_a, np, n_cells, plan->cell_start);
         hipLaunchKernelGGL(k_cell_stats, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream,
                            plan->cell_start, n_cells, small);
-
-        // cells with points, keyed along the rays; cells without points listed
-        const int32_t key_cols = (g.feat_w + kKeyCols - 1) / kKeyCols;
-        const int32_t key_bins = (g.n_depth + kKeyBins - 1) / kKeyBins;
-        KeyArgs ka;
-        ka.cell_start = plan->cell_start;
-        ka.sorted_point = plan->sorted_point;
-        ka.n_cells = n_cells;
-        ka.HW = HW;
-        ka.W = g.feat_w;
-        ka.D = g.n_depth;
-        ka.key_cols = key_cols;
-        ka.key_bins = key_bins;
-        ka.key = cell_key;
-        ka.nonempty_flag = flag_a;
-        ka.empty_flag = flag_b;
-        BEVPOOL_HIP(hipMemsetAsync(flag_a, 0, sizeof(int32_t) * (size_t(n_cells) + 1), stream));
-        BEVPOOL_HIP(hipMemsetAsync(flag_b, 0, sizeof(int32_t) * (size_t(n_cells) + 1), stream));
-        hipLaunchKernelGGL(k_cell_keys, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream, ka);
-        scan_with_total(flag_a, n_cells, small + 3, stream);
-        scan_with_total(flag_b, n_cells, small + 3, stream);
         BEVPOOL_HIP(hipGetLastError());
-        int32_t host[2], counts2[2];
-        BEVPOOL_HIP(hipMemcpyAsync(host, small, sizeof(host), hipMemcpyDeviceToHost, stream));
-        BEVPOOL_HIP(hipMemcpyAsync(&counts2[0], flag_a + n_cells, sizeof(int32_t),
-                                   hipMemcpyDeviceToHost, stream));
-        BEVPOOL_HIP(hipMemcpyAsync(&counts2[1], flag_b + n_cells, sizeof(int32_t),
-                                   hipMemcpyDeviceToHost, stream));
-        int32_t kept;
-        BEVPOOL_HIP(hipMemcpyAsync(&kept, plan->cell_start + n_cells, sizeof(kept),
-                                   hipMemcpyDeviceToHost, stream));
+
+        // combos, cell classes and the column table
+        if ((rc2 = dev_alloc(&combo_cell, size_t(n_combo), "combo cells"))) return rc2;
+        if ((rc2 = dev_alloc(&combo_range, size_t(n_combo), "combo ranges"))) return rc2;
+        if ((rc2 = dev_alloc(&cell_generic, size_t(n_cells), "cell classes"))) return rc2;
+        if ((rc2 = dev_alloc(&cell_ncombo, size_t(n_cells), "cell combos"))) return rc2;
+        if ((rc2 = dev_alloc(&cell_item_min, size_t(n_cells), "cell items"))) return rc2;
+        if ((rc2 = dev_alloc(&cell_item_max, size_t(n_cells), "cell items"))) return rc2;
+        if ((rc2 = dev_alloc(&cell_first, size_t(n_cells), "cell first combos"))) return rc2;
+        fill(cell_generic, n_cells, 0);
+        fill(cell_ncombo, n_cells, 0);
+        fill(cell_item_min, n_cells, INT32_MAX);
+        fill(cell_item_max, n_cells, -1);
+        fill(cell_first, n_cells, INT32_MAX);
+        fill(flag_a, int64_t(n_cells) + 1, 0);
+        fill(flag_b, int64_t(n_cells) + 1, 0);
+        ComboArgs ca;
+        ca.cell_of_point = plan->cell_of_point;
+        ca.N = N;
+        ca.D = D;
+        ca.H = H;
+        ca.W = W;
+        ca.items_d = (D + kColDepth - 1) / kColDepth;
+        ca.items_w = (W + kColWidth - 1) / kColWidth;
+        ca.allow_clean = H < kMaxFeatH ? 1 : 0;
+        ca.combo_cell = combo_cell;
+        ca.combo_range = combo_range;
+        ca.cell_generic = cell_generic;
+        ca.cell_ncombo = cell_ncombo;
+        ca.cell_item_min = cell_item_min;
+        ca.cell_item_max = cell_item_max;
+        ca.cell_first = cell_first;
+        hipLaunchKernelGGL(k_combo_walk, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream, ca);
+        hipLaunchKernelGGL(k_cell_class, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream, ca,
+                           plan->cell_start, n_cells, flag_a, flag_b, small + 4);
+        hipLaunchKernelGGL(k_combo_table, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream, ca,
+                           plan->column_table);
+        scan_with_total(flag_a, n_cells, small + 3, stream);   // generic cells
+        scan_with_total(flag_b, n_cells, small + 3, stream);   // empty cells
+        BEVPOOL_HIP(hipGetLastError());
+        int32_t stats[2], counters[2], n_gen, n_empty, kept;
+        BEVPOOL_HIP(hipMemcpyAsync(stats, small, sizeof(stats), hipMemcpyDeviceToHost, stream));
+        BEVPOOL_HIP(hipMemcpyAsync(counters, small + 4, sizeof(counters), hipMemcpyDeviceToHost,
+                                   stream));
+        if ((rc2 = to_host(&n_gen, flag_a + n_cells))) return rc2;
+        if ((rc2 = to_host(&n_empty, flag_b + n_cells))) return rc2;
+        if ((rc2 = to_host(&kept, plan->cell_start + n_cells))) return rc2;
         BEVPOOL_HIP(hipStreamSynchronize(stream));
-        plan->n_nonempty = host[0];
-        plan->max_per_cell = host[1];
+        plan->n_nonempty = stats[0];
+        plan->max_per_cell = stats[1];
         plan->n_kept = kept;
-        const int32_t n_ne = counts2[0];
-        plan->n_empty = counts2[1];
+        plan->n_column = counters[0];
+        plan->n_generic_heavy = counters[1];
+        plan->n_generic = n_gen;
+        plan->n_empty = n_empty;
 
-        if ((rc2 = dev_alloc(&plan->tile_cells, size_t(n_ne), "tile_cells"))) return rc2;
-        if ((rc2 = dev_alloc(&plan->comp_cell_start, size_t(n_ne) + 1, "comp_cell_start"))) return rc2;
-        if ((rc2 = dev_alloc(&plan->empty_cells, size_t(plan->n_empty), "empty_cells"))) return rc2;
-        // compact into (key, cell) pairs in keys_b / vals_b's partner buffers
-        uint32_t *ne_key = keys_a;     // free again after k_cell_start
-        int32_t *ne_cell = plan->tile_cells;
-        hipLaunchKernelGGL(k_compact_cells, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream,
-                           plan->cell_start, n_cells, cell_key, flag_a, flag_b, ne_key, ne_cell,
-                           plan->empty_cells);
+        // cells without points, and generic cells by descending point count
+        if ((rc2 = dev_alloc(&plan->empty_cells, size_t(n_empty), "empty_cells"))) return rc2;
+        if ((rc2 = dev_alloc(&plan->generic_hdr, size_t(n_gen), "generic_hdr"))) return rc2;
+        uint32_t *gen_key = keys_a;   // free again after k_cell_start
+        int32_t *gen_cell = vals_a;
+        hipLaunchKernelGGL(k_compact_classes, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream,
+                           plan->cell_start, n_cells, flag_a, flag_b, plan->max_per_cell, gen_key,
+                           gen_cell, plan->empty_cells);
         BEVPOOL_HIP(hipGetLastError());
-        const int64_t max_key = int64_t(g.n_cams) * key_cols * key_bins;
-        if ((rc2 = radix_sort(ne_key, ne_cell, n_ne, bits_for(max_key)))) return rc2;
+        if ((rc2 = radix_sort(gen_key, gen_cell, n_gen, bits_for(plan->max_per_cell)))) return rc2;
 
-        // point counts in tile order and their running sum
-        BEVPOOL_HIP(hipMemsetAsync(plan->comp_cell_start, 0, sizeof(int32_t) * (size_t(n_ne) + 1),
-                                   stream));
-        if (launch_ok(n_ne)) {
-            hipLaunchKernelGGL(k_listed_counts, dim3(blocks_for(n_ne)), dim3(kBlock), 0, stream,
-                               plan->tile_cells, n_ne, plan->cell_start, plan->comp_cell_start,
-                               pos_of_cell);
-        }
-        scan_with_total(plan->comp_cell_start, n_ne, small + 3, stream);
-
-        // key groups, then tiles
-        BEVPOOL_HIP(hipMemsetAsync(flag_a, 0, sizeof(int32_t) * (size_t(n_ne) + 1), stream));
-        BEVPOOL_HIP(hipMemsetAsync(flag_b, 0, sizeof(int32_t) * (size_t(n_ne) + 1), stream));
-        if (launch_ok(n_ne))
-            hipLaunchKernelGGL(k_group_flags, dim3(blocks_for(n_ne)), dim3(kBlock), 0, stream,
-                               ne_key, n_ne, flag_a);
-        scan_with_total(flag_a, n_ne, small + 3, stream);
-        hipLaunchKernelGGL(k_group_first, dim3(blocks_for(int64_t(n_ne) + 1)), dim3(kBlock), 0,
-                           stream, flag_a, n_ne, group_first);
-        TileFlagArgs ta;
-        ta.group_scan = flag_a;
-        ta.group_first = group_first;
-        ta.X = plan->comp_cell_start;
-        ta.n = n_ne;
-        ta.flag = flag_b;
-        if (launch_ok(n_ne))
-            hipLaunchKernelGGL(k_tile_flags, dim3(blocks_for(n_ne)), dim3(kBlock), 0, stream, ta);
-        scan_with_total(flag_b, n_ne, small + 3, stream);
-        BEVPOOL_HIP(hipGetLastError());
-        BEVPOOL_HIP(hipMemcpyAsync(&plan->n_tiles, flag_b + n_ne, sizeof(int32_t),
-                                   hipMemcpyDeviceToHost, stream));
-        BEVPOOL_HIP(hipStreamSynchronize(stream));
-        const int32_t n_tiles = plan->n_tiles;
-        if ((rc2 = dev_alloc(&plan->tile_cell_begin, size_t(n_tiles) + 1, "tile_cell_begin"))) return rc2;
-        if ((rc2 = dev_alloc(&plan->tile_row_begin, size_t(n_tiles) + 1, "tile_row_begin"))) return rc2;
-        hipLaunchKernelGGL(k_tile_emit, dim3(blocks_for(int64_t(n_ne) + 1)), dim3(kBlock), 0,
-                           stream, flag_b, n_ne, plan->tile_cells, plan->tile_cell_begin,
-                           tile_of_cell);
-        BEVPOOL_HIP(hipGetLastError());
-
-        // points in tile order, staged rows and each point's row
-        if ((rc2 = dev_alloc(&plan->comp_point, size_t(kept), "comp_point"))) return rc2;
-        if ((rc2 = dev_alloc(&plan->comp_row, size_t(kept), "comp_row"))) return rc2;
-        if ((rc2 = dev_alloc(&row_scan, size_t(kept) + 1, "row scan"))) return rc2;
-        BEVPOOL_HIP(hipMemsetAsync(row_scan, 0, sizeof(int32_t) * (size_t(kept) + 1), stream));
-        if (launch_ok(kept)) {
-            hipLaunchKernelGGL(k_comp_points, dim3(blocks_for(kept)), dim3(kBlock), 0, stream,
-                               plan->sorted_point, kept, plan->cell_of_point, plan->cell_start,
-                               pos_of_cell, plan->comp_cell_start, plan->comp_point, pos_of_point);
+        // runs of the generic cells, in list order
+        if ((rc2 = dev_alloc(&run_scan, size_t(kept) + 1, "run flags"))) return rc2;
+        if ((rc2 = dev_alloc(&run_begin, size_t(n_gen) + 1, "run offsets"))) return rc2;
+        if ((rc2 = dev_alloc(&pos_of_cell, size_t(n_cells), "cell positions"))) return rc2;
+        fill(run_scan, int64_t(kept) + 1, 0);
+        fill(run_begin, int64_t(n_gen) + 1, 0);
+        const FastDiv div_hw = make_fastdiv(uint32_t(HW)), div_d = make_fastdiv(uint32_t(D));
+        if (kept > 0)
             hipLaunchKernelGGL(k_run_flags, dim3(blocks_for(kept)), dim3(kBlock), 0, stream,
-                               plan->comp_point, kept, plan->cell_of_point, tile_of_cell, HW,
-                               make_fastdiv(uint32_t(HW)), make_fastdiv(uint32_t(g.n_depth)),
-                               g.n_depth, row_scan);
-        }
-        scan_with_total(row_scan, kept, small + 3, stream);
-        hipLaunchKernelGGL(k_tile_row_begin, dim3(blocks_for(int64_t(n_tiles) + 1)), dim3(kBlock), 0,
-                           stream, plan->tile_cell_begin, plan->comp_cell_start, row_scan, n_tiles,
-                           plan->tile_row_begin);
+                               plan->sorted_point, kept, plan->cell_of_point, flag_a, HW, div_hw,
+                               div_d, D, run_scan);
+        scan_with_total(run_scan, kept, small + 3, stream);
+        if (n_gen > 0)
+            hipLaunchKernelGGL(k_generic_counts, dim3(blocks_for(n_gen)), dim3(kBlock), 0, stream,
+                               gen_cell, n_gen, plan->cell_start, run_scan, run_begin, pos_of_cell);
+        scan_with_total(run_begin, n_gen, small + 3, stream);
+        if (n_gen > 0)
+            hipLaunchKernelGGL(k_generic_hdr, dim3(blocks_for(n_gen)), dim3(kBlock), 0, stream,
+                               gen_cell, n_gen, plan->cell_start, run_begin, plan->generic_hdr);
         BEVPOOL_HIP(hipGetLastError());
-        int32_t n_rows;
-        BEVPOOL_HIP(hipMemcpyAsync(&n_rows, row_scan + kept, sizeof(n_rows), hipMemcpyDeviceToHost,
-                                   stream));
+        int32_t n_runs;
+        if ((rc2 = to_host(&n_runs, run_begin + n_gen))) return rc2;
         BEVPOOL_HIP(hipStreamSynchronize(stream));
-        plan->n_rows = n_rows;
-        if ((rc2 = dev_alloc(&plan->row_pix, size_t(n_rows), "row_pix"))) return rc2;
-        hipLaunchKernelGGL(k_rows, dim3(blocks_for(n_pix)), dim3(kBlock), 0, stream,
-                           plan->cell_of_point, pos_of_point, tile_of_cell, row_scan,
-                           plan->tile_row_begin, n_pix, HW, g.n_depth, plan->row_pix,
-                           plan->comp_row);
-        BEVPOOL_HIP(hipGetLastError());
-
-        // headers, heavy tiles and the persistent workgroups' tile runs
-        if ((rc2 = dev_alloc(&plan->tile_hdr, size_t(n_tiles) * 8, "tile_hdr"))) return rc2;
-        if ((rc2 = dev_alloc(&plan->group_tile_begin, size_t(kPersistentGroups) + 1, "tile runs"))) return rc2;
-        BEVPOOL_HIP(hipMemsetAsync(flag_a, 0, sizeof(int32_t) * (size_t(n_tiles) + 1), stream));
-        BEVPOOL_HIP(hipMemsetAsync(flag_b, 0, sizeof(int32_t) * (size_t(n_tiles) + 1), stream));
-        if (launch_ok(n_tiles))
-            hipLaunchKernelGGL(k_tile_headers, dim3(blocks_for(n_tiles)), dim3(kBlock), 0, stream,
-                               plan->tile_cell_begin, plan->tile_row_begin, plan->comp_cell_start,
-                               n_tiles, plan->tile_hdr, flag_a, flag_b);
-        scan_with_total(flag_a, n_tiles, small + 3, stream);
-        scan_with_total(flag_b, n_tiles, small + 3, stream);
-        hipLaunchKernelGGL(k_group_ranges, dim3(blocks_for(kPersistentGroups + 1)), dim3(kBlock), 0,
-                           stream, flag_b, n_tiles, plan->group_tile_begin);
-        BEVPOOL_HIP(hipMemcpyAsync(&plan->n_heavy, flag_a + n_tiles, sizeof(int32_t),
-                                   hipMemcpyDeviceToHost, stream));
-        BEVPOOL_HIP(hipStreamSynchronize(stream));
-        if ((rc2 = dev_alloc(&plan->heavy_tiles, size_t(plan->n_heavy), "heavy_tiles"))) return rc2;
-        if (launch_ok(n_tiles))
-            hipLaunchKernelGGL(k_heavy_list, dim3(blocks_for(n_tiles)), dim3(kBlock), 0, stream,
-                               flag_a, n_tiles, plan->heavy_tiles);
+        plan->n_runs = n_runs;
+        if ((rc2 = dev_alloc(&plan->generic_runs, size_t(n_runs), "generic_runs"))) return rc2;
+        if (kept > 0)
+            hipLaunchKernelGGL(k_generic_runs, dim3(blocks_for(kept)), dim3(kBlock), 0, stream,
+                               plan->sorted_point, kept, plan->cell_of_point, plan->cell_start,
+                               run_scan, pos_of_cell, run_begin, HW, D, div_hw, div_d,
+                               plan->generic_runs);
         BEVPOOL_HIP(hipGetLastError());
         BEVPOOL_HIP(hipStreamSynchronize(stream));
         return BEVPOOL_OK;

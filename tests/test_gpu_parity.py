@@ -39,8 +39,8 @@ def pkg(torch_cuda):
 
 
 def _coarse_rig():
-    """The nuScenes rig on a 3 m grid: cells with thousands of points (heavy
-    single-cell tiles staged in several rounds)."""
+    """The nuScenes rig on a 3 m grid: cells with thousands of points, fed by
+    combos of several column items (generic cells summed by a workgroup)."""
     return dataclasses.replace(wl.ring_rig(), nx=36, ny=36, cell_x=3.0, cell_y=3.0)
 
 
@@ -192,20 +192,23 @@ def test_forward_edge_rigs(torch_cuda, pkg, oracle_lib, oracle_plans, name):
     got = _run(torch_cuda, pkg, plan, w)
     _check_fp32(got, ref, np.diff(cs))
     if name == "coarse":
-        assert plan.info.max_per_cell > 1536      # exercises the multi-round path
+        assert plan.info.max_per_cell > 1536
+        assert plan.info.n_generic > 0            # exercises the heavy generic role
     if name == "empty":
         assert plan.info.n_kept == 0 and (got == 0).all()
 
 
-@pytest.mark.parametrize("channels", [1, 3, 5, 12, 64, 260])
-def test_forward_channel_counts(torch_cuda, pkg, oracle_lib, oracle_plans, channels):
-    """C not a multiple of 4 takes the scalar path; C > 256 takes two
-    channel passes on the vector path."""
-    _say(f"[forward channels] C={channels}")
-    rig = wl.tilt_rig(wl.ring_rig())
+@pytest.mark.parametrize("rig_name", ["nuscenes", "nuscenes_tilted"])
+@pytest.mark.parametrize("channels", [1, 3, 5, 12, 17, 33, 64, 81, 260])
+def test_forward_channel_counts(torch_cuda, pkg, oracle_lib, oracle_plans, channels, rig_name):
+    """Every lane-chunk count (1..5 channels per lane of a 16-lane group),
+    ragged last chunks, and rows split into channel slices (81, 260). The
+    level rig runs mostly column items, the tilted one mostly generic cells."""
+    _say(f"[forward channels] {rig_name} C={channels}")
+    rig = RIGS[rig_name]()
     P, F = wl.frames(rig, channels, 1, "peaked", seed=channels)
     w = wl.Workload("c", rig, channels, 1, "f32", P, F)
-    cop, _, cs = oracle_plans("nuscenes_tilted")
+    cop, _, cs = oracle_plans(rig_name)
     ref = oracle_lib.pool(rig, cop, P, F)
     plan = pkg.Plan.from_rig(rig)
     _check_fp32(_run(torch_cuda, pkg, plan, w), ref, np.diff(cs))
@@ -223,7 +226,7 @@ def test_count_test_on_gpu(torch_cuda, pkg, oracle_plans):
     assert np.array_equal(out, np.diff(cs).astype(np.float32))
 
 
-def test_unaligned_inputs_take_the_scalar_path(torch_cuda, pkg, oracle_lib, oracle_plans):
+def test_inputs_aligned_to_one_element(torch_cuda, pkg, oracle_lib, oracle_plans):
     torch = torch_cuda
     w = wl.make("nuscenes", seed=3)
     cop, _, cs = oracle_plans("nuscenes")
@@ -260,3 +263,19 @@ def test_plan_reuse_and_shape_checks(torch_cuda, pkg):
     with pytest.raises(pkg.BevpoolError):
         plan.forward(P, F.to(torch.float16))
     assert (plan.forward(P, F) == 0).all()
+
+
+@pytest.mark.parametrize("name", ["nuscenes", "nuscenes_tilted", "coarse", "anisotropic", "tiny"])
+def test_plan_partition_counts(pkg, oracle_plans, name):
+    """Every cell is column-served, generic or empty; the level rig is
+    served almost entirely by column items."""
+    rig = RIGS[name]()
+    plan = pkg.Plan.from_rig(rig)
+    info = plan.info
+    counts = np.diff(oracle_plans(name)[2])
+    assert info.n_column + info.n_generic == int((counts > 0).sum())
+    assert info.n_empty == int((counts == 0).sum())
+    assert info.n_runs >= info.n_generic
+    if name == "nuscenes":
+        assert info.n_column > 0.8 * info.n_nonempty
+    plan.close()
