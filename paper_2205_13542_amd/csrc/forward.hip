@@ -9,7 +9,7 @@
 //                  and holds kColDepth fp32 accumulators per channel. Each
 //                  feature row (n, h, w) is read once and applied to every
 //                  depth bin of the item; the depth probabilities are read
-//                  one per lane and broadcast inside the row with DPP.
+//                  one per lane and broadcast to the group through LDS.
 //                  Single-combo cells are stored from registers; the
 //                  combos of a multi-combo cell meet in LDS and the cell's
 //                  first combo adds them in slot order.
@@ -83,14 +83,14 @@ __device__ __forceinline__ void store_f32(Rsrc r, uint32_t off, float v) {
 
 struct FwdArgs {
     const char *P, *F;
-    float *out;
+    float *out, *part;
     const int2 *table;
     const int4 *gen_hdr;
     const int4 *gen_runs;
     const int32_t *empty_cells;
     int32_t N, D, H, W, HW;
     int32_t n_cells, C, slice_c;
-    uint32_t p_bytes, f_bytes, o_bytes, run_bytes;   // per frame (runs: whole table)
+    uint32_t p_bytes, f_bytes, o_bytes, s_bytes, run_bytes;   // per frame (runs: whole table)
     int32_t items_d, items_w, n_items;
     int32_t n_heavy, n_light, n_empty;
     int32_t base_col, base_zero, base_light;
@@ -98,21 +98,22 @@ struct FwdArgs {
     FastDiv div_units;
 };
 
-// The three buffers of frame b.
+// The buffers of frame b: depth probabilities, features, BEV map and the
+// partial-sum slots.
 struct Frame {
-    Rsrc P, F, O;
+    Rsrc P, F, O, S;
     __device__ __forceinline__ Frame(const FwdArgs &a, int b)
         : P(make_rsrc(a.P + int64_t(b) * a.p_bytes, a.p_bytes)),
           F(make_rsrc(a.F + int64_t(b) * a.f_bytes, a.f_bytes)),
-          O(make_rsrc(reinterpret_cast<const char *>(a.out) + int64_t(b) * a.o_bytes, a.o_bytes)) {}
+          O(make_rsrc(reinterpret_cast<const char *>(a.out) + int64_t(b) * a.o_bytes, a.o_bytes)),
+          S(make_rsrc(reinterpret_cast<const char *>(a.part) + int64_t(b) * a.s_bytes, a.s_bytes)) {}
 };
 
-constexpr int kSlots = kColDepth * kColWidth;   // 128 combos per item
 constexpr int kStages = 6;                      // row-pair stages in flight per wave
-constexpr int kZeroCells = kSlots;              // empty rows per zeroing workgroup
+constexpr int kZeroCells = 128;                 // empty rows per zeroing workgroup
 
-// LDS row stride of a slot: 16*NCH floats, padded so that the four groups
-// of a wave start on different bank quarters.
+// LDS row stride of a lane group's partial sums: 16*NCH floats, padded so
+// that the four groups of a wave start on different bank quarters.
 template <int NCH>
 constexpr int slot_stride() { return 16 * NCH + ((NCH % 2 == 0) ? 16 : 0); }
 
@@ -164,50 +165,45 @@ __device__ __forceinline__ void store_row(Rsrc dst, uint32_t off, const float *v
     store_f32(dst, tail_ok ? off + uint32_t(NCH - 1) * 64 : kOff, v[NCH - 1]);
 }
 
-// acc[J] += P(depth bin J, this row) * f for every depth bin J of the item;
-// the probabilities sit in lanes OFF..OFF+7 of the row (0 where a bin has
-// no point in this row). Branch-free: skipping absent bins saves little.
-template <int OFF, int J, int NCH>
-struct Apply {
-    static __device__ __forceinline__ void run(float (&acc)[kColDepth][NCH], float pv,
-                                               const Row<NCH> &f) {
-        const float pb = row_bcast<OFF + J>(pv);
+// acc[J] += pb[J] * f for the kColDepth depth bins of one row: pb holds the
+// row's probabilities of this lane group's column, read back from LDS as
+// broadcasts (a DPP broadcast operand would halve the FMA issue rate).
+template <int NCH>
+__device__ __forceinline__ void apply_row(float (&acc)[kColDepth][NCH], const float4 &lo,
+                                          const float4 &hi, const Row<NCH> &f) {
+    const float pb[kColDepth] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
 #pragma unroll
-        for (int k = 0; k < NCH; ++k) acc[J][k] = __builtin_fmaf(pb, f.v[k], acc[J][k]);
-        Apply<OFF, J + 1, NCH>::run(acc, pv, f);
-    }
-};
-template <int OFF, int NCH>
-struct Apply<OFF, kColDepth, NCH> {
-    static __device__ __forceinline__ void run(float (&)[kColDepth][NCH], float, const Row<NCH> &) {}
-};
+    for (int J = 0; J < kColDepth; ++J)
+#pragma unroll
+        for (int k = 0; k < NCH; ++k) acc[J][k] = __builtin_fmaf(pb[J], f.v[k], acc[J][k]);
+}
 
-// After the row loop: single-combo cells are stored, multi-combo partials
-// go to their LDS slot. Lane J of the group holds the entry of depth bin J.
+// After the row loop: each depth bin's sums go to its single-combo cell's
+// row of the BEV map, or to the partial-sum slot of its combo. Lane J of
+// the group holds the entry of depth bin J.
 template <int J, int NCH>
 struct Emit {
-    static __device__ __forceinline__ void run(const float (&acc)[kColDepth][NCH], int ecell, int ey,
-                                               uint32_t dm, Rsrc out, uint32_t ch_off, int C,
-                                               float *s_part, int wl, bool tail_ok) {
+    static __device__ __forceinline__ void run(const float (&acc)[kColDepth][NCH], int ex, int ey,
+                                               uint32_t dm, Rsrc out, Rsrc part, uint32_t ch_off,
+                                               int C, bool tail_ok) {
         if (dm & (1u << J)) {
-            const int cell = row_bcast<J>(ecell);
+            const int x = row_bcast<J>(ex);
             const uint32_t y = uint32_t(row_bcast<J>(ey));
-            const bool single = cell >= 0 && !(y & kComboMulti);
-            store_row<NCH>(out, single ? uint32_t(cell) * uint32_t(C) * 4u + ch_off : kOff, acc[J],
-                           tail_ok);
-            if (cell >= 0 && (y & kComboMulti)) {
-                float *dst = s_part + (J * kColWidth + wl) * slot_stride<NCH>() + (threadIdx.x & 15);
-#pragma unroll
-                for (int k = 0; k < NCH; ++k) dst[16 * k] = acc[J][k];
+            if (x >= 0) {
+                const uint32_t off = uint32_t(x) * uint32_t(C) * 4u + ch_off;
+                if (y & kComboMulti)
+                    store_row<NCH>(part, off, acc[J], tail_ok);
+                else
+                    store_row<NCH>(out, off, acc[J], tail_ok);
             }
         }
-        Emit<J + 1, NCH>::run(acc, ecell, ey, dm, out, ch_off, C, s_part, wl, tail_ok);
+        Emit<J + 1, NCH>::run(acc, ex, ey, dm, out, part, ch_off, C, tail_ok);
     }
 };
 template <int NCH>
 struct Emit<kColDepth, NCH> {
     static __device__ __forceinline__ void run(const float (&)[kColDepth][NCH], int, int, uint32_t,
-                                               Rsrc, uint32_t, int, float *, int, bool) {}
+                                               Rsrc, Rsrc, uint32_t, int, bool) {}
 };
 
 // Rows of kZeroCells listed empty cells of frame b (in slice 0 only),
@@ -239,7 +235,7 @@ __device__ void zero_rows(const FwdArgs &a, int zb, int b, int *s_cell) {
 
 template <int DT, int NCH>
 __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0, int cn,
-                            float *s_part, int *s_cell) {
+                            float *s_pb) {
     constexpr uint32_t ES = Elem<DT>::kBytes;
     const int db = item % a.items_d;
     const int t = item / a.items_d;
@@ -279,7 +275,6 @@ __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0,
     const uint32_t ey = uint32_t(e.y);
     const int hlo = act ? int(ey & 0xFFFFu) : 0x7FFFFFFF;
     const int hhi = act ? int((ey >> 16) & 0x3FFFu) : 0;
-    if (j < 8) s_cell[jd * kColWidth + wl] = (act && (ey & kComboMulti)) ? e.x : -1;
     // depth bins present in the wave (a wave without any skips the loop)
     const uint64_t bal = __ballot(act);
     const uint32_t dm = uint32_t((bal | (bal >> 16) | (bal >> 32) | (bal >> 48)) & 0xFFu);
@@ -291,54 +286,32 @@ __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0,
         for (int k = 0; k < NCH; ++k) acc[q][k] = 0.f;
 
     if (dm != 0) {
-        // a ring of kStages stages of two rows: while one stage is applied,
-        // the loads of the next kStages - 1 are outstanding
+        // A ring of kStages stages of two rows: while one stage is applied,
+        // the loads of the next kStages - 1 are outstanding. Each lane's
+        // masked probability (depth bin j & 7, row j >> 3 of the stage) goes
+        // through this group's 16 LDS words and comes back to all 16 lanes.
+        float *pq = s_pb + (wave * 4 + (lane >> 4)) * 16;
         for (int h = 0; h < H; h += 2 * kStages) {
 #pragma unroll
             for (int u = 0; u < kStages; ++u) {
                 const int hs = h + 2 * u;
                 if (hs >= H) break;
                 const int hp = hs + hsel;
-                const float pv = (hp >= hlo && hp < hhi) ? st[u].pv : 0.f;
-                Apply<0, 0, NCH>::run(acc, pv, st[u].f0);
-                Apply<8, 0, NCH>::run(acc, pv, st[u].f1);
+                pq[j] = (hp >= hlo && hp < hhi) ? st[u].pv : 0.f;
+                __builtin_amdgcn_wave_barrier();
+                const float4 r0a = *reinterpret_cast<const float4 *>(pq);
+                const float4 r0b = *reinterpret_cast<const float4 *>(pq + 4);
+                const float4 r1a = *reinterpret_cast<const float4 *>(pq + 8);
+                const float4 r1b = *reinterpret_cast<const float4 *>(pq + 12);
+                __builtin_amdgcn_wave_barrier();
+                apply_row<NCH>(acc, r0a, r0b, st[u].f0);
+                apply_row<NCH>(acc, r1a, r1b, st[u].f1);
                 load_stage(st[u], hs + 2 * kStages);
             }
         }
     }
 
-    const uint32_t ch_off = uint32_t(c0 + j) * 4u;
-    Emit<0, NCH>::run(acc, e.x, e.y, dm, fr.O, ch_off, a.C, s_part, wl, tail_ok);
-    __syncthreads();
-
-    // Multi-combo cells: the group of the cell's first combo adds the cell's
-    // slots in ascending slot order. A cell's slots all lie in this item, at
-    // or after its first combo.
-    constexpr int SS = slot_stride<NCH>();
-    const int gsh = (lane >> 4) * 16;
-#pragma unroll
-    for (int J = 0; J < kColDepth; ++J) {
-        const int s0 = J * kColWidth + wl;
-        const int cell = s_cell[s0];
-        const bool owner = cell >= 0 && (uint32_t(__shfl(e.y, (lane & 48) | J)) & kComboOwner);
-        if (__ballot(owner) == 0) continue;
-        float sum[NCH];
-#pragma unroll
-        for (int k = 0; k < NCH; ++k) sum[k] = 0.f;
-        for (int r = J; r < kColDepth; ++r) {
-            const int tt = r * kColWidth + j;
-            const bool m = owner && tt >= s0 && s_cell[tt] == cell;
-            uint32_t gm = uint32_t(__ballot(m) >> gsh) & 0xFFFFu;
-            while (gm) {
-                const int k0 = __builtin_ctz(gm);
-                gm &= gm - 1;
-                const float *src = s_part + (r * kColWidth + k0) * SS + j;
-#pragma unroll
-                for (int k = 0; k < NCH; ++k) sum[k] += src[16 * k];
-            }
-        }
-        store_row<NCH>(fr.O, owner ? uint32_t(cell) * uint32_t(a.C) * 4u + ch_off : kOff, sum, tail_ok);
-    }
+    Emit<0, NCH>::run(acc, e.x, e.y, dm, fr.O, fr.S, uint32_t(c0 + j) * 4u, a.C, tail_ok);
 }
 
 // A generic cell's runs in chunks of 64: lane i loads run i of the chunk and
@@ -426,8 +399,9 @@ __device__ void heavy_generic(const FwdArgs &a, const Frame &fr, int k, int c0, 
 
 template <int DT, int NCH>
 __global__ __launch_bounds__(kBlock) void k_forward(FwdArgs a) {
-    __shared__ float s_part[kSlots * slot_stride<NCH>()];
-    __shared__ int s_cell[kSlots];
+    __shared__ float s_part[kColWidth * slot_stride<NCH>()];   // heavy cells: group partials
+    __shared__ int s_cell[kZeroCells];                         // zero rows: cell ids
+    __shared__ __align__(16) float s_pb[kBlock];   // probability broadcast: 16 words per lane group
     const int bx = blockIdx.x, b = blockIdx.y;
     const int c0 = blockIdx.z * a.slice_c;
     const int cn = min(a.slice_c, a.C - c0);
@@ -436,8 +410,7 @@ __global__ __launch_bounds__(kBlock) void k_forward(FwdArgs a) {
     } else if (bx < a.base_col) {
         return;  // padding: column items start on a multiple of 8
     } else if (bx < a.base_col + a.n_items) {
-        column_item<DT, NCH>(a, Frame(a, b), xcd_remap(bx - a.base_col, a.n_items), c0, cn,
-                             s_part, s_cell);
+        column_item<DT, NCH>(a, Frame(a, b), xcd_remap(bx - a.base_col, a.n_items), c0, cn, s_pb);
     } else if (bx < a.base_zero) {
         return;
     } else if (bx < a.base_light) {
@@ -445,6 +418,55 @@ __global__ __launch_bounds__(kBlock) void k_forward(FwdArgs a) {
     } else {
         const int k = (bx - a.base_light) * kWaves + int(threadIdx.x >> 6);
         if (k < a.n_light) light_generic<DT, NCH>(a, Frame(a, b), k, c0, cn);
+    }
+}
+
+// Cells fed by several combos: the slots of multi-combo cell k are
+// multi_begin[k] .. multi_begin[k+1]-1, added in that order. One group of 16
+// lanes per cell, channels j, j + 16, ...
+constexpr int kCombineChunks = 5;   // 16-channel chunks per pass (80 channels)
+constexpr int kCombineSlots = 4;    // slots loaded per step
+
+struct CombineArgs {
+    const float *part;
+    float *out;
+    const int32_t *multi_begin, *multi_cell;
+    int32_t n_multi, C, n_cells, n_partials;
+    uint32_t o_bytes, s_bytes;
+};
+
+__global__ __launch_bounds__(kBlock) void k_combine(CombineArgs a) {
+    const int b = blockIdx.y;
+    const int k = blockIdx.x * kColWidth + int(threadIdx.x >> 4);
+    if (k >= a.n_multi) return;
+    const int j = threadIdx.x & 15;
+    const Rsrc S = make_rsrc(reinterpret_cast<const char *>(a.part) + int64_t(b) * a.s_bytes, a.s_bytes);
+    const Rsrc O = make_rsrc(reinterpret_cast<const char *>(a.out) + int64_t(b) * a.o_bytes, a.o_bytes);
+    const int s0 = a.multi_begin[k], s1 = a.multi_begin[k + 1];
+    const uint32_t obase = uint32_t(a.multi_cell[k]) * uint32_t(a.C) * 4u;
+    const uint32_t row = uint32_t(a.C) * 4u;
+    for (int c = j; c < a.C; c += kCombineChunks * 16) {
+        float sum[kCombineChunks];
+#pragma unroll
+        for (int q = 0; q < kCombineChunks; ++q) sum[q] = 0.f;
+        // kCombineSlots slots' loads in flight at a time, added in slot order
+        for (int sl = s0; sl < s1; sl += kCombineSlots) {
+            float v[kCombineSlots][kCombineChunks];
+#pragma unroll
+            for (int u = 0; u < kCombineSlots; ++u)
+#pragma unroll
+                for (int q = 0; q < kCombineChunks; ++q)
+                    v[u][q] = Elem<BEVPOOL_F32>::load(
+                        S, (sl + u < s1 && c + 16 * q < a.C) ? uint32_t(sl + u) * row + uint32_t(c + 16 * q) * 4u : kOff);
+#pragma unroll
+            for (int u = 0; u < kCombineSlots; ++u)
+#pragma unroll
+                for (int q = 0; q < kCombineChunks; ++q)
+                    if (sl + u < s1) sum[q] += v[u][q];
+        }
+#pragma unroll
+        for (int q = 0; q < kCombineChunks; ++q)
+            store_f32(O, c + 16 * q < a.C ? obase + uint32_t(c + 16 * q) * 4u : kOff, sum[q]);
     }
 }
 
@@ -466,23 +488,43 @@ int round8(int x) { return (x + 7) & ~7; }
 
 using namespace bevpool;
 
-int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *plan, float *out,
+int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *cplan, float *out,
                            int32_t batch, int32_t channels, int32_t dtype, hipStream_t stream) {
+    // The plan's partial-sum scratch grows here; the rest of the plan is
+    // read-only for the forward pass.
+    bevpool_plan_s *plan = const_cast<bevpool_plan_s *>(cplan);
     const bevpool_geometry &g = plan->geom;
     const int64_t n_pix = int64_t(g.n_cams) * g.feat_h * g.feat_w;
     const int64_t esize = dtype == BEVPOOL_F32 ? 4 : 2;
     const int64_t p_bytes = plan->n_points * esize;
     const int64_t f_bytes = n_pix * channels * esize;
     const int64_t o_bytes = int64_t(plan->n_cells) * channels * 4;
+    const int64_t s_bytes = int64_t(plan->n_partials) * channels * 4;
     const int64_t run_bytes = int64_t(plan->n_runs) * 16;
     constexpr int64_t kLimit = int64_t(1) << 31;
-    if (p_bytes >= kLimit || f_bytes >= kLimit || o_bytes >= kLimit || run_bytes >= kLimit)
+    if (p_bytes >= kLimit || f_bytes >= kLimit || o_bytes >= kLimit || s_bytes >= kLimit ||
+        run_bytes >= kLimit)
         return bevpool_fail(BEVPOOL_ERR_OVERFLOW,
                             "channels=%d: one frame's depth (%lld B), feature (%lld B) or BEV "
                             "(%lld B) tensor reaches 2 GiB", channels, (long long)p_bytes,
                             (long long)f_bytes, (long long)o_bytes);
     if (batch > 65535)
         return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "batch=%d exceeds 65535 frames per call", batch);
+
+    const size_t need = size_t(s_bytes) * size_t(batch);
+    if (need > plan->scratch_bytes) {
+        BEVPOOL_HIP(hipStreamSynchronize(stream));
+        (void)hipFree(plan->scratch);
+        plan->scratch = nullptr;
+        plan->scratch_bytes = 0;
+        hipError_t e = hipMalloc(reinterpret_cast<void **>(&plan->scratch), need);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            return bevpool_fail(BEVPOOL_ERR_OOM, "out of device memory for %zu bytes of partial sums",
+                                need);
+        }
+        plan->scratch_bytes = need;
+    }
 
     const int n_slices = (channels + kSliceChannels - 1) / kSliceChannels;
     const int slice_c = (channels + n_slices - 1) / n_slices;
@@ -492,6 +534,7 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
     a.P = static_cast<const char *>(P);
     a.F = static_cast<const char *>(F);
     a.out = out;
+    a.part = plan->scratch;
     a.table = plan->column_table;
     a.gen_hdr = plan->generic_hdr;
     a.gen_runs = plan->generic_runs;
@@ -507,6 +550,7 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
     a.p_bytes = uint32_t(p_bytes);
     a.f_bytes = uint32_t(f_bytes);
     a.o_bytes = uint32_t(o_bytes);
+    a.s_bytes = uint32_t(s_bytes);
     a.run_bytes = uint32_t(run_bytes);
     a.items_d = (g.n_depth + kColDepth - 1) / kColDepth;
     a.items_w = (g.feat_w + kColWidth - 1) / kColWidth;
@@ -529,5 +573,21 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
         default: launch_dtype<BEVPOOL_F16>(a, grid, nch, stream); break;
     }
     BEVPOOL_HIP(hipGetLastError());
+    if (plan->n_multi > 0) {
+        CombineArgs ca;
+        ca.part = plan->scratch;
+        ca.out = out;
+        ca.multi_begin = plan->multi_begin;
+        ca.multi_cell = plan->multi_cell;
+        ca.n_multi = plan->n_multi;
+        ca.C = channels;
+        ca.n_cells = plan->n_cells;
+        ca.n_partials = plan->n_partials;
+        ca.o_bytes = uint32_t(o_bytes);
+        ca.s_bytes = uint32_t(s_bytes);
+        hipLaunchKernelGGL(k_combine, dim3((plan->n_multi + kColWidth - 1) / kColWidth, batch),
+                           dim3(kBlock), 0, stream, ca);
+        BEVPOOL_HIP(hipGetLastError());
+    }
     return BEVPOOL_OK;
 }

@@ -16,29 +16,30 @@ namespace bevpool {
 // form one range h_lo..h_hi-1. A level camera makes almost every combo
 // clean, since its rows then differ only in height.
 //
-// The points are split over column items of kColDepth depth bins x
-// kColWidth pixel columns of one camera. A cell is "column-served" when
-// all its points come from clean combos inside one item. Such a cell is
-// computed by that item's workgroup: the workgroup reads each feature row
-// (n, h, w) of its columns once and applies it to the kColDepth depth bins
-// held in registers. A cell fed by a single combo is stored from
-// registers; a cell fed by several combos of the item is summed through
-// LDS. Every other cell with points is "generic": its points are gathered
-// in runs of consecutive depth bins of one pixel. A generic cell gets one
-// wave, or a whole workgroup when it has more than kGenHeavy points. Cells
-// without points are zeroed by workgroups of their own.
+// A cell whose points all come from clean combos is "column-served". The
+// forward pass reads each feature row (n, h, w) once per block of
+// kColDepth depth bins and applies it to all of them, with the sums of the
+// block's combos held in registers (column items of kColDepth x
+// kColWidth combos of one camera). A cell fed by one combo is stored from
+// registers. A cell fed by several combos (near the rig a cell spans
+// several pixel columns) gets one partial-sum slot per combo, and a second
+// kernel adds the slots of each such cell in slot order. Every other cell
+// with points is "generic": its points are gathered in runs of consecutive
+// depth bins of one pixel, by one wave, or by a whole workgroup when it has
+// more than kGenHeavy points. Cells without points are zeroed by
+// workgroups of their own.
 constexpr int kWaveSize = 64;
 constexpr int kWaves = 4;
-constexpr int kBlock = kWaves * kWaveSize;      // plan kernels and the forward kernel
-constexpr int kGroupLanes = 16;                 // lanes per pixel column (one DPP row)
+constexpr int kBlock = kWaves * kWaveSize;      // plan kernels and the forward kernels
+constexpr int kGroupLanes = 16;                 // lanes per pixel column
 constexpr int kColDepth = 8;
 constexpr int kColWidth = kBlock / kGroupLanes; // 16 columns per item
 constexpr int kGenHeavy = 256;
-constexpr int kSliceChannels = 80;              // channels per pass (LDS partials)
+constexpr int kSliceChannels = 80;              // channels per pass
 
-// Column-table entry flags (second word: h_lo | h_hi << 16 | flags).
-constexpr uint32_t kComboMulti = 1u << 31;      // the cell has other combos
-constexpr uint32_t kComboOwner = 1u << 30;      // first combo of a multi cell
+// Column-table entry: {cell (single-combo cell) or partial slot (multi),
+// h_lo | h_hi << 16 | kComboMulti}.
+constexpr uint32_t kComboMulti = 1u << 31;
 constexpr int kMaxFeatH = 1 << 14;              // rows must fit the 15-bit fields
 
 // Unsigned division by a run-time constant through a multiply-high, after
@@ -70,12 +71,17 @@ struct bevpool_plan_s {
     int64_t n_points, n_kept;
     int32_t n_cells, n_nonempty, max_per_cell;
     int32_t n_column, n_generic, n_generic_heavy, n_runs, n_empty;
+    int32_t n_partials, n_multi;
     // canonical association (exported)
     int32_t *cell_of_point;  // [n_points]
     int32_t *sorted_point;   // [n_points]: kept ids by (cell, id), then dropped ids
     int32_t *cell_start;     // [n_cells + 1]
     // forward work partition
-    int2 *column_table;      // [N][D][W]: {cell or -1, h_lo | h_hi << 16 | flags}
+    int2 *column_table;      // [N][D][W]: {cell, slot or -1, h_lo | h_hi << 16 | flags}
+    int32_t *multi_begin;    // [n_multi + 1]: first partial slot of each multi-combo cell
+    int32_t *multi_cell;     // [n_multi]
+    float *scratch;          // partial sums, [batch][n_partials][channels], grown on demand
+    size_t scratch_bytes;
     int4 *generic_hdr;       // [n_generic]: {cell, first run, runs, points}, most points first
     int4 *generic_runs;      // [n_runs]: {first point id, pixel, depth bins, 0}
     int32_t *empty_cells;    // [n_empty] cells without points, ascending

@@ -267,13 +267,12 @@ __global__ __launch_bounds__(kBlock) void k_fill(int32_t *p, int64_t n, int32_t 
 
 struct ComboArgs {
     const int32_t *cell_of_point;
-    int32_t N, D, H, W, items_d, items_w;
+    int32_t N, D, H, W;
     int32_t allow_clean;        // 0 when rows do not fit the packed row range
     int32_t *combo_cell;        // [N*D*W]: cell of a clean combo, -1 none kept, -2 not clean
     int32_t *combo_range;       // [N*D*W]: h_lo | h_hi << 16
     int32_t *cell_generic;      // [n_cells]: 1 if a combo that is not clean touches the cell
     int32_t *cell_ncombo;       // [n_cells]: clean combos of the cell
-    int32_t *cell_item_min, *cell_item_max, *cell_first;
 };
 
 // One thread per combo walks its H rows.
@@ -283,7 +282,6 @@ __global__ __launch_bounds__(kBlock) void k_combo_walk(ComboArgs a) {
     if (x >= n_combo) return;
     const int32_t X = int32_t(x);
     const int32_t w = X % a.W, nd = X / a.W;
-    const int32_t d = nd % a.D, n = nd / a.D;
     const int64_t base = int64_t(nd) * a.H * a.W + w;
     int32_t c0 = -1, hlo = -1, hlast = -1, kept = 0;
     bool one_cell = true;
@@ -306,13 +304,9 @@ __global__ __launch_bounds__(kBlock) void k_combo_walk(ComboArgs a) {
     }
     const bool clean = a.allow_clean && one_cell && kept == hlast - hlo + 1;
     if (clean) {
-        const int32_t item = (n * a.items_d + d / kColDepth) * a.items_w + w / kColWidth;
         a.combo_cell[X] = c0;
         a.combo_range[X] = hlo | ((hlast + 1) << 16);
         atomicAdd(&a.cell_ncombo[c0], 1);
-        atomicMin(&a.cell_item_min[c0], item);
-        atomicMax(&a.cell_item_max[c0], item);
-        atomicMin(&a.cell_first[c0], X);
     } else {
         a.combo_cell[X] = -2;
         a.combo_range[X] = 0;
@@ -323,38 +317,71 @@ __global__ __launch_bounds__(kBlock) void k_combo_walk(ComboArgs a) {
     }
 }
 
-__device__ __forceinline__ bool column_served(const ComboArgs &a, int32_t c) {
-    return a.cell_generic[c] == 0 && a.cell_item_min[c] == a.cell_item_max[c];
-}
-
-// Per cell: generic flag, empty flag; counters[0] += served, counters[1] +=
-// heavy generic.
+// Per cell: generic flag, empty flag; counters[0] += column-served cells,
+// counters[1] += heavy generic cells.
 __global__ __launch_bounds__(kBlock) void k_cell_class(ComboArgs a, const int32_t *cell_start,
                                                        int32_t n_cells, int32_t *generic_flag,
                                                        int32_t *empty_flag, int32_t *counters) {
     const int32_t c = blockIdx.x * kBlock + threadIdx.x;
     if (c >= n_cells) return;
     const int32_t cnt = cell_start[c + 1] - cell_start[c];
-    const bool served = cnt > 0 && column_served(a, c);
+    const bool served = cnt > 0 && a.cell_generic[c] == 0;
     generic_flag[c] = (cnt > 0 && !served) ? 1 : 0;
     empty_flag[c] = cnt == 0 ? 1 : 0;
     if (served) atomicAdd(&counters[0], 1);
     if (cnt > kGenHeavy && !served) atomicAdd(&counters[1], 1);
 }
 
-__global__ __launch_bounds__(kBlock) void k_combo_table(ComboArgs a, int2 *table) {
+// Column table entries, and a flag on each combo of a multi-combo cell.
+__global__ __launch_bounds__(kBlock) void k_combo_table(ComboArgs a, int2 *table, int32_t *multi_flag) {
     const int64_t x = int64_t(blockIdx.x) * kBlock + threadIdx.x;
     if (x >= int64_t(a.N) * a.D * a.W) return;
     const int32_t X = int32_t(x);
     const int32_t c = a.combo_cell[X];
     int2 e = make_int2(-1, 0);
-    if (c >= 0 && column_served(a, c)) {
-        uint32_t y = uint32_t(a.combo_range[X]);
-        if (a.cell_ncombo[c] > 1) y |= kComboMulti;
-        if (a.cell_first[c] == X) y |= kComboOwner;
-        e = make_int2(c, int32_t(y));
+    bool multi = false;
+    if (c >= 0 && a.cell_generic[c] == 0) {
+        multi = a.cell_ncombo[c] > 1;
+        e = make_int2(c, a.combo_range[X] | int32_t(multi ? kComboMulti : 0u));
     }
     table[X] = e;
+    multi_flag[X] = multi ? 1 : 0;
+}
+
+// Combos of multi-combo cells as (cell, combo) pairs in combo order.
+__global__ __launch_bounds__(kBlock) void k_multi_compact(const int32_t *combo_cell,
+                                                          const int32_t *multi_pos, int32_t n_combo,
+                                                          uint32_t *key, int32_t *val) {
+    const int32_t X = blockIdx.x * kBlock + threadIdx.x;
+    if (X >= n_combo || multi_pos[X + 1] == multi_pos[X]) return;
+    key[multi_pos[X]] = uint32_t(combo_cell[X]);
+    val[multi_pos[X]] = X;
+}
+
+// After the stable sort by cell, position i is the partial-sum slot of combo
+// val[i]: a cell's slots are contiguous and in combo order. The table entry
+// of the combo then names its slot; cell heads are flagged.
+__global__ __launch_bounds__(kBlock) void k_multi_slots(const uint32_t *key, const int32_t *val,
+                                                        int32_t n, int2 *table, int32_t *head_flag) {
+    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+    if (i >= n) return;
+    table[val[i]].x = i;
+    head_flag[i] = (i == 0 || key[i] != key[i - 1]) ? 1 : 0;
+}
+
+__global__ __launch_bounds__(kBlock) void k_multi_cells(const uint32_t *key, const int32_t *head_scan,
+                                                        int32_t n, int32_t *multi_begin,
+                                                        int32_t *multi_cell) {
+    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+    if (i > n) return;
+    if (i == n) {
+        multi_begin[head_scan[n]] = n;
+        return;
+    }
+    if (head_scan[i + 1] != head_scan[i]) {
+        multi_begin[head_scan[i]] = i;
+        multi_cell[head_scan[i]] = int32_t(key[i]);
+    }
 }
 
 // Generic cells keyed for a descending sort by point count; empty cells
@@ -486,17 +513,16 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
     uint32_t *keys_a = nullptr, *keys_b = nullptr;
     int32_t *vals_a = nullptr, *vals_b = nullptr, *hist = nullptr, *small = nullptr;
     int32_t *flag_a = nullptr, *flag_b = nullptr;
-    int32_t *combo_cell = nullptr, *combo_range = nullptr, *cell_generic = nullptr;
-    int32_t *cell_ncombo = nullptr, *cell_item_min = nullptr, *cell_item_max = nullptr;
-    int32_t *cell_first = nullptr, *run_scan = nullptr, *run_begin = nullptr;
-    int32_t *pos_of_cell = nullptr;
+    int32_t *combo_cell = nullptr, *combo_range = nullptr, *combo_flag = nullptr;
+    int32_t *cell_generic = nullptr, *cell_ncombo = nullptr, *head_scan = nullptr;
+    int32_t *run_scan = nullptr, *run_begin = nullptr, *pos_of_cell = nullptr;
     auto cleanup = [&]() {
         for (void *q : {(void *)d_calib, (void *)keys_a, (void *)keys_b, (void *)vals_a,
                         (void *)vals_b, (void *)hist, (void *)small, (void *)flag_a,
                         (void *)flag_b, (void *)combo_cell, (void *)combo_range,
-                        (void *)cell_generic, (void *)cell_ncombo, (void *)cell_item_min,
-                        (void *)cell_item_max, (void *)cell_first, (void *)run_scan,
-                        (void *)run_begin, (void *)pos_of_cell})
+                        (void *)combo_flag, (void *)cell_generic, (void *)cell_ncombo,
+                        (void *)head_scan, (void *)run_scan, (void *)run_begin,
+                        (void *)pos_of_cell})
             (void)hipFree(q);
     };
 
@@ -584,49 +610,42 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         // combos, cell classes and the column table
         if ((rc2 = dev_alloc(&combo_cell, size_t(n_combo), "combo cells"))) return rc2;
         if ((rc2 = dev_alloc(&combo_range, size_t(n_combo), "combo ranges"))) return rc2;
+        if ((rc2 = dev_alloc(&combo_flag, size_t(n_combo) + 1, "combo flags"))) return rc2;
         if ((rc2 = dev_alloc(&cell_generic, size_t(n_cells), "cell classes"))) return rc2;
         if ((rc2 = dev_alloc(&cell_ncombo, size_t(n_cells), "cell combos"))) return rc2;
-        if ((rc2 = dev_alloc(&cell_item_min, size_t(n_cells), "cell items"))) return rc2;
-        if ((rc2 = dev_alloc(&cell_item_max, size_t(n_cells), "cell items"))) return rc2;
-        if ((rc2 = dev_alloc(&cell_first, size_t(n_cells), "cell first combos"))) return rc2;
         fill(cell_generic, n_cells, 0);
         fill(cell_ncombo, n_cells, 0);
-        fill(cell_item_min, n_cells, INT32_MAX);
-        fill(cell_item_max, n_cells, -1);
-        fill(cell_first, n_cells, INT32_MAX);
         fill(flag_a, int64_t(n_cells) + 1, 0);
         fill(flag_b, int64_t(n_cells) + 1, 0);
+        fill(combo_flag, n_combo + 1, 0);
         ComboArgs ca;
         ca.cell_of_point = plan->cell_of_point;
         ca.N = N;
         ca.D = D;
         ca.H = H;
         ca.W = W;
-        ca.items_d = (D + kColDepth - 1) / kColDepth;
-        ca.items_w = (W + kColWidth - 1) / kColWidth;
         ca.allow_clean = H < kMaxFeatH ? 1 : 0;
         ca.combo_cell = combo_cell;
         ca.combo_range = combo_range;
         ca.cell_generic = cell_generic;
         ca.cell_ncombo = cell_ncombo;
-        ca.cell_item_min = cell_item_min;
-        ca.cell_item_max = cell_item_max;
-        ca.cell_first = cell_first;
         hipLaunchKernelGGL(k_combo_walk, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream, ca);
         hipLaunchKernelGGL(k_cell_class, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream, ca,
                            plan->cell_start, n_cells, flag_a, flag_b, small + 4);
         hipLaunchKernelGGL(k_combo_table, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream, ca,
-                           plan->column_table);
+                           plan->column_table, combo_flag);
         scan_with_total(flag_a, n_cells, small + 3, stream);   // generic cells
         scan_with_total(flag_b, n_cells, small + 3, stream);   // empty cells
+        scan_with_total(combo_flag, n_combo, small + 3, stream);   // combos of multi cells
         BEVPOOL_HIP(hipGetLastError());
-        int32_t stats[2], counters[2], n_gen, n_empty, kept;
+        int32_t stats[2], counters[2], n_gen, n_empty, kept, n_part;
         BEVPOOL_HIP(hipMemcpyAsync(stats, small, sizeof(stats), hipMemcpyDeviceToHost, stream));
         BEVPOOL_HIP(hipMemcpyAsync(counters, small + 4, sizeof(counters), hipMemcpyDeviceToHost,
                                    stream));
         if ((rc2 = to_host(&n_gen, flag_a + n_cells))) return rc2;
         if ((rc2 = to_host(&n_empty, flag_b + n_cells))) return rc2;
         if ((rc2 = to_host(&kept, plan->cell_start + n_cells))) return rc2;
+        if ((rc2 = to_host(&n_part, combo_flag + n_combo))) return rc2;
         BEVPOOL_HIP(hipStreamSynchronize(stream));
         plan->n_nonempty = stats[0];
         plan->max_per_cell = stats[1];
@@ -635,6 +654,29 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         plan->n_generic_heavy = counters[1];
         plan->n_generic = n_gen;
         plan->n_empty = n_empty;
+        plan->n_partials = n_part;
+
+        // partial-sum slots of the multi-combo cells
+        if ((rc2 = dev_alloc(&head_scan, size_t(n_part) + 1, "multi heads"))) return rc2;
+        fill(head_scan, int64_t(n_part) + 1, 0);
+        if (n_part > 0) {
+            hipLaunchKernelGGL(k_multi_compact, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream,
+                               combo_cell, combo_flag, int32_t(n_combo), keys_a, vals_a);
+            if ((rc2 = radix_sort(keys_a, vals_a, n_part, bits_for(n_cells)))) return rc2;
+            hipLaunchKernelGGL(k_multi_slots, dim3(blocks_for(n_part)), dim3(kBlock), 0, stream,
+                               keys_a, vals_a, n_part, plan->column_table, head_scan);
+        }
+        scan_with_total(head_scan, n_part, small + 3, stream);
+        BEVPOOL_HIP(hipGetLastError());
+        int32_t n_multi;
+        if ((rc2 = to_host(&n_multi, head_scan + n_part))) return rc2;
+        BEVPOOL_HIP(hipStreamSynchronize(stream));
+        plan->n_multi = n_multi;
+        if ((rc2 = dev_alloc(&plan->multi_begin, size_t(n_multi) + 1, "multi_begin"))) return rc2;
+        if ((rc2 = dev_alloc(&plan->multi_cell, size_t(n_multi), "multi_cell"))) return rc2;
+        hipLaunchKernelGGL(k_multi_cells, dim3(blocks_for(int64_t(n_part) + 1)), dim3(kBlock), 0,
+                           stream, keys_a, head_scan, n_part, plan->multi_begin, plan->multi_cell);
+        BEVPOOL_HIP(hipGetLastError());
 
         // cells without points, and generic cells by descending point count
         if ((rc2 = dev_alloc(&plan->empty_cells, size_t(n_empty), "empty_cells"))) return rc2;

@@ -39,9 +39,15 @@ def pkg(torch_cuda):
 
 
 def _coarse_rig():
-    """The nuScenes rig on a 3 m grid: cells with thousands of points, fed by
-    combos of several column items (generic cells summed by a workgroup)."""
+    """The nuScenes rig on a 3 m grid: cells with thousands of points, each
+    fed by many combos (partial-sum slots added by the second kernel)."""
     return dataclasses.replace(wl.ring_rig(), nx=36, ny=36, cell_x=3.0, cell_y=3.0)
+
+
+def _coarse_tilted_rig():
+    """The tilted rig on a 3 m grid: generic cells with thousands of points,
+    summed by a whole workgroup over many 64-run chunks."""
+    return dataclasses.replace(wl.tilt_rig(wl.ring_rig()), nx=36, ny=36, cell_x=3.0, cell_y=3.0)
 
 
 def _anisotropic_rig():
@@ -66,7 +72,8 @@ def _one_cell_rig():
 RIGS = {
     "tiny": wl.tiny_rig, "tiny_identity": wl.identity_rig, "nuscenes": wl.ring_rig,
     "nuscenes_tilted": lambda: wl.tilt_rig(wl.ring_rig()), "highres": lambda: wl.ring_rig(2),
-    "anisotropic": _anisotropic_rig, "coarse": _coarse_rig, "empty": _empty_rig,
+    "anisotropic": _anisotropic_rig, "coarse": _coarse_rig, "coarse_tilted": _coarse_tilted_rig,
+    "empty": _empty_rig,
     "one_cell": _one_cell_rig,
 }
 
@@ -180,7 +187,7 @@ def test_forward_highres(torch_cuda, pkg, oracle_lib, oracle_plans):
     _check_fp32(got, ref, np.diff(cs))
 
 
-@pytest.mark.parametrize("name", ["coarse", "anisotropic", "empty", "one_cell"])
+@pytest.mark.parametrize("name", ["coarse", "coarse_tilted", "anisotropic", "empty", "one_cell"])
 def test_forward_edge_rigs(torch_cuda, pkg, oracle_lib, oracle_plans, name):
     _say(f"[forward edge] {name}")
     rig = RIGS[name]()
@@ -193,7 +200,9 @@ def test_forward_edge_rigs(torch_cuda, pkg, oracle_lib, oracle_plans, name):
     _check_fp32(got, ref, np.diff(cs))
     if name == "coarse":
         assert plan.info.max_per_cell > 1536
-        assert plan.info.n_generic > 0            # exercises the heavy generic role
+        assert plan.info.n_partials > 0           # exercises the partial-sum combine
+    if name == "coarse_tilted":
+        assert plan.info.n_generic > 0 and plan.info.max_per_cell > 1536   # heavy generic cells
     if name == "empty":
         assert plan.info.n_kept == 0 and (got == 0).all()
 
@@ -267,8 +276,8 @@ def test_plan_reuse_and_shape_checks(torch_cuda, pkg):
 
 @pytest.mark.parametrize("name", ["nuscenes", "nuscenes_tilted", "coarse", "anisotropic", "tiny"])
 def test_plan_partition_counts(pkg, oracle_plans, name):
-    """Every cell is column-served, generic or empty; the level rig is
-    served almost entirely by column items."""
+    """Every cell is column-served, generic or empty; the level rig has no
+    generic cell at all."""
     rig = RIGS[name]()
     plan = pkg.Plan.from_rig(rig)
     info = plan.info
@@ -277,5 +286,5 @@ def test_plan_partition_counts(pkg, oracle_plans, name):
     assert info.n_empty == int((counts == 0).sum())
     assert info.n_runs >= info.n_generic
     if name == "nuscenes":
-        assert info.n_column > 0.8 * info.n_nonempty
+        assert info.n_generic == 0 and info.n_partials > 0
     plan.close()
