@@ -113,36 +113,53 @@ BEVPOOL_API int bevpool_plan(const double *intrinsics, const double *extrinsics,
 
 /*
  * Pool one batch of frames with a plan (Sec. III-B: lift P x F, sum each
- * cell's points; "Interval Reduction": the result is written per cell,
- * without partial sums in memory).
+ * cell's points; "Interval Reduction": each cell's sum is written once).
  *
  *  depth_prob: device [batch][N][D][H][W] of dtype.
  *  cam_feat:   device [batch][N][H][W][channels] of dtype.
  *  bev_out:    device float [batch][ny][nx][channels]. Every element is
  *              overwritten, and cells with no kept point are set to 0.
- *  batch, channels >= 1. N, D, H, W, nx and ny come from the plan; the
- *  caller's buffers must have those sizes (the library cannot see them).
+ *  batch in 1..65535, channels >= 1. N, D, H, W, nx and ny come from the
+ *  plan; the caller's buffers must have those sizes (the library cannot see
+ *  them).
  *
  * out[b][cell][c] = sum over kept points p of cell of
  * depth_prob[b][p] * cam_feat[b][pixel(p)][c]. The sum is accumulated in fp32
  * in an order fixed by the plan, so repeated calls give bitwise equal
- * results. bev_out is written with plain stores, no atomics.
+ * results. No atomics touch bev_out. A cell fed by several (camera, depth
+ * bin, pixel column) combos is summed in two steps: the combos' partial sums
+ * are parked in rows of bev_out that belong to empty cells, then added in a
+ * fixed order by a second kernel, which also zeroes those rows.
  *
  * Inputs must be finite; non-finite inputs give unspecified output.
  * Asynchronous on hip_stream: no host synchronisation, no allocation.
- * Inputs must not overlap bev_out.
- * The fast path needs channels % 4 == 0 and 16-byte aligned cam_feat and
- * bev_out (8-byte aligned cam_feat for 16-bit dtypes); other cases take a
- * slower path with the same results.
- * A plan may be used from several streams at once.
- * Errors: INVALID_ARG (null pointer or a bad plan handle, batch or
- * channels < 1), UNSUPPORTED_DTYPE, OVERFLOW (N*H*W*channels or
- * nx*ny*channels does not fit in int32), HIP (launch failure).
+ * Inputs must not overlap bev_out. Buffers need only element alignment;
+ * 16-byte aligned bev_out with channels % 4 == 0 zeroes empty rows with
+ * 16-byte stores.
+ * A plan is not modified by the forward pass and may be used from several
+ * streams at once (with distinct output buffers).
+ * Errors: INVALID_ARG (null pointer or a bad plan handle, batch outside
+ * 1..65535, channels < 1), UNSUPPORTED_DTYPE, OVERFLOW (one frame's
+ * depth_prob, cam_feat or bev_out reaches 2 GiB), HIP (launch failure).
  */
 BEVPOOL_API int bevpool_forward(const void *depth_prob, const void *cam_feat,
                     const bevpool_plan_t *plan, float *bev_out,
                     int32_t batch, int32_t channels, int32_t dtype,
                     void *hip_stream);
+
+/*
+ * bevpool_forward with kernel-boundary timing, for measurement: start_event
+ * and stop_event (hipEvent_t handles created by the caller; either may be
+ * NULL) are recorded by the first and the last kernel dispatch of the
+ * forward pass itself, so hipEventElapsedTime(start, stop) is the GPU time
+ * of the forward pass without the queue gaps that events recorded as
+ * separate stream entries add (several microseconds on MI355X). Arguments,
+ * results and errors are otherwise those of bevpool_forward.
+ */
+BEVPOOL_API int bevpool_forward_timed(const void *depth_prob, const void *cam_feat,
+                          const bevpool_plan_t *plan, float *bev_out,
+                          int32_t batch, int32_t channels, int32_t dtype,
+                          void *hip_stream, void *start_event, void *stop_event);
 
 /* Sizes of a plan. All counts are per frame. */
 typedef struct {

@@ -15,12 +15,14 @@ import numpy as np
 
 from . import _binding
 from ._binding import (BEVPOOL_BF16, BEVPOOL_F16, BEVPOOL_F32, BevpoolError,
-                       bevpool_forward, bevpool_geometry, bevpool_last_error,
+                       bevpool_forward, bevpool_forward_timed, bevpool_geometry,
+                       bevpool_last_error,
                        bevpool_plan, bevpool_plan_destroy, bevpool_plan_export,
                        bevpool_plan_info_get, bevpool_version)
 
 __all__ = [
-    "Plan", "BevpoolError", "bevpool_plan", "bevpool_forward", "bevpool_plan_info_get",
+    "Plan", "BevpoolError", "bevpool_plan", "bevpool_forward", "bevpool_forward_timed",
+    "bevpool_plan_info_get",
     "bevpool_plan_export", "bevpool_plan_destroy", "bevpool_last_error", "bevpool_version",
     "bevpool_geometry", "geometry_of", "BEVPOOL_F32", "BEVPOOL_BF16", "BEVPOOL_F16",
 ]
@@ -90,9 +92,12 @@ class Plan:
         bevpool_plan_export(self.handle, cop, sp, cs)
         return cop, sp, cs
 
-    def forward(self, depth_prob, cam_feat, out=None, stream=None):
+    def forward(self, depth_prob, cam_feat, out=None, stream=None, events=None):
         """depth_prob [B][N][D][H][W], cam_feat [B][N][H][W][C] device tensors
-        of one dtype (fp32, bf16 or fp16); returns fp32 [B][ny][nx][C]."""
+        of one dtype (fp32, bf16 or fp16); returns fp32 [B][ny][nx][C].
+        events: optional (start, stop) pair of timing-enabled torch.cuda.Event,
+        recorded by the forward's own first and last kernel dispatch
+        (bevpool_forward_timed)."""
         torch = _torch()
         i = self.info
         if depth_prob.dim() != 5 or cam_feat.dim() != 5:
@@ -120,6 +125,15 @@ class Plan:
                                "out must be a contiguous fp32 device tensor [B][ny][nx][C]")
         if stream is None:
             stream = torch.cuda.current_stream(cam_feat.device)
-        bevpool_forward(depth_prob.data_ptr(), cam_feat.data_ptr(), self.handle, out.data_ptr(),
-                        B, C, _dtype_code(cam_feat), stream.cuda_stream)
+        if events is None:
+            bevpool_forward(depth_prob.data_ptr(), cam_feat.data_ptr(), self.handle,
+                            out.data_ptr(), B, C, _dtype_code(cam_feat), stream.cuda_stream)
+        else:
+            start, stop = events
+            for e in (start, stop):
+                if e.cuda_event == 0:       # torch creates the HIP event on first record
+                    e.record(stream)
+            bevpool_forward_timed(depth_prob.data_ptr(), cam_feat.data_ptr(), self.handle,
+                                  out.data_ptr(), B, C, _dtype_code(cam_feat), stream.cuda_stream,
+                                  start.cuda_event, stop.cuda_event)
         return out

@@ -36,7 +36,6 @@ void free_plan(bevpool_plan_s *plan) {
     (void)hipFree(plan->empty_cells);
     (void)hipFree(plan->multi_begin);
     (void)hipFree(plan->multi_cell);
-    (void)hipFree(plan->scratch);
     if (prev >= 0 && prev != plan->device) (void)hipSetDevice(prev);
     plan->magic = 0;
     delete plan;
@@ -113,9 +112,10 @@ int bevpool_plan(const double *intrinsics, const double *extrinsics, const bevpo
     return BEVPOOL_OK;
 }
 
-int bevpool_forward(const void *depth_prob, const void *cam_feat, const bevpool_plan_t *plan,
+namespace {
+int forward_checked(const void *depth_prob, const void *cam_feat, const bevpool_plan_t *plan,
                     float *bev_out, int32_t batch, int32_t channels, int32_t dtype,
-                    void *hip_stream) {
+                    void *hip_stream, void *start_event, void *stop_event) {
     if (!valid_plan(plan)) return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "invalid plan handle");
     if (!depth_prob || !cam_feat || !bev_out)
         return bevpool_fail(BEVPOOL_ERR_INVALID_ARG,
@@ -126,7 +126,23 @@ int bevpool_forward(const void *depth_prob, const void *cam_feat, const bevpool_
     if (dtype != BEVPOOL_F32 && dtype != BEVPOOL_BF16 && dtype != BEVPOOL_F16)
         return bevpool_fail(BEVPOOL_ERR_UNSUPPORTED_DTYPE, "dtype %d is not F32, BF16 or F16", dtype);
     return bevpool_launch_forward(depth_prob, cam_feat, plan, bev_out, batch, channels, dtype,
-                                  hipStream_t(hip_stream));
+                                  hipStream_t(hip_stream), hipEvent_t(start_event),
+                                  hipEvent_t(stop_event));
+}
+}  // namespace
+
+int bevpool_forward(const void *depth_prob, const void *cam_feat, const bevpool_plan_t *plan,
+                    float *bev_out, int32_t batch, int32_t channels, int32_t dtype,
+                    void *hip_stream) {
+    return forward_checked(depth_prob, cam_feat, plan, bev_out, batch, channels, dtype, hip_stream,
+                           nullptr, nullptr);
+}
+
+int bevpool_forward_timed(const void *depth_prob, const void *cam_feat, const bevpool_plan_t *plan,
+                          float *bev_out, int32_t batch, int32_t channels, int32_t dtype,
+                          void *hip_stream, void *start_event, void *stop_event) {
+    return forward_checked(depth_prob, cam_feat, plan, bev_out, batch, channels, dtype, hip_stream,
+                           start_event, stop_event);
 }
 
 int bevpool_plan_info_get(const bevpool_plan_t *plan, bevpool_plan_info *info) {

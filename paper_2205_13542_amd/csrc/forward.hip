@@ -39,6 +39,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <hip/hip_ext.h>
+
 #include "internal.h"
 
 namespace bevpool {
@@ -83,30 +85,28 @@ __device__ __forceinline__ void store_f32(Rsrc r, uint32_t off, float v) {
 
 struct FwdArgs {
     const char *P, *F;
-    float *out, *part;
+    float *out;
     const int2 *table;
     const int4 *gen_hdr;
     const int4 *gen_runs;
     const int32_t *empty_cells;
     int32_t N, D, H, W, HW;
     int32_t n_cells, C, slice_c;
-    uint32_t p_bytes, f_bytes, o_bytes, s_bytes, run_bytes;   // per frame (runs: whole table)
+    uint32_t p_bytes, f_bytes, o_bytes, run_bytes;   // per frame (runs: whole table)
     int32_t items_d, items_w, n_items;
-    int32_t n_heavy, n_light, n_empty;
+    int32_t n_heavy, n_light, n_empty, n_partials;
     int32_t base_col, base_zero, base_light;
     int32_t zero_vec, zero_units;       // empty rows: float4 units (or floats) per row
     FastDiv div_units;
 };
 
-// The buffers of frame b: depth probabilities, features, BEV map and the
-// partial-sum slots.
+// The buffers of frame b: depth probabilities, features, BEV map.
 struct Frame {
-    Rsrc P, F, O, S;
+    Rsrc P, F, O;
     __device__ __forceinline__ Frame(const FwdArgs &a, int b)
         : P(make_rsrc(a.P + int64_t(b) * a.p_bytes, a.p_bytes)),
           F(make_rsrc(a.F + int64_t(b) * a.f_bytes, a.f_bytes)),
-          O(make_rsrc(reinterpret_cast<const char *>(a.out) + int64_t(b) * a.o_bytes, a.o_bytes)),
-          S(make_rsrc(reinterpret_cast<const char *>(a.part) + int64_t(b) * a.s_bytes, a.s_bytes)) {}
+          O(make_rsrc(reinterpret_cast<const char *>(a.out) + int64_t(b) * a.o_bytes, a.o_bytes)) {}
 };
 
 constexpr int kStages = 6;                      // row-pair stages in flight per wave
@@ -178,41 +178,38 @@ __device__ __forceinline__ void apply_row(float (&acc)[kColDepth][NCH], const fl
         for (int k = 0; k < NCH; ++k) acc[J][k] = __builtin_fmaf(pb[J], f.v[k], acc[J][k]);
 }
 
-// After the row loop: each depth bin's sums go to its single-combo cell's
-// row of the BEV map, or to the partial-sum slot of its combo. Lane J of
-// the group holds the entry of depth bin J.
+// After the row loop: each depth bin's sums go to the BEV row named by its
+// table entry: its single-combo cell, or the borrowed empty-cell row that
+// holds the partial sum of its combo. Lane J of the group holds the entry of
+// depth bin J.
 template <int J, int NCH>
 struct Emit {
-    static __device__ __forceinline__ void run(const float (&acc)[kColDepth][NCH], int ex, int ey,
-                                               uint32_t dm, Rsrc out, Rsrc part, uint32_t ch_off,
-                                               int C, bool tail_ok) {
+    static __device__ __forceinline__ void run(const float (&acc)[kColDepth][NCH], int ex,
+                                               uint32_t dm, Rsrc out, uint32_t ch_off, int C,
+                                               bool tail_ok) {
         if (dm & (1u << J)) {
             const int x = row_bcast<J>(ex);
-            const uint32_t y = uint32_t(row_bcast<J>(ey));
-            if (x >= 0) {
-                const uint32_t off = uint32_t(x) * uint32_t(C) * 4u + ch_off;
-                if (y & kComboMulti)
-                    store_row<NCH>(part, off, acc[J], tail_ok);
-                else
-                    store_row<NCH>(out, off, acc[J], tail_ok);
-            }
+            store_row<NCH>(out, x >= 0 ? uint32_t(x) * uint32_t(C) * 4u + ch_off : kOff, acc[J],
+                           tail_ok);
         }
-        Emit<J + 1, NCH>::run(acc, ex, ey, dm, out, part, ch_off, C, tail_ok);
+        Emit<J + 1, NCH>::run(acc, ex, dm, out, ch_off, C, tail_ok);
     }
 };
 template <int NCH>
 struct Emit<kColDepth, NCH> {
-    static __device__ __forceinline__ void run(const float (&)[kColDepth][NCH], int, int, uint32_t,
-                                               Rsrc, Rsrc, uint32_t, int, bool) {}
+    static __device__ __forceinline__ void run(const float (&)[kColDepth][NCH], int, uint32_t, Rsrc,
+                                               uint32_t, int, bool) {}
 };
 
-// Rows of kZeroCells listed empty cells of frame b (in slice 0 only),
+// Rows of kZeroCells listed empty cells of frame b (in slice 0 only), from
+// entry n_partials on (the rows before it hold partial sums and are zeroed
+// by the combine kernel),
 // written as one flat sequence of 16-byte (or 4-byte) units: unit f is unit
 // f % U of row f / U. Rows of consecutive cells are adjacent in memory, so
 // runs of empty cells become contiguous stores. The cell ids are staged in
 // LDS first, so no store waits on a load.
 __device__ void zero_rows(const FwdArgs &a, int zb, int b, int *s_cell) {
-    const int e0 = zb * kZeroCells;
+    const int e0 = a.n_partials + zb * kZeroCells;
     const int ne = min(kZeroCells, a.n_empty - e0);
     if (int(threadIdx.x) < ne) s_cell[threadIdx.x] = a.empty_cells[e0 + threadIdx.x];
     __syncthreads();
@@ -311,7 +308,7 @@ __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0,
         }
     }
 
-    Emit<0, NCH>::run(acc, e.x, e.y, dm, fr.O, fr.S, uint32_t(c0 + j) * 4u, a.C, tail_ok);
+    Emit<0, NCH>::run(acc, e.x, dm, fr.O, uint32_t(c0 + j) * 4u, a.C, tail_ok);
 }
 
 // A generic cell's runs in chunks of 64: lane i loads run i of the chunk and
@@ -422,17 +419,18 @@ __global__ __launch_bounds__(kBlock) void k_forward(FwdArgs a) {
 }
 
 // Cells fed by several combos: the slots of multi-combo cell k are
-// multi_begin[k] .. multi_begin[k+1]-1, added in that order. One group of 16
-// lanes per cell, channels j, j + 16, ...
+// multi_begin[k] .. multi_begin[k+1]-1, slot s held in the BEV row of empty
+// cell empty_cells[s]. They are added in slot order into the cell's row,
+// and the borrowed rows are zeroed. One group of 16 lanes per cell,
+// channels j, j + 16, ...
 constexpr int kCombineChunks = 5;   // 16-channel chunks per pass (80 channels)
 constexpr int kCombineSlots = 4;    // slots loaded per step
 
 struct CombineArgs {
-    const float *part;
     float *out;
-    const int32_t *multi_begin, *multi_cell;
-    int32_t n_multi, C, n_cells, n_partials;
-    uint32_t o_bytes, s_bytes;
+    const int32_t *multi_begin, *multi_cell, *empty_cells;
+    int32_t n_multi, C;
+    uint32_t o_bytes;
 };
 
 __global__ __launch_bounds__(kBlock) void k_combine(CombineArgs a) {
@@ -440,29 +438,37 @@ __global__ __launch_bounds__(kBlock) void k_combine(CombineArgs a) {
     const int k = blockIdx.x * kColWidth + int(threadIdx.x >> 4);
     if (k >= a.n_multi) return;
     const int j = threadIdx.x & 15;
-    const Rsrc S = make_rsrc(reinterpret_cast<const char *>(a.part) + int64_t(b) * a.s_bytes, a.s_bytes);
     const Rsrc O = make_rsrc(reinterpret_cast<const char *>(a.out) + int64_t(b) * a.o_bytes, a.o_bytes);
     const int s0 = a.multi_begin[k], s1 = a.multi_begin[k + 1];
-    const uint32_t obase = uint32_t(a.multi_cell[k]) * uint32_t(a.C) * 4u;
     const uint32_t row = uint32_t(a.C) * 4u;
+    const uint32_t obase = uint32_t(a.multi_cell[k]) * row;
     for (int c = j; c < a.C; c += kCombineChunks * 16) {
         float sum[kCombineChunks];
 #pragma unroll
         for (int q = 0; q < kCombineChunks; ++q) sum[q] = 0.f;
         // kCombineSlots slots' loads in flight at a time, added in slot order
         for (int sl = s0; sl < s1; sl += kCombineSlots) {
+            uint32_t rb[kCombineSlots];
+#pragma unroll
+            for (int u = 0; u < kCombineSlots; ++u)
+                rb[u] = sl + u < s1 ? uint32_t(a.empty_cells[sl + u]) * row : kOff;
             float v[kCombineSlots][kCombineChunks];
 #pragma unroll
             for (int u = 0; u < kCombineSlots; ++u)
 #pragma unroll
                 for (int q = 0; q < kCombineChunks; ++q)
                     v[u][q] = Elem<BEVPOOL_F32>::load(
-                        S, (sl + u < s1 && c + 16 * q < a.C) ? uint32_t(sl + u) * row + uint32_t(c + 16 * q) * 4u : kOff);
+                        O, c + 16 * q < a.C ? rb[u] + uint32_t(c + 16 * q) * 4u : kOff);
 #pragma unroll
             for (int u = 0; u < kCombineSlots; ++u)
 #pragma unroll
                 for (int q = 0; q < kCombineChunks; ++q)
                     if (sl + u < s1) sum[q] += v[u][q];
+#pragma unroll
+            for (int u = 0; u < kCombineSlots; ++u)
+#pragma unroll
+                for (int q = 0; q < kCombineChunks; ++q)
+                    store_f32(O, c + 16 * q < a.C ? rb[u] + uint32_t(c + 16 * q) * 4u : kOff, 0.f);
         }
 #pragma unroll
         for (int q = 0; q < kCombineChunks; ++q)
@@ -470,14 +476,16 @@ __global__ __launch_bounds__(kBlock) void k_combine(CombineArgs a) {
     }
 }
 
+// Kernel-boundary events (either may be null): they take the timestamps of
+// the dispatch itself rather than of separate queue entries.
 template <int DT>
-void launch_dtype(const FwdArgs &a, dim3 grid, int nch, hipStream_t s) {
+void launch_dtype(const FwdArgs &a, dim3 grid, int nch, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     switch (nch) {
-        case 1: hipLaunchKernelGGL((k_forward<DT, 1>), grid, dim3(kBlock), 0, s, a); break;
-        case 2: hipLaunchKernelGGL((k_forward<DT, 2>), grid, dim3(kBlock), 0, s, a); break;
-        case 3: hipLaunchKernelGGL((k_forward<DT, 3>), grid, dim3(kBlock), 0, s, a); break;
-        case 4: hipLaunchKernelGGL((k_forward<DT, 4>), grid, dim3(kBlock), 0, s, a); break;
-        default: hipLaunchKernelGGL((k_forward<DT, 5>), grid, dim3(kBlock), 0, s, a); break;
+        case 1: hipExtLaunchKernelGGL((k_forward<DT, 1>), grid, dim3(kBlock), 0, s, e0, e1, 0, a); break;
+        case 2: hipExtLaunchKernelGGL((k_forward<DT, 2>), grid, dim3(kBlock), 0, s, e0, e1, 0, a); break;
+        case 3: hipExtLaunchKernelGGL((k_forward<DT, 3>), grid, dim3(kBlock), 0, s, e0, e1, 0, a); break;
+        case 4: hipExtLaunchKernelGGL((k_forward<DT, 4>), grid, dim3(kBlock), 0, s, e0, e1, 0, a); break;
+        default: hipExtLaunchKernelGGL((k_forward<DT, 5>), grid, dim3(kBlock), 0, s, e0, e1, 0, a); break;
     }
 }
 
@@ -488,43 +496,24 @@ int round8(int x) { return (x + 7) & ~7; }
 
 using namespace bevpool;
 
-int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *cplan, float *out,
-                           int32_t batch, int32_t channels, int32_t dtype, hipStream_t stream) {
-    // The plan's partial-sum scratch grows here; the rest of the plan is
-    // read-only for the forward pass.
-    bevpool_plan_s *plan = const_cast<bevpool_plan_s *>(cplan);
+int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *plan, float *out,
+                           int32_t batch, int32_t channels, int32_t dtype, hipStream_t stream,
+                           hipEvent_t start, hipEvent_t stop) {
     const bevpool_geometry &g = plan->geom;
     const int64_t n_pix = int64_t(g.n_cams) * g.feat_h * g.feat_w;
     const int64_t esize = dtype == BEVPOOL_F32 ? 4 : 2;
     const int64_t p_bytes = plan->n_points * esize;
     const int64_t f_bytes = n_pix * channels * esize;
     const int64_t o_bytes = int64_t(plan->n_cells) * channels * 4;
-    const int64_t s_bytes = int64_t(plan->n_partials) * channels * 4;
     const int64_t run_bytes = int64_t(plan->n_runs) * 16;
     constexpr int64_t kLimit = int64_t(1) << 31;
-    if (p_bytes >= kLimit || f_bytes >= kLimit || o_bytes >= kLimit || s_bytes >= kLimit ||
-        run_bytes >= kLimit)
+    if (p_bytes >= kLimit || f_bytes >= kLimit || o_bytes >= kLimit || run_bytes >= kLimit)
         return bevpool_fail(BEVPOOL_ERR_OVERFLOW,
                             "channels=%d: one frame's depth (%lld B), feature (%lld B) or BEV "
                             "(%lld B) tensor reaches 2 GiB", channels, (long long)p_bytes,
                             (long long)f_bytes, (long long)o_bytes);
     if (batch > 65535)
         return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "batch=%d exceeds 65535 frames per call", batch);
-
-    const size_t need = size_t(s_bytes) * size_t(batch);
-    if (need > plan->scratch_bytes) {
-        BEVPOOL_HIP(hipStreamSynchronize(stream));
-        (void)hipFree(plan->scratch);
-        plan->scratch = nullptr;
-        plan->scratch_bytes = 0;
-        hipError_t e = hipMalloc(reinterpret_cast<void **>(&plan->scratch), need);
-        if (e != hipSuccess) {
-            (void)hipGetLastError();
-            return bevpool_fail(BEVPOOL_ERR_OOM, "out of device memory for %zu bytes of partial sums",
-                                need);
-        }
-        plan->scratch_bytes = need;
-    }
 
     const int n_slices = (channels + kSliceChannels - 1) / kSliceChannels;
     const int slice_c = (channels + n_slices - 1) / n_slices;
@@ -534,7 +523,6 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *c
     a.P = static_cast<const char *>(P);
     a.F = static_cast<const char *>(F);
     a.out = out;
-    a.part = plan->scratch;
     a.table = plan->column_table;
     a.gen_hdr = plan->generic_hdr;
     a.gen_runs = plan->generic_runs;
@@ -550,7 +538,6 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *c
     a.p_bytes = uint32_t(p_bytes);
     a.f_bytes = uint32_t(f_bytes);
     a.o_bytes = uint32_t(o_bytes);
-    a.s_bytes = uint32_t(s_bytes);
     a.run_bytes = uint32_t(run_bytes);
     a.items_d = (g.n_depth + kColDepth - 1) / kColDepth;
     a.items_w = (g.feat_w + kColWidth - 1) / kColWidth;
@@ -558,35 +545,35 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *c
     a.n_heavy = plan->n_generic_heavy;
     a.n_light = plan->n_generic - plan->n_generic_heavy;
     a.n_empty = plan->n_empty;
+    a.n_partials = plan->n_partials;
     a.base_col = round8(a.n_heavy);
     a.base_zero = round8(a.base_col + a.n_items);
-    a.base_light = a.base_zero + (a.n_empty + kZeroCells - 1) / kZeroCells;
+    a.base_light = a.base_zero + (a.n_empty - a.n_partials + kZeroCells - 1) / kZeroCells;
     a.zero_vec = (channels % 4 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0) ? 1 : 0;
     a.zero_units = a.zero_vec ? channels / 4 : channels;
     a.div_units = make_fastdiv(uint32_t(a.zero_units));
     const int n_blocks = a.base_light + (a.n_light + kWaves - 1) / kWaves;
 
+    // the last kernel of the forward carries the stop event
+    const bool combine = plan->n_multi > 0;
     const dim3 grid(n_blocks, batch, n_slices);
     switch (dtype) {
-        case BEVPOOL_F32: launch_dtype<BEVPOOL_F32>(a, grid, nch, stream); break;
-        case BEVPOOL_BF16: launch_dtype<BEVPOOL_BF16>(a, grid, nch, stream); break;
-        default: launch_dtype<BEVPOOL_F16>(a, grid, nch, stream); break;
+        case BEVPOOL_F32: launch_dtype<BEVPOOL_F32>(a, grid, nch, stream, start, combine ? nullptr : stop); break;
+        case BEVPOOL_BF16: launch_dtype<BEVPOOL_BF16>(a, grid, nch, stream, start, combine ? nullptr : stop); break;
+        default: launch_dtype<BEVPOOL_F16>(a, grid, nch, stream, start, combine ? nullptr : stop); break;
     }
     BEVPOOL_HIP(hipGetLastError());
-    if (plan->n_multi > 0) {
+    if (combine) {
         CombineArgs ca;
-        ca.part = plan->scratch;
         ca.out = out;
         ca.multi_begin = plan->multi_begin;
         ca.multi_cell = plan->multi_cell;
+        ca.empty_cells = plan->empty_cells;
         ca.n_multi = plan->n_multi;
         ca.C = channels;
-        ca.n_cells = plan->n_cells;
-        ca.n_partials = plan->n_partials;
         ca.o_bytes = uint32_t(o_bytes);
-        ca.s_bytes = uint32_t(s_bytes);
-        hipLaunchKernelGGL(k_combine, dim3((plan->n_multi + kColWidth - 1) / kColWidth, batch),
-                           dim3(kBlock), 0, stream, ca);
+        hipExtLaunchKernelGGL(k_combine, dim3((plan->n_multi + kColWidth - 1) / kColWidth, batch),
+                              dim3(kBlock), 0, stream, nullptr, stop, 0, ca);
         BEVPOOL_HIP(hipGetLastError());
     }
     return BEVPOOL_OK;

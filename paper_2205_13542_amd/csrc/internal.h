@@ -22,8 +22,11 @@ namespace bevpool {
 // block's combos held in registers (column items of kColDepth x
 // kColWidth combos of one camera). A cell fed by one combo is stored from
 // registers. A cell fed by several combos (near the rig a cell spans
-// several pixel columns) gets one partial-sum slot per combo, and a second
-// kernel adds the slots of each such cell in slot order. Every other cell
+// several pixel columns) gets one partial-sum slot per combo; slot s is the
+// output row of the s-th empty cell, which is free until zeroed. A second
+// kernel adds the slots of each such cell in slot order and then zeroes the
+// borrowed rows. (A grid with fewer empty cells than slots serves these
+// cells generically instead.) Every other cell
 // with points is "generic": its points are gathered in runs of consecutive
 // depth bins of one pixel, by one wave, or by a whole workgroup when it has
 // more than kGenHeavy points. Cells without points are zeroed by
@@ -37,8 +40,8 @@ constexpr int kColWidth = kBlock / kGroupLanes; // 16 columns per item
 constexpr int kGenHeavy = 256;
 constexpr int kSliceChannels = 80;              // channels per pass
 
-// Column-table entry: {cell (single-combo cell) or partial slot (multi),
-// h_lo | h_hi << 16 | kComboMulti}.
+// Column-table entry: {cell (single-combo cell) or borrowed row of its
+// partial slot (multi), h_lo | h_hi << 16 | kComboMulti}.
 constexpr uint32_t kComboMulti = 1u << 31;
 constexpr int kMaxFeatH = 1 << 14;              // rows must fit the 15-bit fields
 
@@ -77,11 +80,9 @@ struct bevpool_plan_s {
     int32_t *sorted_point;   // [n_points]: kept ids by (cell, id), then dropped ids
     int32_t *cell_start;     // [n_cells + 1]
     // forward work partition
-    int2 *column_table;      // [N][D][W]: {cell, slot or -1, h_lo | h_hi << 16 | flags}
+    int2 *column_table;      // [N][D][W]: {cell or borrowed row or -1, h_lo | h_hi << 16 | flags}
     int32_t *multi_begin;    // [n_multi + 1]: first partial slot of each multi-combo cell
     int32_t *multi_cell;     // [n_multi]
-    float *scratch;          // partial sums, [batch][n_partials][channels], grown on demand
-    size_t scratch_bytes;
     int4 *generic_hdr;       // [n_generic]: {cell, first run, runs, points}, most points first
     int4 *generic_runs;      // [n_runs]: {first point id, pixel, depth bins, 0}
     int32_t *empty_cells;    // [n_empty] cells without points, ascending
@@ -105,4 +106,5 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
                        bevpool_plan_s *plan);
 int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *plan,
                            float *out, int32_t batch, int32_t channels,
-                           int32_t dtype, hipStream_t stream);
+                           int32_t dtype, hipStream_t stream, hipEvent_t start,
+                           hipEvent_t stop);

@@ -348,6 +348,19 @@ __global__ __launch_bounds__(kBlock) void k_combo_table(ComboArgs a, int2 *table
     multi_flag[X] = multi ? 1 : 0;
 }
 
+// Not enough empty rows to hold the partial sums: cells fed by several
+// combos become generic.
+__global__ __launch_bounds__(kBlock) void k_demote_multi(ComboArgs a, int32_t n_cells) {
+    const int32_t c = blockIdx.x * kBlock + threadIdx.x;
+    if (c < n_cells && a.cell_generic[c] == 0 && a.cell_ncombo[c] > 1) a.cell_generic[c] = 1;
+}
+
+__global__ __launch_bounds__(kBlock) void k_empty_list(const int32_t *empty_pos, int32_t n_cells,
+                                                       int32_t *empty_cells) {
+    const int32_t c = blockIdx.x * kBlock + threadIdx.x;
+    if (c < n_cells && empty_pos[c + 1] != empty_pos[c]) empty_cells[empty_pos[c]] = c;
+}
+
 // Combos of multi-combo cells as (cell, combo) pairs in combo order.
 __global__ __launch_bounds__(kBlock) void k_multi_compact(const int32_t *combo_cell,
                                                           const int32_t *multi_pos, int32_t n_combo,
@@ -359,13 +372,16 @@ __global__ __launch_bounds__(kBlock) void k_multi_compact(const int32_t *combo_c
 }
 
 // After the stable sort by cell, position i is the partial-sum slot of combo
-// val[i]: a cell's slots are contiguous and in combo order. The table entry
-// of the combo then names its slot; cell heads are flagged.
+// val[i]: a cell's slots are contiguous and in combo order. Slot i is kept in
+// the BEV row of empty cell i (the output has a row for every cell, and the
+// rows of empty cells are free until they are zeroed), so the table entry of
+// the combo names that row; cell heads are flagged.
 __global__ __launch_bounds__(kBlock) void k_multi_slots(const uint32_t *key, const int32_t *val,
-                                                        int32_t n, int2 *table, int32_t *head_flag) {
+                                                        int32_t n, const int32_t *empty_cells,
+                                                        int2 *table, int32_t *head_flag) {
     const int32_t i = blockIdx.x * kBlock + threadIdx.x;
     if (i >= n) return;
-    table[val[i]].x = i;
+    table[val[i]].x = empty_cells[i];
     head_flag[i] = (i == 0 || key[i] != key[i - 1]) ? 1 : 0;
 }
 
@@ -384,21 +400,15 @@ __global__ __launch_bounds__(kBlock) void k_multi_cells(const uint32_t *key, con
     }
 }
 
-// Generic cells keyed for a descending sort by point count; empty cells
-// listed in ascending order.
-__global__ __launch_bounds__(kBlock) void k_compact_classes(const int32_t *cell_start, int32_t n_cells,
+// Generic cells keyed for a descending sort by point count.
+__global__ __launch_bounds__(kBlock) void k_compact_generic(const int32_t *cell_start, int32_t n_cells,
                                                             const int32_t *generic_pos,
-                                                            const int32_t *empty_pos,
                                                             int32_t max_per_cell, uint32_t *gen_key,
-                                                            int32_t *gen_cell, int32_t *empty_cells) {
+                                                            int32_t *gen_cell) {
     const int32_t c = blockIdx.x * kBlock + threadIdx.x;
-    if (c >= n_cells) return;
-    const int32_t cnt = cell_start[c + 1] - cell_start[c];
-    if (generic_pos[c + 1] != generic_pos[c]) {
-        gen_key[generic_pos[c]] = uint32_t(max_per_cell - cnt);
-        gen_cell[generic_pos[c]] = c;
-    }
-    if (empty_pos[c + 1] != empty_pos[c]) empty_cells[empty_pos[c]] = c;
+    if (c >= n_cells || generic_pos[c + 1] == generic_pos[c]) return;
+    gen_key[generic_pos[c]] = uint32_t(max_per_cell - (cell_start[c + 1] - cell_start[c]));
+    gen_cell[generic_pos[c]] = c;
 }
 
 // 1 where a kept point of a generic cell starts a run: its previous depth
@@ -615,9 +625,6 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         if ((rc2 = dev_alloc(&cell_ncombo, size_t(n_cells), "cell combos"))) return rc2;
         fill(cell_generic, n_cells, 0);
         fill(cell_ncombo, n_cells, 0);
-        fill(flag_a, int64_t(n_cells) + 1, 0);
-        fill(flag_b, int64_t(n_cells) + 1, 0);
-        fill(combo_flag, n_combo + 1, 0);
         ComboArgs ca;
         ca.cell_of_point = plan->cell_of_point;
         ca.N = N;
@@ -630,23 +637,37 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         ca.cell_generic = cell_generic;
         ca.cell_ncombo = cell_ncombo;
         hipLaunchKernelGGL(k_combo_walk, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream, ca);
-        hipLaunchKernelGGL(k_cell_class, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream, ca,
-                           plan->cell_start, n_cells, flag_a, flag_b, small + 4);
-        hipLaunchKernelGGL(k_combo_table, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream, ca,
-                           plan->column_table, combo_flag);
-        scan_with_total(flag_a, n_cells, small + 3, stream);   // generic cells
-        scan_with_total(flag_b, n_cells, small + 3, stream);   // empty cells
-        scan_with_total(combo_flag, n_combo, small + 3, stream);   // combos of multi cells
-        BEVPOOL_HIP(hipGetLastError());
-        int32_t stats[2], counters[2], n_gen, n_empty, kept, n_part;
-        BEVPOOL_HIP(hipMemcpyAsync(stats, small, sizeof(stats), hipMemcpyDeviceToHost, stream));
-        BEVPOOL_HIP(hipMemcpyAsync(counters, small + 4, sizeof(counters), hipMemcpyDeviceToHost,
-                                   stream));
-        if ((rc2 = to_host(&n_gen, flag_a + n_cells))) return rc2;
-        if ((rc2 = to_host(&n_empty, flag_b + n_cells))) return rc2;
-        if ((rc2 = to_host(&kept, plan->cell_start + n_cells))) return rc2;
-        if ((rc2 = to_host(&n_part, combo_flag + n_combo))) return rc2;
-        BEVPOOL_HIP(hipStreamSynchronize(stream));
+        int32_t stats[2], counters[2], n_gen = 0, n_empty = 0, kept = 0, n_part = 0;
+        auto classify = [&]() -> int {
+            fill(flag_a, int64_t(n_cells) + 1, 0);
+            fill(flag_b, int64_t(n_cells) + 1, 0);
+            fill(combo_flag, n_combo + 1, 0);
+            fill(small + 4, 2, 0);
+            hipLaunchKernelGGL(k_cell_class, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream, ca,
+                               plan->cell_start, n_cells, flag_a, flag_b, small + 4);
+            hipLaunchKernelGGL(k_combo_table, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream,
+                               ca, plan->column_table, combo_flag);
+            scan_with_total(flag_a, n_cells, small + 3, stream);       // generic cells
+            scan_with_total(flag_b, n_cells, small + 3, stream);       // empty cells
+            scan_with_total(combo_flag, n_combo, small + 3, stream);   // combos of multi cells
+            BEVPOOL_HIP(hipGetLastError());
+            BEVPOOL_HIP(hipMemcpyAsync(stats, small, sizeof(stats), hipMemcpyDeviceToHost, stream));
+            BEVPOOL_HIP(hipMemcpyAsync(counters, small + 4, sizeof(counters),
+                                       hipMemcpyDeviceToHost, stream));
+            int rc3;
+            if ((rc3 = to_host(&n_gen, flag_a + n_cells))) return rc3;
+            if ((rc3 = to_host(&n_empty, flag_b + n_cells))) return rc3;
+            if ((rc3 = to_host(&kept, plan->cell_start + n_cells))) return rc3;
+            if ((rc3 = to_host(&n_part, combo_flag + n_combo))) return rc3;
+            BEVPOOL_HIP(hipStreamSynchronize(stream));
+            return BEVPOOL_OK;
+        };
+        if ((rc2 = classify())) return rc2;
+        if (n_part > n_empty) {
+            hipLaunchKernelGGL(k_demote_multi, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream, ca,
+                               n_cells);
+            if ((rc2 = classify())) return rc2;
+        }
         plan->n_nonempty = stats[0];
         plan->max_per_cell = stats[1];
         plan->n_kept = kept;
@@ -656,7 +677,13 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         plan->n_empty = n_empty;
         plan->n_partials = n_part;
 
-        // partial-sum slots of the multi-combo cells
+        // cells without points, ascending
+        if ((rc2 = dev_alloc(&plan->empty_cells, size_t(n_empty), "empty_cells"))) return rc2;
+        hipLaunchKernelGGL(k_empty_list, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream, flag_b,
+                           n_cells, plan->empty_cells);
+
+        // partial-sum slots of the multi-combo cells, kept in the first
+        // n_part empty rows
         if ((rc2 = dev_alloc(&head_scan, size_t(n_part) + 1, "multi heads"))) return rc2;
         fill(head_scan, int64_t(n_part) + 1, 0);
         if (n_part > 0) {
@@ -664,7 +691,8 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
                                combo_cell, combo_flag, int32_t(n_combo), keys_a, vals_a);
             if ((rc2 = radix_sort(keys_a, vals_a, n_part, bits_for(n_cells)))) return rc2;
             hipLaunchKernelGGL(k_multi_slots, dim3(blocks_for(n_part)), dim3(kBlock), 0, stream,
-                               keys_a, vals_a, n_part, plan->column_table, head_scan);
+                               keys_a, vals_a, n_part, plan->empty_cells, plan->column_table,
+                               head_scan);
         }
         scan_with_total(head_scan, n_part, small + 3, stream);
         BEVPOOL_HIP(hipGetLastError());
@@ -678,14 +706,12 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
                            stream, keys_a, head_scan, n_part, plan->multi_begin, plan->multi_cell);
         BEVPOOL_HIP(hipGetLastError());
 
-        // cells without points, and generic cells by descending point count
-        if ((rc2 = dev_alloc(&plan->empty_cells, size_t(n_empty), "empty_cells"))) return rc2;
+        // generic cells by descending point count
         if ((rc2 = dev_alloc(&plan->generic_hdr, size_t(n_gen), "generic_hdr"))) return rc2;
-        uint32_t *gen_key = keys_a;   // free again after k_cell_start
+        uint32_t *gen_key = keys_a;   // free again after k_multi_cells
         int32_t *gen_cell = vals_a;
-        hipLaunchKernelGGL(k_compact_classes, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream,
-                           plan->cell_start, n_cells, flag_a, flag_b, plan->max_per_cell, gen_key,
-                           gen_cell, plan->empty_cells);
+        hipLaunchKernelGGL(k_compact_generic, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream,
+                           plan->cell_start, n_cells, flag_a, plan->max_per_cell, gen_key, gen_cell);
         BEVPOOL_HIP(hipGetLastError());
         if ((rc2 = radix_sort(gen_key, gen_cell, n_gen, bits_for(plan->max_per_cell)))) return rc2;
 
