@@ -217,13 +217,13 @@ __device__ void zero_rows(const FwdArgs &a, int zb, int b, int *s_cell) {
     const int total = ne * U;
     if (a.zero_vec) {
         float4 *o = reinterpret_cast<float4 *>(a.out + int64_t(b) * a.n_cells * a.C);
-        for (int f = threadIdx.x; f < total; f += kBlock) {
+        for (int f = threadIdx.x; f < total; f += kFwdBlock) {
             const int r = int(fdiv(uint32_t(f), a.div_units));
             o[int64_t(s_cell[r]) * U + (f - r * U)] = make_float4(0.f, 0.f, 0.f, 0.f);
         }
     } else {
         float *o = a.out + int64_t(b) * a.n_cells * a.C;
-        for (int f = threadIdx.x; f < total; f += kBlock) {
+        for (int f = threadIdx.x; f < total; f += kFwdBlock) {
             const int r = int(fdiv(uint32_t(f), a.div_units));
             o[int64_t(s_cell[r]) * U + (f - r * U)] = 0.f;
         }
@@ -378,7 +378,7 @@ __device__ void heavy_generic(const FwdArgs &a, const Frame &fr, int k, int c0, 
     float acc[NCH];
 #pragma unroll
     for (int q = 0; q < NCH; ++q) acc[q] = 0.f;
-    generic_runs<DT, NCH>(acc, a, fr, hdr, c0, wave, kWaves);
+    generic_runs<DT, NCH>(acc, a, fr, hdr, c0, wave, kFwdWaves);
 #pragma unroll
     for (int q = 0; q < NCH; ++q) s_part[wl * SS + j + 16 * q] = acc[q];
     __syncthreads();
@@ -395,10 +395,10 @@ __device__ void heavy_generic(const FwdArgs &a, const Frame &fr, int k, int c0, 
 }
 
 template <int DT, int NCH>
-__global__ __launch_bounds__(kBlock) void k_forward(FwdArgs a) {
+__global__ __launch_bounds__(kFwdBlock) void k_forward(FwdArgs a) {
     __shared__ float s_part[kColWidth * slot_stride<NCH>()];   // heavy cells: group partials
     __shared__ int s_cell[kZeroCells];                         // zero rows: cell ids
-    __shared__ __align__(16) float s_pb[kBlock];   // probability broadcast: 16 words per lane group
+    __shared__ __align__(16) float s_pb[kFwdBlock];   // probability broadcast: 16 words per lane group
     const int bx = blockIdx.x, b = blockIdx.y;
     const int c0 = blockIdx.z * a.slice_c;
     const int cn = min(a.slice_c, a.C - c0);
@@ -413,7 +413,7 @@ __global__ __launch_bounds__(kBlock) void k_forward(FwdArgs a) {
     } else if (bx < a.base_light) {
         if (blockIdx.z == 0) zero_rows(a, bx - a.base_zero, b, s_cell);   // whole rows
     } else {
-        const int k = (bx - a.base_light) * kWaves + int(threadIdx.x >> 6);
+        const int k = (bx - a.base_light) * kFwdWaves + int(threadIdx.x >> 6);
         if (k < a.n_light) light_generic<DT, NCH>(a, Frame(a, b), k, c0, cn);
     }
 }
@@ -425,6 +425,7 @@ __global__ __launch_bounds__(kBlock) void k_forward(FwdArgs a) {
 // channels j, j + 16, ...
 constexpr int kCombineChunks = 5;   // 16-channel chunks per pass (80 channels)
 constexpr int kCombineSlots = 4;    // slots loaded per step
+constexpr int kCombineGroups = kBlock / 16;   // cells per workgroup
 
 struct CombineArgs {
     float *out;
@@ -435,7 +436,7 @@ struct CombineArgs {
 
 __global__ __launch_bounds__(kBlock) void k_combine(CombineArgs a) {
     const int b = blockIdx.y;
-    const int k = blockIdx.x * kColWidth + int(threadIdx.x >> 4);
+    const int k = blockIdx.x * kCombineGroups + int(threadIdx.x >> 4);
     if (k >= a.n_multi) return;
     const int j = threadIdx.x & 15;
     const Rsrc O = make_rsrc(reinterpret_cast<const char *>(a.out) + int64_t(b) * a.o_bytes, a.o_bytes);
@@ -481,11 +482,11 @@ __global__ __launch_bounds__(kBlock) void k_combine(CombineArgs a) {
 template <int DT>
 void launch_dtype(const FwdArgs &a, dim3 grid, int nch, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     switch (nch) {
-        case 1: hipExtLaunchKernelGGL((k_forward<DT, 1>), grid, dim3(kBlock), 0, s, e0, e1, 0, a); break;
-        case 2: hipExtLaunchKernelGGL((k_forward<DT, 2>), grid, dim3(kBlock), 0, s, e0, e1, 0, a); break;
-        case 3: hipExtLaunchKernelGGL((k_forward<DT, 3>), grid, dim3(kBlock), 0, s, e0, e1, 0, a); break;
-        case 4: hipExtLaunchKernelGGL((k_forward<DT, 4>), grid, dim3(kBlock), 0, s, e0, e1, 0, a); break;
-        default: hipExtLaunchKernelGGL((k_forward<DT, 5>), grid, dim3(kBlock), 0, s, e0, e1, 0, a); break;
+        case 1: hipExtLaunchKernelGGL((k_forward<DT, 1>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a); break;
+        case 2: hipExtLaunchKernelGGL((k_forward<DT, 2>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a); break;
+        case 3: hipExtLaunchKernelGGL((k_forward<DT, 3>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a); break;
+        case 4: hipExtLaunchKernelGGL((k_forward<DT, 4>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a); break;
+        default: hipExtLaunchKernelGGL((k_forward<DT, 5>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a); break;
     }
 }
 
@@ -552,7 +553,7 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
     a.zero_vec = (channels % 4 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0) ? 1 : 0;
     a.zero_units = a.zero_vec ? channels / 4 : channels;
     a.div_units = make_fastdiv(uint32_t(a.zero_units));
-    const int n_blocks = a.base_light + (a.n_light + kWaves - 1) / kWaves;
+    const int n_blocks = a.base_light + (a.n_light + kFwdWaves - 1) / kFwdWaves;
 
     // the last kernel of the forward carries the stop event
     const bool combine = plan->n_multi > 0;
@@ -572,7 +573,7 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
         ca.n_multi = plan->n_multi;
         ca.C = channels;
         ca.o_bytes = uint32_t(o_bytes);
-        hipExtLaunchKernelGGL(k_combine, dim3((plan->n_multi + kColWidth - 1) / kColWidth, batch),
+        hipExtLaunchKernelGGL(k_combine, dim3((plan->n_multi + kCombineGroups - 1) / kCombineGroups, batch),
                               dim3(kBlock), 0, stream, nullptr, stop, 0, ca);
         BEVPOOL_HIP(hipGetLastError());
     }

@@ -33,10 +33,12 @@ namespace bevpool {
 // workgroups of their own.
 constexpr int kWaveSize = 64;
 constexpr int kWaves = 4;
-constexpr int kBlock = kWaves * kWaveSize;      // plan kernels and the forward kernels
+constexpr int kBlock = kWaves * kWaveSize;      // plan kernels, combine kernel
+constexpr int kFwdWaves = 2;
+constexpr int kFwdBlock = kFwdWaves * kWaveSize;  // forward kernel
 constexpr int kGroupLanes = 16;                 // lanes per pixel column
 constexpr int kColDepth = 8;
-constexpr int kColWidth = kBlock / kGroupLanes; // 16 columns per item
+constexpr int kColWidth = kFwdBlock / kGroupLanes;  // 8 columns per item
 constexpr int kGenHeavy = 256;
 constexpr int kSliceChannels = 80;              // channels per pass
 
