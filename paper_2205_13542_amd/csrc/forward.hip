@@ -10,9 +10,9 @@
 //                  feature row (n, h, w) is read once and applied to every
 //                  depth bin of the item; the depth probabilities are read
 //                  one per lane and broadcast to the group through LDS.
-//                  Single-combo cells are stored from registers; the
-//                  combos of a multi-combo cell meet in LDS and the cell's
-//                  first combo adds them in slot order.
+//                  Single-combo cells are stored from registers; each
+//                  combo of a multi-combo cell stores its sum in the
+//                  borrowed row of its partial slot.
 //   light generic  one wave per generic cell. Its runs (consecutive depth
 //                  bins of one pixel) are taken 64 at a time: each lane loads
 //                  one run record and sums the run's depth probabilities,
@@ -21,8 +21,14 @@
 //   heavy generic  one workgroup per generic cell with more than kGenHeavy
 //                  points; its waves take the 64-run chunks in turn, and the
 //                  16 groups are combined through LDS.
-//   zero rows      cells without points, kZeroCells per workgroup, as one
-//                  flat run of 16-byte stores over their rows.
+//   zero rows      cells without points, one per thread of a workgroup,
+//                  as one flat run of 16-byte stores over their rows.
+//
+// A second launch, k_combine, runs when the plan has multi-combo cells: it
+// adds each such cell's partial slots in slot order, zeroes the borrowed
+// rows, and zeroes the last share of the empty rows. That share is
+// bandwidth-bound work that covers the latency of the slot reads, and the
+// first launch gets shorter by as much.
 //
 // Channels go across the 16 lanes of a group (channel j + 16k in lane j), so
 // every load and store of a row is contiguous across the group. Rows wider
@@ -83,21 +89,30 @@ __device__ __forceinline__ void store_f32(Rsrc r, uint32_t off, float v) {
     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, int(off), 0, 0);
 }
 
+// Rows of empty cells to zero: entries zero_begin .. zero_end-1 of the
+// empty-cell list.
+struct ZeroArgs {
+    float *out;
+    const int32_t *empty_cells;
+    int32_t n_cells, C;
+    int32_t zero_begin, zero_end;
+    int32_t zero_vec, zero_units;       // float4 units (or floats) per row
+    FastDiv div_units;
+};
+
 struct FwdArgs {
     const char *P, *F;
     float *out;
     const int2 *table;
     const int4 *gen_hdr;
     const int4 *gen_runs;
-    const int32_t *empty_cells;
     int32_t N, D, H, W, HW;
     int32_t n_cells, C, slice_c;
     uint32_t p_bytes, f_bytes, o_bytes, run_bytes;   // per frame (runs: whole table)
     int32_t items_d, items_w, n_items;
-    int32_t n_heavy, n_light, n_empty, n_partials;
+    int32_t n_heavy, n_light;
     int32_t base_col, base_zero, base_light;
-    int32_t zero_vec, zero_units;       // empty rows: float4 units (or floats) per row
-    FastDiv div_units;
+    ZeroArgs zero;
 };
 
 // The buffers of frame b: depth probabilities, features, BEV map.
@@ -110,7 +125,6 @@ struct Frame {
 };
 
 constexpr int kStages = 6;                      // row-pair stages in flight per wave
-constexpr int kZeroCells = 128;                 // empty rows per zeroing workgroup
 
 // LDS row stride of a lane group's partial sums: 16*NCH floats, padded so
 // that the four groups of a wave start on different bank quarters.
@@ -201,34 +215,38 @@ struct Emit<kColDepth, NCH> {
                                                uint32_t, int, bool) {}
 };
 
-// Rows of kZeroCells listed empty cells of frame b (in slice 0 only), from
-// entry n_partials on (the rows before it hold partial sums and are zeroed
-// by the combine kernel),
-// written as one flat sequence of 16-byte (or 4-byte) units: unit f is unit
-// f % U of row f / U. Rows of consecutive cells are adjacent in memory, so
-// runs of empty cells become contiguous stores. The cell ids are staged in
-// LDS first, so no store waits on a load.
-__device__ void zero_rows(const FwdArgs &a, int zb, int b, int *s_cell) {
-    const int e0 = a.n_partials + zb * kZeroCells;
-    const int ne = min(kZeroCells, a.n_empty - e0);
-    if (int(threadIdx.x) < ne) s_cell[threadIdx.x] = a.empty_cells[e0 + threadIdx.x];
+// Zeroing workgroup zb of BS threads: the rows of BS listed empty cells of
+// frame b, from entry z.zero_begin + zb * BS on, written as one flat
+// sequence of 16-byte (or 4-byte) units: unit f is unit f % U of row f / U.
+// Rows of consecutive cells are adjacent in memory, so runs of empty cells
+// become contiguous stores. The cell ids are staged in LDS first, so no
+// store waits on a load.
+template <int BS>
+__device__ void zero_rows(const ZeroArgs &z, int zb, int b, int *s_cell) {
+    const int e0 = z.zero_begin + zb * BS;
+    const int ne = min(BS, z.zero_end - e0);
+    if (int(threadIdx.x) < ne) s_cell[threadIdx.x] = z.empty_cells[e0 + threadIdx.x];
     __syncthreads();
-    const int U = a.zero_units;
+    const int U = z.zero_units;
     const int total = ne * U;
-    if (a.zero_vec) {
-        float4 *o = reinterpret_cast<float4 *>(a.out + int64_t(b) * a.n_cells * a.C);
-        for (int f = threadIdx.x; f < total; f += kFwdBlock) {
-            const int r = int(fdiv(uint32_t(f), a.div_units));
+    if (z.zero_vec) {
+        float4 *o = reinterpret_cast<float4 *>(z.out + int64_t(b) * z.n_cells * z.C);
+        for (int f = threadIdx.x; f < total; f += BS) {
+            const int r = int(fdiv(uint32_t(f), z.div_units));
             o[int64_t(s_cell[r]) * U + (f - r * U)] = make_float4(0.f, 0.f, 0.f, 0.f);
         }
     } else {
-        float *o = a.out + int64_t(b) * a.n_cells * a.C;
-        for (int f = threadIdx.x; f < total; f += kFwdBlock) {
-            const int r = int(fdiv(uint32_t(f), a.div_units));
+        float *o = z.out + int64_t(b) * z.n_cells * z.C;
+        for (int f = threadIdx.x; f < total; f += BS) {
+            const int r = int(fdiv(uint32_t(f), z.div_units));
             o[int64_t(s_cell[r]) * U + (f - r * U)] = 0.f;
         }
     }
 }
+
+// Zeroing workgroups of BS threads needed for the entries of z.
+template <int BS>
+int zero_blocks(const ZeroArgs &z) { return (z.zero_end - z.zero_begin + BS - 1) / BS; }
 
 template <int DT, int NCH>
 __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0, int cn,
@@ -397,7 +415,7 @@ __device__ void heavy_generic(const FwdArgs &a, const Frame &fr, int k, int c0, 
 template <int DT, int NCH>
 __global__ __launch_bounds__(kFwdBlock) void k_forward(FwdArgs a) {
     __shared__ float s_part[kColWidth * slot_stride<NCH>()];   // heavy cells: group partials
-    __shared__ int s_cell[kZeroCells];                         // zero rows: cell ids
+    __shared__ int s_cell[kFwdBlock];                          // zero rows: cell ids
     __shared__ __align__(16) float s_pb[kFwdBlock];   // probability broadcast: 16 words per lane group
     const int bx = blockIdx.x, b = blockIdx.y;
     const int c0 = blockIdx.z * a.slice_c;
@@ -411,7 +429,7 @@ __global__ __launch_bounds__(kFwdBlock) void k_forward(FwdArgs a) {
     } else if (bx < a.base_zero) {
         return;
     } else if (bx < a.base_light) {
-        if (blockIdx.z == 0) zero_rows(a, bx - a.base_zero, b, s_cell);   // whole rows
+        if (blockIdx.z == 0) zero_rows<kFwdBlock>(a.zero, bx - a.base_zero, b, s_cell);   // whole rows
     } else {
         const int k = (bx - a.base_light) * kFwdWaves + int(threadIdx.x >> 6);
         if (k < a.n_light) light_generic<DT, NCH>(a, Frame(a, b), k, c0, cn);
@@ -422,7 +440,7 @@ __global__ __launch_bounds__(kFwdBlock) void k_forward(FwdArgs a) {
 // multi_begin[k] .. multi_begin[k+1]-1, slot s held in the BEV row of empty
 // cell empty_cells[s]. They are added in slot order into the cell's row,
 // and the borrowed rows are zeroed. One group of 16 lanes per cell,
-// channels j, j + 16, ...
+// channels j, j + 16, ... Workgroups from n_cblocks on zero empty rows.
 constexpr int kCombineChunks = 5;   // 16-channel chunks per pass (80 channels)
 constexpr int kCombineSlots = 4;    // slots loaded per step
 constexpr int kCombineGroups = kBlock / 16;   // cells per workgroup
@@ -430,12 +448,18 @@ constexpr int kCombineGroups = kBlock / 16;   // cells per workgroup
 struct CombineArgs {
     float *out;
     const int32_t *multi_begin, *multi_cell, *empty_cells;
-    int32_t n_multi, C;
+    int32_t n_multi, C, n_cblocks;
     uint32_t o_bytes;
+    ZeroArgs zero;
 };
 
 __global__ __launch_bounds__(kBlock) void k_combine(CombineArgs a) {
+    __shared__ int s_cell[kBlock];
     const int b = blockIdx.y;
+    if (int(blockIdx.x) >= a.n_cblocks) {
+        zero_rows<kBlock>(a.zero, blockIdx.x - a.n_cblocks, b, s_cell);
+        return;
+    }
     const int k = blockIdx.x * kCombineGroups + int(threadIdx.x >> 4);
     if (k >= a.n_multi) return;
     const int j = threadIdx.x & 15;
@@ -492,6 +516,9 @@ void launch_dtype(const FwdArgs &a, dim3 grid, int nch, hipStream_t s, hipEvent_
 
 int round8(int x) { return (x + 7) & ~7; }
 
+// Eighths of the unborrowed empty rows that the combine kernel zeroes.
+constexpr int kZeroLate = 8;
+
 }  // namespace
 }  // namespace bevpool
 
@@ -527,7 +554,6 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
     a.table = plan->column_table;
     a.gen_hdr = plan->generic_hdr;
     a.gen_runs = plan->generic_runs;
-    a.empty_cells = plan->empty_cells;
     a.N = g.n_cams;
     a.D = g.n_depth;
     a.H = g.feat_h;
@@ -545,18 +571,30 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
     a.n_items = g.n_cams * a.items_d * a.items_w;
     a.n_heavy = plan->n_generic_heavy;
     a.n_light = plan->n_generic - plan->n_generic_heavy;
-    a.n_empty = plan->n_empty;
-    a.n_partials = plan->n_partials;
+
+    // Empty rows: the first n_partials entries of the list are borrowed by
+    // partial slots (the combine kernel zeroes them); of the rest, the
+    // combine kernel, when there is one, takes the last kZeroLate / 8.
+    const bool combine = plan->n_multi > 0;
+    ZeroArgs z;
+    z.out = out;
+    z.empty_cells = plan->empty_cells;
+    z.n_cells = plan->n_cells;
+    z.C = channels;
+    z.zero_vec = (channels % 4 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0) ? 1 : 0;
+    z.zero_units = z.zero_vec ? channels / 4 : channels;
+    z.div_units = make_fastdiv(uint32_t(z.zero_units));
+    const int n_free = plan->n_empty - plan->n_partials;
+    const int n_late = combine ? int(int64_t(n_free) * kZeroLate / 8) : 0;
+    a.zero = z;
+    a.zero.zero_begin = plan->n_partials;
+    a.zero.zero_end = plan->n_empty - n_late;
     a.base_col = round8(a.n_heavy);
     a.base_zero = round8(a.base_col + a.n_items);
-    a.base_light = a.base_zero + (a.n_empty - a.n_partials + kZeroCells - 1) / kZeroCells;
-    a.zero_vec = (channels % 4 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0) ? 1 : 0;
-    a.zero_units = a.zero_vec ? channels / 4 : channels;
-    a.div_units = make_fastdiv(uint32_t(a.zero_units));
+    a.base_light = a.base_zero + zero_blocks<kFwdBlock>(a.zero);
     const int n_blocks = a.base_light + (a.n_light + kFwdWaves - 1) / kFwdWaves;
 
     // the last kernel of the forward carries the stop event
-    const bool combine = plan->n_multi > 0;
     const dim3 grid(n_blocks, batch, n_slices);
     switch (dtype) {
         case BEVPOOL_F32: launch_dtype<BEVPOOL_F32>(a, grid, nch, stream, start, combine ? nullptr : stop); break;
@@ -572,8 +610,12 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
         ca.empty_cells = plan->empty_cells;
         ca.n_multi = plan->n_multi;
         ca.C = channels;
+        ca.n_cblocks = (plan->n_multi + kCombineGroups - 1) / kCombineGroups;
         ca.o_bytes = uint32_t(o_bytes);
-        hipExtLaunchKernelGGL(k_combine, dim3((plan->n_multi + kCombineGroups - 1) / kCombineGroups, batch),
+        ca.zero = z;
+        ca.zero.zero_begin = plan->n_empty - n_late;
+        ca.zero.zero_end = plan->n_empty;
+        hipExtLaunchKernelGGL(k_combine, dim3(ca.n_cblocks + zero_blocks<kBlock>(ca.zero), batch),
                               dim3(kBlock), 0, stream, nullptr, stop, 0, ca);
         BEVPOOL_HIP(hipGetLastError());
     }
