@@ -63,11 +63,17 @@ __device__ __forceinline__ Rsrc make_rsrc(const void *base, uint32_t bytes) {
 
 template <int DT>
 struct Elem;
+// load: one element as fp32; load4: four consecutive elements.
 template <>
 struct Elem<BEVPOOL_F32> {
     static constexpr uint32_t kBytes = 4;
     static __device__ __forceinline__ float load(Rsrc r, uint32_t off) {
         return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, int(off), 0, 0));
+    }
+    static __device__ __forceinline__ void load4(Rsrc r, uint32_t off, float *v) {
+        const auto q = __builtin_amdgcn_raw_buffer_load_b128(r, int(off), 0, 0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = __uint_as_float(q[i]);
     }
 };
 template <>
@@ -76,12 +82,28 @@ struct Elem<BEVPOOL_BF16> {
     static __device__ __forceinline__ float load(Rsrc r, uint32_t off) {
         return __uint_as_float(uint32_t(__builtin_amdgcn_raw_buffer_load_b16(r, int(off), 0, 0)) << 16);
     }
+    static __device__ __forceinline__ void load4(Rsrc r, uint32_t off, float *v) {
+        const auto q = __builtin_amdgcn_raw_buffer_load_b64(r, int(off), 0, 0);
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            v[2 * i] = __uint_as_float(uint32_t(q[i]) << 16);
+            v[2 * i + 1] = __uint_as_float(uint32_t(q[i]) & 0xFFFF0000u);
+        }
+    }
 };
 template <>
 struct Elem<BEVPOOL_F16> {
     static constexpr uint32_t kBytes = 2;
     static __device__ __forceinline__ float load(Rsrc r, uint32_t off) {
         return float(__builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(r, int(off), 0, 0)));
+    }
+    static __device__ __forceinline__ void load4(Rsrc r, uint32_t off, float *v) {
+        const auto q = __builtin_amdgcn_raw_buffer_load_b64(r, int(off), 0, 0);
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            v[2 * i] = float(__builtin_bit_cast(_Float16, uint16_t(uint32_t(q[i]) & 0xFFFFu)));
+            v[2 * i + 1] = float(__builtin_bit_cast(_Float16, uint16_t(uint32_t(q[i]) >> 16)));
+        }
     }
 };
 
@@ -124,7 +146,7 @@ struct Frame {
           O(make_rsrc(reinterpret_cast<const char *>(a.out) + int64_t(b) * a.o_bytes, a.o_bytes)) {}
 };
 
-constexpr int kStages = 6;                      // row-pair stages in flight per wave
+constexpr int kStages = 4;                      // row-pair stages in flight per wave
 
 // LDS row stride of a lane group's partial sums: 16*NCH floats, padded so
 // that the four groups of a wave start on different bank quarters.
@@ -161,22 +183,45 @@ struct Stage {
     Row<NCH> f0, f1;
 };
 
-// Chunks k = 0..NCH-1 of a row slice (element offset of chunk 0 in bytes,
-// or kOff). Lanes past the slice's last channel read bytes that are never
-// stored.
-template <int DT, int NCH>
+// Channels of a row slice held by lane j of a 16-lane group: value k is
+// channel j + 16k. With VEC (slices of 65..80 channels whose rows start on
+// 16-byte boundaries), values 0..3 are channels 4j..4j+3 and value 4 is
+// channel 64 + j instead, so that 64 of the channels move as one 4-element
+// access per lane. Lanes past the slice's last channel read bytes that are
+// never stored.
+
+// Row slice at byte offset off of its first channel (or kOff plus less than
+// 2^31: every access is then out of range).
+template <int DT, int NCH, bool VEC>
 __device__ __forceinline__ void load_row(Row<NCH> &r, Rsrc src, uint32_t off) {
+    static_assert(!VEC || NCH == 5, "4-element lanes need five values");
+    constexpr uint32_t ES = Elem<DT>::kBytes;
+    const uint32_t j = threadIdx.x & 15;
+    if constexpr (VEC) {
+        Elem<DT>::load4(src, off + 4 * j * ES, r.v);
+        r.v[4] = Elem<DT>::load(src, off + (64 + j) * ES);
+    } else {
 #pragma unroll
-    for (int k = 0; k < NCH; ++k) r.v[k] = Elem<DT>::load(src, off + uint32_t(k) * 16 * Elem<DT>::kBytes);
+        for (int k = 0; k < NCH; ++k) r.v[k] = Elem<DT>::load(src, off + (j + 16 * k) * ES);
+    }
 }
 
-// Store chunks of a row slice at byte offset off (or kOff). Only the last
-// chunk can run past the slice: tail_ok says whether it does not.
-template <int NCH>
+// Store a row slice of fp32 at byte offset off of its first channel (or
+// kOff). Only the last value can lie past the slice: tail_ok says whether it
+// does not.
+template <int NCH, bool VEC>
 __device__ __forceinline__ void store_row(Rsrc dst, uint32_t off, const float *v, bool tail_ok) {
+    const uint32_t j = threadIdx.x & 15;
+    if constexpr (VEC) {
+        __builtin_amdgcn_raw_buffer_store_b128(
+            (__attribute__((ext_vector_type(4))) uint32_t){__float_as_uint(v[0]), __float_as_uint(v[1]),
+                                                           __float_as_uint(v[2]), __float_as_uint(v[3])},
+            dst, int(off + 16 * j), 0, 0);
+    } else {
 #pragma unroll
-    for (int k = 0; k < NCH - 1; ++k) store_f32(dst, off + uint32_t(k) * 64, v[k]);
-    store_f32(dst, tail_ok ? off + uint32_t(NCH - 1) * 64 : kOff, v[NCH - 1]);
+        for (int k = 0; k < NCH - 1; ++k) store_f32(dst, off + (j + 16 * k) * 4, v[k]);
+    }
+    store_f32(dst, tail_ok ? off + (j + 16 * (NCH - 1)) * 4 : kOff, v[NCH - 1]);
 }
 
 // acc[J] += pb[J] * f for the kColDepth depth bins of one row: pb holds the
@@ -196,21 +241,21 @@ __device__ __forceinline__ void apply_row(float (&acc)[kColDepth][NCH], const fl
 // table entry: its single-combo cell, or the borrowed empty-cell row that
 // holds the partial sum of its combo. Lane J of the group holds the entry of
 // depth bin J.
-template <int J, int NCH>
+template <int J, int NCH, bool VEC>
 struct Emit {
     static __device__ __forceinline__ void run(const float (&acc)[kColDepth][NCH], int ex,
                                                uint32_t dm, Rsrc out, uint32_t ch_off, int C,
                                                bool tail_ok) {
         if (dm & (1u << J)) {
             const int x = row_bcast<J>(ex);
-            store_row<NCH>(out, x >= 0 ? uint32_t(x) * uint32_t(C) * 4u + ch_off : kOff, acc[J],
+            store_row<NCH, VEC>(out, x >= 0 ? uint32_t(x) * uint32_t(C) * 4u + ch_off : kOff, acc[J],
                            tail_ok);
         }
-        Emit<J + 1, NCH>::run(acc, ex, dm, out, ch_off, C, tail_ok);
+        Emit<J + 1, NCH, VEC>::run(acc, ex, dm, out, ch_off, C, tail_ok);
     }
 };
-template <int NCH>
-struct Emit<kColDepth, NCH> {
+template <int NCH, bool VEC>
+struct Emit<kColDepth, NCH, VEC> {
     static __device__ __forceinline__ void run(const float (&)[kColDepth][NCH], int, uint32_t, Rsrc,
                                                uint32_t, int, bool) {}
 };
@@ -248,7 +293,7 @@ __device__ void zero_rows(const ZeroArgs &z, int zb, int b, int *s_cell) {
 template <int BS>
 int zero_blocks(const ZeroArgs &z) { return (z.zero_end - z.zero_begin + BS - 1) / BS; }
 
-template <int DT, int NCH>
+template <int DT, int NCH, bool VEC>
 __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0, int cn,
                             float *s_pb) {
     constexpr uint32_t ES = Elem<DT>::kBytes;
@@ -271,14 +316,14 @@ __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0,
     const bool dw_ok = in_w && d < a.D;
     const uint32_t p_col = dw_ok ? uint32_t(((n * a.D + d) * a.H) * a.W + w) * ES : kOff;
     const uint32_t p_row = uint32_t(a.W) * ES;
-    const uint32_t f_col = in_w ? (uint32_t(n * a.HW + w) * uint32_t(a.C) + uint32_t(c0 + j)) * ES : kOff;
+    const uint32_t f_col = in_w ? (uint32_t(n * a.HW + w) * uint32_t(a.C) + uint32_t(c0)) * ES : kOff;
     const uint32_t f_row = uint32_t(a.W) * uint32_t(a.C) * ES;
     const int hsel = j >> 3;
     const int H = a.H;
     auto load_stage = [&](Stage<NCH> &st, int h) {
         st.pv = Elem<DT>::load(fr.P, h + hsel < H ? p_col + uint32_t(h + hsel) * p_row : kOff);
-        load_row<DT, NCH>(st.f0, fr.F, h < H ? f_col + uint32_t(h) * f_row : kOff);
-        load_row<DT, NCH>(st.f1, fr.F, h + 1 < H ? f_col + uint32_t(h + 1) * f_row : kOff);
+        load_row<DT, NCH, VEC>(st.f0, fr.F, h < H ? f_col + uint32_t(h) * f_row : kOff);
+        load_row<DT, NCH, VEC>(st.f1, fr.F, h + 1 < H ? f_col + uint32_t(h + 1) * f_row : kOff);
     };
     int2 e = make_int2(-1, 0);
     if (dw_ok) e = a.table[(int64_t(n) * a.D + d) * a.W + w];
@@ -326,19 +371,19 @@ __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0,
         }
     }
 
-    Emit<0, NCH>::run(acc, e.x, dm, fr.O, uint32_t(c0 + j) * 4u, a.C, tail_ok);
+    Emit<0, NCH, VEC>::run(acc, e.x, dm, fr.O, uint32_t(c0) * 4u, a.C, tail_ok);
 }
 
 // A generic cell's runs in chunks of 64: lane i loads run i of the chunk and
 // sums its depth probabilities; then the four lane groups take the runs
 // round-robin, four at a time, each run costing one feature row. A group's
 // runs are added in a fixed order.
-template <int DT, int NCH>
+template <int DT, int NCH, bool VEC>
 __device__ __forceinline__ void generic_runs(float (&acc)[NCH], const FwdArgs &a, const Frame &fr,
                                              int4 hdr, int c0, int first_chunk, int chunk_step) {
     constexpr uint32_t ES = Elem<DT>::kBytes;
     const int lane = threadIdx.x & 63;
-    const int j = lane & 15, grp = lane >> 4;
+    const int grp = lane >> 4;
     const Rsrc runs = make_rsrc(a.gen_runs, a.run_bytes);
     for (int ch = first_chunk; ch * 64 < hdr.z; ch += chunk_step) {
         const int nr = min(64, hdr.z - ch * 64);
@@ -355,8 +400,8 @@ __device__ __forceinline__ void generic_runs(float (&acc)[NCH], const FwdArgs &a
                 const int i = i0 + 4 * u + grp;
                 pr[u] = __shfl(ps, i & 63);
                 const int px = __shfl(pix, i & 63);
-                load_row<DT, NCH>(f[u], fr.F,
-                                  i < nr ? (uint32_t(px) * uint32_t(a.C) + uint32_t(c0 + j)) * ES : kOff);
+                load_row<DT, NCH, VEC>(f[u], fr.F,
+                                  i < nr ? (uint32_t(px) * uint32_t(a.C) + uint32_t(c0)) * ES : kOff);
             }
 #pragma unroll
             for (int u = 0; u < 4; ++u)
@@ -366,7 +411,7 @@ __device__ __forceinline__ void generic_runs(float (&acc)[NCH], const FwdArgs &a
     }
 }
 
-template <int DT, int NCH>
+template <int DT, int NCH, bool VEC>
 __device__ void light_generic(const FwdArgs &a, const Frame &fr, int k, int c0, int cn) {
     const int lane = threadIdx.x & 63;
     const int j = lane & 15, grp = lane >> 4;
@@ -374,18 +419,18 @@ __device__ void light_generic(const FwdArgs &a, const Frame &fr, int k, int c0, 
     float acc[NCH];
 #pragma unroll
     for (int q = 0; q < NCH; ++q) acc[q] = 0.f;
-    generic_runs<DT, NCH>(acc, a, fr, hdr, c0, 0, 1);
+    generic_runs<DT, NCH, VEC>(acc, a, fr, hdr, c0, 0, 1);
     // (g0 + g1) + (g2 + g3), the same in every lane of the wave
 #pragma unroll
     for (int q = 0; q < NCH; ++q) {
         const float s = acc[q] + __shfl_xor(acc[q], 16);
         acc[q] = s + __shfl_xor(s, 32);
     }
-    store_row<NCH>(fr.O, grp == 0 ? (uint32_t(hdr.x) * uint32_t(a.C) + uint32_t(c0 + j)) * 4u : kOff,
+    store_row<NCH, VEC>(fr.O, grp == 0 ? (uint32_t(hdr.x) * uint32_t(a.C) + uint32_t(c0)) * 4u : kOff,
                    acc, j + 16 * (NCH - 1) < cn);
 }
 
-template <int DT, int NCH>
+template <int DT, int NCH, bool VEC>
 __device__ void heavy_generic(const FwdArgs &a, const Frame &fr, int k, int c0, int cn,
                               float *s_part) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -396,7 +441,7 @@ __device__ void heavy_generic(const FwdArgs &a, const Frame &fr, int k, int c0, 
     float acc[NCH];
 #pragma unroll
     for (int q = 0; q < NCH; ++q) acc[q] = 0.f;
-    generic_runs<DT, NCH>(acc, a, fr, hdr, c0, wave, kFwdWaves);
+    generic_runs<DT, NCH, VEC>(acc, a, fr, hdr, c0, wave, kFwdWaves);
 #pragma unroll
     for (int q = 0; q < NCH; ++q) s_part[wl * SS + j + 16 * q] = acc[q];
     __syncthreads();
@@ -407,12 +452,12 @@ __device__ void heavy_generic(const FwdArgs &a, const Frame &fr, int k, int c0, 
         for (int g = 0; g < kColWidth; ++g)
 #pragma unroll
             for (int q = 0; q < NCH; ++q) sum[q] += s_part[g * SS + j + 16 * q];
-        store_row<NCH>(fr.O, (uint32_t(hdr.x) * uint32_t(a.C) + uint32_t(c0 + j)) * 4u, sum,
+        store_row<NCH, VEC>(fr.O, (uint32_t(hdr.x) * uint32_t(a.C) + uint32_t(c0)) * 4u, sum,
                        j + 16 * (NCH - 1) < cn);
     }
 }
 
-template <int DT, int NCH>
+template <int DT, int NCH, bool VEC>
 __global__ __launch_bounds__(kFwdBlock) void k_forward(FwdArgs a) {
     __shared__ float s_part[kColWidth * slot_stride<NCH>()];   // heavy cells: group partials
     __shared__ int s_cell[kFwdBlock];                          // zero rows: cell ids
@@ -421,18 +466,18 @@ __global__ __launch_bounds__(kFwdBlock) void k_forward(FwdArgs a) {
     const int c0 = blockIdx.z * a.slice_c;
     const int cn = min(a.slice_c, a.C - c0);
     if (bx < a.n_heavy) {
-        heavy_generic<DT, NCH>(a, Frame(a, b), bx, c0, cn, s_part);
+        heavy_generic<DT, NCH, VEC>(a, Frame(a, b), bx, c0, cn, s_part);
     } else if (bx < a.base_col) {
         return;  // padding: column items start on a multiple of 8
     } else if (bx < a.base_col + a.n_items) {
-        column_item<DT, NCH>(a, Frame(a, b), xcd_remap(bx - a.base_col, a.n_items), c0, cn, s_pb);
+        column_item<DT, NCH, VEC>(a, Frame(a, b), xcd_remap(bx - a.base_col, a.n_items), c0, cn, s_pb);
     } else if (bx < a.base_zero) {
         return;
     } else if (bx < a.base_light) {
         if (blockIdx.z == 0) zero_rows<kFwdBlock>(a.zero, bx - a.base_zero, b, s_cell);   // whole rows
     } else {
         const int k = (bx - a.base_light) * kFwdWaves + int(threadIdx.x >> 6);
-        if (k < a.n_light) light_generic<DT, NCH>(a, Frame(a, b), k, c0, cn);
+        if (k < a.n_light) light_generic<DT, NCH, VEC>(a, Frame(a, b), k, c0, cn);
     }
 }
 
@@ -504,13 +549,17 @@ __global__ __launch_bounds__(kBlock) void k_combine(CombineArgs a) {
 // Kernel-boundary events (either may be null): they take the timestamps of
 // the dispatch itself rather than of separate queue entries.
 template <int DT>
-void launch_dtype(const FwdArgs &a, dim3 grid, int nch, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+void launch_dtype(const FwdArgs &a, dim3 grid, int nch, bool vec, hipStream_t s, hipEvent_t e0,
+                  hipEvent_t e1) {
     switch (nch) {
-        case 1: hipExtLaunchKernelGGL((k_forward<DT, 1>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a); break;
-        case 2: hipExtLaunchKernelGGL((k_forward<DT, 2>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a); break;
-        case 3: hipExtLaunchKernelGGL((k_forward<DT, 3>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a); break;
-        case 4: hipExtLaunchKernelGGL((k_forward<DT, 4>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a); break;
-        default: hipExtLaunchKernelGGL((k_forward<DT, 5>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a); break;
+        case 1: hipExtLaunchKernelGGL((k_forward<DT, 1, false>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a); break;
+        case 2: hipExtLaunchKernelGGL((k_forward<DT, 2, false>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a); break;
+        case 3: hipExtLaunchKernelGGL((k_forward<DT, 3, false>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a); break;
+        case 4: hipExtLaunchKernelGGL((k_forward<DT, 4, false>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a); break;
+        default:
+            if (vec) hipExtLaunchKernelGGL((k_forward<DT, 5, true>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a);
+            else hipExtLaunchKernelGGL((k_forward<DT, 5, false>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a);
+            break;
     }
 }
 
@@ -596,10 +645,15 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
 
     // the last kernel of the forward carries the stop event
     const dim3 grid(n_blocks, batch, n_slices);
+    // 4-element lanes: every row slice of F (elements) and of the output
+    // (fp32) starts on a 4-element boundary of an aligned buffer
+    const bool vec = nch == 5 && channels % 4 == 0 && slice_c % 4 == 0 &&
+                     reinterpret_cast<uintptr_t>(F) % (4 * esize) == 0 &&
+                     reinterpret_cast<uintptr_t>(out) % 16 == 0;
     switch (dtype) {
-        case BEVPOOL_F32: launch_dtype<BEVPOOL_F32>(a, grid, nch, stream, start, combine ? nullptr : stop); break;
-        case BEVPOOL_BF16: launch_dtype<BEVPOOL_BF16>(a, grid, nch, stream, start, combine ? nullptr : stop); break;
-        default: launch_dtype<BEVPOOL_F16>(a, grid, nch, stream, start, combine ? nullptr : stop); break;
+        case BEVPOOL_F32: launch_dtype<BEVPOOL_F32>(a, grid, nch, vec, stream, start, combine ? nullptr : stop); break;
+        case BEVPOOL_BF16: launch_dtype<BEVPOOL_BF16>(a, grid, nch, vec, stream, start, combine ? nullptr : stop); break;
+        default: launch_dtype<BEVPOOL_F16>(a, grid, nch, vec, stream, start, combine ? nullptr : stop); break;
     }
     BEVPOOL_HIP(hipGetLastError());
     if (combine) {

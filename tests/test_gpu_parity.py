@@ -211,11 +211,13 @@ def test_forward_edge_rigs(torch_cuda, pkg, oracle_lib, oracle_plans, name):
 
 
 @pytest.mark.parametrize("rig_name", ["nuscenes", "nuscenes_tilted"])
-@pytest.mark.parametrize("channels", [1, 3, 5, 12, 17, 33, 64, 81, 260])
+@pytest.mark.parametrize("channels", [1, 3, 5, 12, 17, 33, 64, 72, 81, 160, 260])
 def test_forward_channel_counts(torch_cuda, pkg, oracle_lib, oracle_plans, channels, rig_name):
     """Every lane-chunk count (1..5 channels per lane of a 16-lane group),
-    ragged last chunks, and rows split into channel slices (81, 260). The
-    level rig runs mostly column items, the tilted one mostly generic cells."""
+    ragged last chunks, rows split into channel slices (81, 160, 260), and
+    4-element lanes (72 and 160; 260 has slices of 65, which are not
+    4-aligned). The level rig runs mostly column items, the tilted one mostly
+    generic cells."""
     _say(f"[forward channels] {rig_name} C={channels}")
     rig = RIGS[rig_name]()
     P, F = wl.frames(rig, channels, 1, "peaked", seed=channels)
@@ -251,6 +253,12 @@ def test_inputs_aligned_to_one_element(torch_cuda, pkg, oracle_lib, oracle_plans
     out = plan.forward(P, F)
     torch.cuda.synchronize()
     _check_fp32(out.cpu().numpy(), ref, np.diff(cs))
+    # the output 4-byte aligned only as well, and the features aligned again
+    oflat = torch.full((out.numel() + 1,), float("nan"), device="cuda")
+    out2 = oflat[1:].view(out.shape)
+    plan.forward(P, _to_device(torch, w.F, "f32"), out=out2)
+    torch.cuda.synchronize()
+    _check_fp32(out2.cpu().numpy(), ref, np.diff(cs))
 
 
 def test_deterministic(torch_cuda, pkg):
