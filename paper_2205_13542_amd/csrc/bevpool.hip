@@ -36,6 +36,7 @@ void free_plan(bevpool_plan_s *plan) {
     (void)hipFree(plan->empty_cells);
     (void)hipFree(plan->multi_begin);
     (void)hipFree(plan->multi_cell);
+    (void)hipFree(plan->multi_rows);
     if (prev >= 0 && prev != plan->device) (void)hipSetDevice(prev);
     plan->magic = 0;
     delete plan;

@@ -483,19 +483,41 @@ __global__ __launch_bounds__(kFwdBlock) void k_forward(FwdArgs a) {
 
 // Cells fed by several combos: the slots of multi-combo cell k are
 // multi_begin[k] .. multi_begin[k+1]-1, slot s held in the BEV row of empty
-// cell empty_cells[s]. They are added in slot order into the cell's row,
-// and the borrowed rows are zeroed. One group of 16 lanes per cell,
+// cell empty_cells[s]; the rows of the first kCombineInline slots are also
+// listed in multi_rows[k], so one round of loads finds the cell, its slot
+// count and those rows. The slots are added in slot order into the cell's
+// row, and the borrowed rows are zeroed. One group of 16 lanes per cell,
 // channels j, j + 16, ... Workgroups from n_cblocks on zero empty rows.
 constexpr int kCombineChunks = 5;   // 16-channel chunks per pass (80 channels)
-constexpr int kCombineSlots = 4;    // slots loaded per step
 constexpr int kCombineGroups = kBlock / 16;   // cells per workgroup
+static_assert(kCombineInline <= 16, "inline rows come from one lane each of a 16-lane group");
 
 struct CombineArgs {
     float *out;
-    const int32_t *multi_begin, *multi_cell, *empty_cells;
+    const int32_t *multi_begin, *multi_cell, *multi_rows, *empty_cells;
     int32_t n_multi, C, n_cblocks;
     uint32_t o_bytes;
     ZeroArgs zero;
+};
+
+// Row of slot sl + U of this lane group's cell (held by its lane U), as a
+// byte offset, or kOff past the cell's last slot.
+template <int U>
+__device__ __forceinline__ uint32_t slot_row(int r, int sl, int n, uint32_t row_bytes) {
+    const int x = row_bcast<U>(r);
+    return sl + U < n ? uint32_t(x) * row_bytes : kOff;
+}
+
+template <int U>
+struct SlotRows {
+    static __device__ __forceinline__ void run(uint32_t *rb, int r, int sl, int n, uint32_t row_bytes) {
+        rb[U] = slot_row<U>(r, sl, n, row_bytes);
+        SlotRows<U + 1>::run(rb, r, sl, n, row_bytes);
+    }
+};
+template <>
+struct SlotRows<kCombineInline> {
+    static __device__ __forceinline__ void run(uint32_t *, int, int, int, uint32_t) {}
 };
 
 __global__ __launch_bounds__(kBlock) void k_combine(CombineArgs a) {
@@ -508,34 +530,40 @@ __global__ __launch_bounds__(kBlock) void k_combine(CombineArgs a) {
     const int k = blockIdx.x * kCombineGroups + int(threadIdx.x >> 4);
     if (k >= a.n_multi) return;
     const int j = threadIdx.x & 15;
+    const int ji = j % kCombineInline;
     const Rsrc O = make_rsrc(reinterpret_cast<const char *>(a.out) + int64_t(b) * a.o_bytes, a.o_bytes);
-    const int s0 = a.multi_begin[k], s1 = a.multi_begin[k + 1];
+    // one round: inline rows (lane u holds slot u), the cell, the slot range
+    const int r_inline = a.multi_rows[int64_t(k) * kCombineInline + ji];
+    const int s0 = a.multi_begin[k];
+    const int n = a.multi_begin[k + 1] - s0;
     const uint32_t row = uint32_t(a.C) * 4u;
     const uint32_t obase = uint32_t(a.multi_cell[k]) * row;
-    for (int c = j; c < a.C; c += kCombineChunks * 16) {
+    // every lane of the group runs every pass (the slot rows are exchanged
+    // between its lanes); channels past C are masked
+    for (int cb = 0; cb < a.C; cb += kCombineChunks * 16) {
+        const int c = cb + j;
         float sum[kCombineChunks];
 #pragma unroll
         for (int q = 0; q < kCombineChunks; ++q) sum[q] = 0.f;
-        // kCombineSlots slots' loads in flight at a time, added in slot order
-        for (int sl = s0; sl < s1; sl += kCombineSlots) {
-            uint32_t rb[kCombineSlots];
+        // kCombineInline slots' loads in flight at a time, added in slot order
+        for (int sl = 0; sl < n; sl += kCombineInline) {
+            const int r = sl == 0 ? r_inline : (sl + ji < n ? a.empty_cells[s0 + sl + ji] : 0);
+            uint32_t rb[kCombineInline];
+            SlotRows<0>::run(rb, r, sl, n, row);
+            float v[kCombineInline][kCombineChunks];
 #pragma unroll
-            for (int u = 0; u < kCombineSlots; ++u)
-                rb[u] = sl + u < s1 ? uint32_t(a.empty_cells[sl + u]) * row : kOff;
-            float v[kCombineSlots][kCombineChunks];
-#pragma unroll
-            for (int u = 0; u < kCombineSlots; ++u)
+            for (int u = 0; u < kCombineInline; ++u)
 #pragma unroll
                 for (int q = 0; q < kCombineChunks; ++q)
                     v[u][q] = Elem<BEVPOOL_F32>::load(
                         O, c + 16 * q < a.C ? rb[u] + uint32_t(c + 16 * q) * 4u : kOff);
 #pragma unroll
-            for (int u = 0; u < kCombineSlots; ++u)
+            for (int u = 0; u < kCombineInline; ++u)
 #pragma unroll
                 for (int q = 0; q < kCombineChunks; ++q)
-                    if (sl + u < s1) sum[q] += v[u][q];
+                    if (sl + u < n) sum[q] += v[u][q];
 #pragma unroll
-            for (int u = 0; u < kCombineSlots; ++u)
+            for (int u = 0; u < kCombineInline; ++u)
 #pragma unroll
                 for (int q = 0; q < kCombineChunks; ++q)
                     store_f32(O, c + 16 * q < a.C ? rb[u] + uint32_t(c + 16 * q) * 4u : kOff, 0.f);
@@ -661,6 +689,7 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
         ca.out = out;
         ca.multi_begin = plan->multi_begin;
         ca.multi_cell = plan->multi_cell;
+        ca.multi_rows = plan->multi_rows;
         ca.empty_cells = plan->empty_cells;
         ca.n_multi = plan->n_multi;
         ca.C = channels;

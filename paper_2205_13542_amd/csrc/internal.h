@@ -41,6 +41,7 @@ constexpr int kColDepth = 8;
 constexpr int kColWidth = kFwdBlock / kGroupLanes;  // 8 columns per item
 constexpr int kGenHeavy = 256;
 constexpr int kSliceChannels = 80;              // channels per pass
+constexpr int kCombineInline = 8;               // borrowed rows listed with each multi-combo cell
 
 // Column-table entry: {cell (single-combo cell) or borrowed row of its
 // partial slot (multi), h_lo | h_hi << 16 | kComboMulti}.
@@ -85,6 +86,7 @@ struct bevpool_plan_s {
     int2 *column_table;      // [N][D][W]: {cell or borrowed row or -1, h_lo | h_hi << 16 | flags}
     int32_t *multi_begin;    // [n_multi + 1]: first partial slot of each multi-combo cell
     int32_t *multi_cell;     // [n_multi]
+    int32_t *multi_rows;     // [n_multi][kCombineInline]: borrowed rows of the first slots, or -1
     int4 *generic_hdr;       // [n_generic]: {cell, first run, runs, points}, most points first
     int4 *generic_runs;      // [n_runs]: {first point id, pixel, depth bins, 0}
     int32_t *empty_cells;    // [n_empty] cells without points, ascending

@@ -400,6 +400,20 @@ __global__ __launch_bounds__(kBlock) void k_multi_cells(const uint32_t *key, con
     }
 }
 
+// The borrowed rows of the first kCombineInline slots of each multi-combo
+// cell, next to each other, so that the combine kernel finds them with one
+// access (slot i belongs to cell head_scan[i + 1] - 1).
+__global__ __launch_bounds__(kBlock) void k_multi_rows(const int32_t *head_scan,
+                                                       const int32_t *multi_begin, int32_t n,
+                                                       const int32_t *empty_cells,
+                                                       int32_t *multi_rows) {
+    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+    if (i >= n) return;
+    const int32_t k = head_scan[i + 1] - 1;
+    const int32_t u = i - multi_begin[k];
+    if (u < kCombineInline) multi_rows[int64_t(k) * kCombineInline + u] = empty_cells[i];
+}
+
 // Generic cells keyed for a descending sort by point count.
 __global__ __launch_bounds__(kBlock) void k_compact_generic(const int32_t *cell_start, int32_t n_cells,
                                                             const int32_t *generic_pos,
@@ -705,6 +719,15 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         hipLaunchKernelGGL(k_multi_cells, dim3(blocks_for(int64_t(n_part) + 1)), dim3(kBlock), 0,
                            stream, keys_a, head_scan, n_part, plan->multi_begin, plan->multi_cell);
         BEVPOOL_HIP(hipGetLastError());
+        if ((rc2 = dev_alloc(&plan->multi_rows, size_t(n_multi) * kCombineInline, "multi_rows")))
+            return rc2;
+        fill(plan->multi_rows, int64_t(n_multi) * kCombineInline, -1);
+        if (n_part > 0) {
+            hipLaunchKernelGGL(k_multi_rows, dim3(blocks_for(n_part)), dim3(kBlock), 0, stream,
+                               head_scan, plan->multi_begin, n_part, plan->empty_cells,
+                               plan->multi_rows);
+            BEVPOOL_HIP(hipGetLastError());
+        }
 
         // generic cells by descending point count
         if ((rc2 = dev_alloc(&plan->generic_hdr, size_t(n_gen), "generic_hdr"))) return rc2;
