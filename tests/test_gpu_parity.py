@@ -296,8 +296,19 @@ def test_plan_partition_counts(pkg, oracle_plans, name):
     assert info.n_column + info.n_generic == int((counts > 0).sum())
     assert info.n_empty == int((counts == 0).sum())
     assert info.n_runs >= info.n_generic
+    assert info.n_partials <= info.n_empty
     if name == "nuscenes":
-        assert info.n_generic == 0 and info.n_partials > 0
+        # a level rig: every combo is clean, so the partial slots are the
+        # combos of cells whose kept points come from two or more (n, d, w)
+        # combos
+        cop, sp, cs = oracle_plans(name)
+        H, W, D = rig.feat_h, rig.feat_w, rig.n_depth
+        p = sp[:cs[-1]].astype(np.int64)
+        combo = (p // (H * W)) * W + p % W                  # (n * D + d) * W + w
+        pairs = np.unique(cop[p].astype(np.int64) * (rig.n_cams * D * W) + combo)
+        per_cell = np.bincount(pairs // (rig.n_cams * D * W), minlength=rig.n_cells)
+        assert info.n_generic == 0
+        assert info.n_partials == int(per_cell[per_cell > 1].sum())   # one slot per combo
     plan.close()
 
 
