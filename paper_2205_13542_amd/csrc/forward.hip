@@ -328,8 +328,15 @@ __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0,
     int2 e = make_int2(-1, 0);
     if (dw_ok) e = a.table[(int64_t(n) * a.D + d) * a.W + w];
     Stage<NCH> st[kStages];
+    // Issued stage by stage, in the order in which the loop consumes them:
+    // the loop's waits count outstanding loads in issue order, and a
+    // prologue reordered by the scheduler would make every iteration wait
+    // for nearly all of them.
 #pragma unroll
-    for (int u = 0; u < kStages; ++u) load_stage(st[u], 2 * u);
+    for (int u = 0; u < kStages; ++u) {
+        load_stage(st[u], 2 * u);
+        __builtin_amdgcn_sched_barrier(0);
+    }
 
     const bool act = e.x >= 0;
     const uint32_t ey = uint32_t(e.y);
@@ -350,12 +357,14 @@ __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0,
         // the loads of the next kStages - 1 are outstanding. Each lane's
         // masked probability (depth bin j & 7, row j >> 3 of the stage) goes
         // through this group's 16 LDS words and comes back to all 16 lanes.
+        // Every pass runs all kStages stages: rows past H load nothing and
+        // add zeros, so the loop has one exit and its waits hold in steady
+        // state.
         float *pq = s_pb + (wave * 4 + (lane >> 4)) * 16;
         for (int h = 0; h < H; h += 2 * kStages) {
 #pragma unroll
             for (int u = 0; u < kStages; ++u) {
                 const int hs = h + 2 * u;
-                if (hs >= H) break;
                 const int hp = hs + hsel;
                 pq[j] = (hp >= hlo && hp < hhi) ? st[u].pv : 0.f;
                 __builtin_amdgcn_wave_barrier();
