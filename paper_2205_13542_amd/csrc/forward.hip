@@ -496,7 +496,9 @@ __global__ __launch_bounds__(kFwdBlock) void k_forward(FwdArgs a) {
 // listed in multi_rows[k], so one round of loads finds the cell, its slot
 // count and those rows. The slots are added in slot order into the cell's
 // row, and the borrowed rows are zeroed. One group of 16 lanes per cell,
-// channels j, j + 16, ... Workgroups from n_cblocks on zero empty rows.
+// channels j, j + 16, ... The first n_zblocks workgroups zero empty rows
+// instead: dispatched first, their bandwidth-bound stores start at once and
+// cover the latency of the slot reads.
 constexpr int kCombineChunks = 5;   // 16-channel chunks per pass (80 channels)
 constexpr int kCombineGroups = kBlock / 16;   // cells per workgroup
 static_assert(kCombineInline <= 16, "inline rows come from one lane each of a 16-lane group");
@@ -504,7 +506,7 @@ static_assert(kCombineInline <= 16, "inline rows come from one lane each of a 16
 struct CombineArgs {
     float *out;
     const int32_t *multi_begin, *multi_cell, *multi_rows, *empty_cells;
-    int32_t n_multi, C, n_cblocks;
+    int32_t n_multi, C, n_zblocks;
     uint32_t o_bytes;
     ZeroArgs zero;
 };
@@ -532,11 +534,11 @@ struct SlotRows<kCombineInline> {
 __global__ __launch_bounds__(kBlock) void k_combine(CombineArgs a) {
     __shared__ int s_cell[kBlock];
     const int b = blockIdx.y;
-    if (int(blockIdx.x) >= a.n_cblocks) {
-        zero_rows<kBlock>(a.zero, blockIdx.x - a.n_cblocks, b, s_cell);
+    if (int(blockIdx.x) < a.n_zblocks) {
+        zero_rows<kBlock>(a.zero, blockIdx.x, b, s_cell);
         return;
     }
-    const int k = blockIdx.x * kCombineGroups + int(threadIdx.x >> 4);
+    const int k = (int(blockIdx.x) - a.n_zblocks) * kCombineGroups + int(threadIdx.x >> 4);
     if (k >= a.n_multi) return;
     const int j = threadIdx.x & 15;
     const int ji = j % kCombineInline;
@@ -702,12 +704,13 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
         ca.empty_cells = plan->empty_cells;
         ca.n_multi = plan->n_multi;
         ca.C = channels;
-        ca.n_cblocks = (plan->n_multi + kCombineGroups - 1) / kCombineGroups;
         ca.o_bytes = uint32_t(o_bytes);
         ca.zero = z;
         ca.zero.zero_begin = plan->n_empty - n_late;
         ca.zero.zero_end = plan->n_empty;
-        hipExtLaunchKernelGGL(k_combine, dim3(ca.n_cblocks + zero_blocks<kBlock>(ca.zero), batch),
+        ca.n_zblocks = zero_blocks<kBlock>(ca.zero);
+        const int n_cblocks = (plan->n_multi + kCombineGroups - 1) / kCombineGroups;
+        hipExtLaunchKernelGGL(k_combine, dim3(ca.n_zblocks + n_cblocks, batch),
                               dim3(kBlock), 0, stream, nullptr, stop, 0, ca);
         BEVPOOL_HIP(hipGetLastError());
     }
