@@ -2,7 +2,8 @@
 // per-cell sum (BEVFusion, arXiv 2205.13542, Sec. III-B, first paragraph and
 // "Interval Reduction"). The paper gives each cell one GPU thread that walks
 // the cell's interval. Here the work follows the camera geometry instead
-// (see the partition in internal.h): one launch, four workgroup roles.
+// (see the partition in internal.h): a launch with four workgroup roles,
+// and a second one when the plan has multi-combo cells.
 //
 //   column items   kColDepth depth bins x kColWidth pixel columns of one
 //                  camera. A group of 16 lanes (one DPP row) owns a column
@@ -20,28 +21,32 @@
 //                  costing one feature row. Groups are combined by shuffles.
 //   heavy generic  one workgroup per generic cell with more than kGenHeavy
 //                  points; its waves take the 64-run chunks in turn, and the
-//                  16 groups are combined through LDS.
+//                  workgroup's lane groups are combined through LDS.
 //   zero rows      cells without points, one per thread of a workgroup,
-//                  as one flat run of 16-byte stores over their rows.
+//                  as one flat run of 16-byte stores over their rows (only
+//                  when there is no second launch).
 //
-// A second launch, k_combine, runs when the plan has multi-combo cells: it
-// adds each such cell's partial slots in slot order, zeroes the borrowed
-// rows, and zeroes the last share of the empty rows. That share is
-// bandwidth-bound work that covers the latency of the slot reads, and the
-// first launch gets shorter by as much.
+// The second launch, k_combine, adds each multi-combo cell's partial slots
+// in slot order, zeroes the borrowed rows, and zeroes the other empty rows.
+// The zeroing is bandwidth-bound work that covers the latency of the slot
+// reads, and the first launch, whose column items are latency-bound, runs
+// without write traffic beside it.
 //
-// Channels go across the 16 lanes of a group (channel j + 16k in lane j), so
-// every load and store of a row is contiguous across the group. Rows wider
-// than kSliceChannels are done in slices (grid z).
+// Channels go across the 16 lanes of a group (channel j + 16k in lane j, or
+// 4j..4j+3 and 64 + j for aligned slices of 65..80 channels), so every load
+// and store of a row is contiguous across the group. Rows wider than
+// kSliceChannels are done in slices (grid z).
 //
 // All reads and writes of P, F and the BEV map go through buffer resources
 // of one frame each. An access that must not happen gets an offset past the
 // end of its buffer: the hardware range check then returns 0 for a load and
 // drops a store, so the hot loops carry no branches for bounds or masks.
 //
-// Every output row is written exactly once with plain stores, and every sum
-// runs in an order fixed by the plan, so results are deterministic. There is
-// no MFMA: each feature row meets only a handful of depth bins.
+// Each output row gets its final value from one plain store (a borrowed row
+// holds a partial sum before it is zeroed), and every sum runs in an order
+// fixed by the plan, so results are deterministic. The per-row products are
+// small (kColDepth bins x a row slice) and done with FMAs: the column items
+// are bound by memory latency, not by arithmetic.
 #include <math.h>
 #include <stdint.h>
 

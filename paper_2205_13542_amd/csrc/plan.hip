@@ -11,8 +11,9 @@
 //   k_cell_start   interval table from the sorted keys
 //   k_cell_stats   non-empty cells and the largest interval
 //   k_combo_walk ... k_generic_runs   work partition of the forward pass:
-//                  clean combos, the column table, generic cells and their
-//                  runs, empty cells
+//                  clean combos, the column table, empty cells, the
+//                  partial-sum slots of multi-combo cells, generic cells and
+//                  their runs
 //
 // The geometry is evaluated in IEEE double with the file built without
 // floating-point contraction, in one fixed expression order, so the cell ids
