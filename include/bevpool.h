@@ -174,6 +174,7 @@ typedef struct {
     int32_t n_empty;      /* cells without points */
     int32_t n_runs;       /* gather runs of the generic cells */
     int32_t n_partials;   /* partial-sum slots of cells fed by several combos */
+    int32_t n_multi;      /* cells with partial-sum slots */
 } bevpool_plan_info;
 
 /* Fill *info. Host only, no device work. Errors: INVALID_ARG. */

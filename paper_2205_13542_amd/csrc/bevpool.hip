@@ -159,6 +159,7 @@ int bevpool_plan_info_get(const bevpool_plan_t *plan, bevpool_plan_info *info) {
     info->n_empty = plan->n_empty;
     info->n_runs = plan->n_runs;
     info->n_partials = plan->n_partials;
+    info->n_multi = plan->n_multi;
     info->n_cams = plan->geom.n_cams;
     info->n_depth = plan->geom.n_depth;
     info->feat_h = plan->geom.feat_h;

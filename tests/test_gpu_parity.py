@@ -309,6 +309,7 @@ def test_plan_partition_counts(pkg, oracle_plans, name):
         per_cell = np.bincount(pairs // (rig.n_cams * D * W), minlength=rig.n_cells)
         assert info.n_generic == 0
         assert info.n_partials == int(per_cell[per_cell > 1].sum())   # one slot per combo
+        assert info.n_multi == int((per_cell > 1).sum())
     plan.close()
 
 
