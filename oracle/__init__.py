@@ -19,12 +19,19 @@ Functions and the passages they follow:
   "Interval Reduction": a cell's points are then consecutive).
 - ``pool``: per-cell sums of P * F ("Interval Reduction": sum is one of the
   symmetric aggregations; "Takeaways": exact, no approximation).
+- ``backward``: the gradients of ``pool`` with respect to P and F for a given
+  gradient of the BEV map (the pooling is one differentiable layer of a
+  model trained end to end): dP[p] = F[pixel(p)] . G[cell(p)] and
+  dF[pixel] = sum over its kept points of P[p] G[cell(p)].
 
 Pins, i.e. what the tests hold this oracle to (none of them re-types its
 formulas): closed-form cell maps of two dyadic rigs, a homogeneous-matrix
 projection through numpy.linalg, numpy's lexsort, a dense 0/1 matrix
 product, the count test, mass conservation, and permutation, linearity and
-boundary cases. Values at the nuScenes-shaped sizes are pinned only by these
+boundary cases; for the gradients, the adjoint identities
+<G, pool(P, F)> = <P, dP> = <F, dF> against ``pool``, a dense Jacobian of
+``pool`` built column by column on the tiny rig, and all-ones cases with
+integer answers. Values at the nuScenes-shaped sizes are pinned only by these
 properties: the paper prints no pooled value (parity unpinned by the paper,
 pinned by the invariants).
 """
@@ -81,6 +88,9 @@ def _load():
     lib.oracle_pool.argtypes = [P, P, P, ctypes.POINTER(_Geom), ctypes.c_int32,
                                 ctypes.c_int32, P, P, P]
     lib.oracle_pool.restype = None
+    lib.oracle_backward.argtypes = [P, P, P, P, ctypes.POINTER(_Geom), ctypes.c_int32,
+                                    ctypes.c_int32, P, P]
+    lib.oracle_backward.restype = None
     lib.oracle_max_threads.argtypes = []
     lib.oracle_max_threads.restype = ctypes.c_int
     _lib = lib
@@ -154,6 +164,27 @@ def pool(rig, cell_of_point: np.ndarray, P: np.ndarray, F: np.ndarray,
     if want_abs:
         res.append(a64)
     return res[0] if len(res) == 1 else tuple(res)
+
+
+def backward(rig, cell_of_point: np.ndarray, P: np.ndarray, F: np.ndarray, G: np.ndarray):
+    """Gradients of ``pool``. P float32 [B][N][D][H][W], F float32
+    [B][N][H][W][C], G float32 [B][ny][nx][C]. Returns (dP, dF) as float64
+    arrays of the shapes of P and F."""
+    lib = _load()
+    P = np.ascontiguousarray(P, dtype=np.float32)
+    F = np.ascontiguousarray(F, dtype=np.float32)
+    G = np.ascontiguousarray(G, dtype=np.float32)
+    B = P.shape[0]
+    C = F.shape[-1]
+    assert P.size == B * rig.n_points and F.size == B * rig.n_pixels * C
+    assert G.size == B * rig.n_cells * C
+    cop = np.ascontiguousarray(cell_of_point, dtype=np.int32)
+    dP = np.empty(P.shape, dtype=np.float64)
+    dF = np.empty(F.shape, dtype=np.float64)
+    g = _geom(rig)
+    lib.oracle_backward(_ptr(P), _ptr(F), _ptr(G), _ptr(cop), ctypes.byref(g), B, C,
+                        _ptr(dP), _ptr(dF))
+    return dP, dF
 
 
 def max_threads() -> int:

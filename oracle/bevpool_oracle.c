@@ -196,6 +196,59 @@ void oracle_pool(const float *P, const float *F, const int32_t *cell_of_point,
     }
 }
 
+/*
+ * Gradients of sum pooling. The forward map is bilinear in (P, F): each kept
+ * point p adds P[p] * F[pixel(p)][:] to its cell's row (Sec. III-B; the
+ * paper trains the whole model end to end, so the pooling is differentiated
+ * like any other layer). With G = d loss / d out [B][ny][nx][C]:
+ *   dP[b][p]        = sum_c F[b][pixel(p)][c] * G[b][cell(p)][c]  (kept p; 0 if dropped)
+ *   dF[b][pix][c]   = sum over kept points p of the pixel of P[b][p] * G[b][cell(p)][c]
+ * accumulated in double: dP over channels in channel order, dF over the
+ * pixel's depth bins in bin order. Each pixel owns its D points and its dF
+ * row, so pixels are split across threads without any shared sum.
+ * dP64: [B][N][D][H][W] double, dF64: [B][N][H][W][C] double.
+ */
+void oracle_backward(const float *P, const float *F, const float *G,
+                     const int32_t *cell_of_point, const oracle_geometry *g,
+                     int32_t batch, int32_t channels, double *dP64, double *dF64) {
+    const int64_t NP = n_points_of(g);
+    const int64_t HW = (int64_t)g->feat_h * g->feat_w;
+    const int64_t D = g->n_depth;
+    const int64_t n_pix = (int64_t)g->n_cams * HW;
+    const int64_t n_cells = (int64_t)g->nx * g->ny;
+    const int64_t C = channels;
+    for (int32_t b = 0; b < batch; ++b) {
+        const float *Pb = P + (size_t)b * NP;
+        const float *Fb = F + (size_t)b * n_pix * C;
+        const float *Gb = G + (size_t)b * n_cells * C;
+        double *dPb = dP64 + (size_t)b * NP;
+        double *dFb = dF64 + (size_t)b * n_pix * C;
+#pragma omp parallel for schedule(static)
+        for (int64_t pix = 0; pix < n_pix; ++pix) {
+            const int64_t n = pix / HW, hw = pix % HW;
+            const float *feat = Fb + pix * C;
+            double *df = dFb + pix * C;
+            for (int64_t c = 0; c < C; ++c) df[c] = 0.0;
+            for (int64_t d = 0; d < D; ++d) {
+                const int64_t p = (n * D + d) * HW + hw;
+                const int32_t cell = cell_of_point[p];
+                if (cell < 0) {
+                    dPb[p] = 0.0;
+                    continue;
+                }
+                const float *grad = Gb + (int64_t)cell * C;
+                const double prob = (double)Pb[p];
+                double dot = 0.0;
+                for (int64_t c = 0; c < C; ++c) {
+                    dot += (double)feat[c] * (double)grad[c];
+                    df[c] += prob * (double)grad[c];
+                }
+                dPb[p] = dot;
+            }
+        }
+    }
+}
+
 int oracle_max_threads(void) {
 #ifdef _OPENMP
     return omp_get_max_threads();

@@ -322,3 +322,69 @@ def test_thread_count_does_not_change_result(oracle_lib, tmp_path):
         subprocess.run([sys.executable, "-c", code, path], check=True, env=env)
         outs.append(np.load(path))
     assert (outs[0] == outs[1]).all()
+
+
+# ---------------------------------------------------------------- gradients
+#
+# The pooling is bilinear in (P, F), so its gradients are pinned by the
+# forward oracle itself (already pinned above) through identities that hold
+# for any G, and by a Jacobian assembled from forward calls.
+
+def _grad_inputs(name, seed, channels=None):
+    w = wl.make(name, seed=seed, channels=channels) if channels else wl.make(name, seed=seed)
+    rng = np.random.default_rng(seed + 100)
+    G = rng.standard_normal((w.batch, w.rig.ny, w.rig.nx, w.channels)).astype(np.float32)
+    return w, G
+
+
+@pytest.mark.parametrize("name", ["tiny", "nuscenes_tilted", "nuscenes"])
+def test_backward_adjoint_identities(oracle_lib, name):
+    """<G, pool(P, F)> = <P, dP> = <F, dF>, each side in double."""
+    w, G = _grad_inputs(name, seed=4)
+    cop = oracle_lib.cell_map(w.rig)
+    _, o64 = oracle_lib.pool(w.rig, cop, w.P, w.F, want_f64=True)
+    dP, dF = oracle_lib.backward(w.rig, cop, w.P, w.F, G)
+    lhs = float((G.astype(np.float64) * o64).sum())
+    via_p = float((w.P.astype(np.float64) * dP).sum())
+    via_f = float((w.F.astype(np.float64) * dF).sum())
+    scale = float((np.abs(G).astype(np.float64) *
+                   oracle_lib.pool(w.rig, cop, np.abs(w.P), np.abs(w.F), want_f64=True)[1]).sum())
+    assert abs(lhs - via_p) <= 1e-12 * scale
+    assert abs(lhs - via_f) <= 1e-12 * scale
+
+
+@pytest.mark.parametrize("name", ["tiny", "tiny_identity"])
+def test_backward_matches_forward_jacobian(oracle_lib, name):
+    """Column p of d out / d P is pool with P = e_p; row-wise the same for F.
+    The Jacobians are assembled from forward calls and contracted with G."""
+    w, G = _grad_inputs(name, seed=5)
+    rig = w.rig
+    cop = oracle_lib.cell_map(rig)
+    C = w.channels
+    dP, dF = oracle_lib.backward(rig, cop, w.P, w.F, G)
+    g64 = G[0].astype(np.float64).reshape(-1)
+    for p in range(rig.n_points):
+        e = np.zeros_like(w.P)
+        e.reshape(-1)[p] = 1.0
+        col = oracle_lib.pool(rig, cop, e, w.F, want_f64=True)[1].reshape(-1)
+        assert abs(float(col @ g64) - dP.reshape(-1)[p]) <= 1e-12 * (np.abs(col) @ np.abs(g64) + 1e-300)
+    for i in range(rig.n_pixels * C):
+        e = np.zeros_like(w.F)
+        e.reshape(-1)[i] = 1.0
+        col = oracle_lib.pool(rig, cop, w.P, e, want_f64=True)[1].reshape(-1)
+        assert abs(float(col @ g64) - dF.reshape(-1)[i]) <= 1e-12 * (np.abs(col) @ np.abs(g64) + 1e-300)
+
+
+def test_backward_all_ones(oracle_lib):
+    """G = 1 and F = 1: dP is C for every kept point and 0 for every dropped
+    one; G = 1 and P = 1: dF[pixel][c] counts the pixel's kept depth bins."""
+    rig = wl.ring_rig()
+    cop = oracle_lib.cell_map(rig)
+    C = 3
+    ones_p = np.ones((1, rig.n_points), dtype=np.float32)
+    ones_f = np.ones((1, rig.n_pixels, C), dtype=np.float32)
+    ones_g = np.ones((1, rig.n_cells, C), dtype=np.float32)
+    dP, dF = oracle_lib.backward(rig, cop, ones_p, ones_f, ones_g)
+    assert (dP.reshape(-1) == np.where(cop >= 0, C, 0)).all()
+    kept = (cop.reshape(rig.n_cams, rig.n_depth, rig.feat_h * rig.feat_w) >= 0).sum(axis=1)
+    assert (dF.reshape(rig.n_pixels, C) == kept.reshape(-1)[:, None]).all()
