@@ -161,6 +161,33 @@ BEVPOOL_API int bevpool_forward_timed(const void *depth_prob, const void *cam_fe
                           int32_t batch, int32_t channels, int32_t dtype,
                           void *hip_stream, void *start_event, void *stop_event);
 
+/*
+ * Gradients of bevpool_forward, for training (the paper trains the model
+ * end to end; the pooling is bilinear in P and F). For each frame b, with
+ * grad_out = d loss / d bev_out:
+ *   grad_depth[b][p] = sum_c cam_feat[b][pixel(p)][c] * grad_out[b][cell(p)][c]
+ *                      for a kept point p, 0 for a dropped one;
+ *   grad_feat[b][pixel][c] = sum over the pixel's kept points p of
+ *                      depth_prob[b][p] * grad_out[b][cell(p)][c]  (0 if none).
+ *
+ *  grad_out:   device float [batch][ny][nx][channels].
+ *  depth_prob, cam_feat: the forward's inputs, device, of dtype.
+ *  grad_depth: device float [batch][N][D][H][W], overwritten; NULL to skip.
+ *  grad_feat:  device float [batch][N][H][W][channels], overwritten; NULL to
+ *              skip (not both NULL).
+ * Sums are accumulated in fp32 in an order fixed by the plan, so repeated
+ * calls give bitwise equal results; no atomics, no allocation, no scratch.
+ * Asynchronous on hip_stream. Buffers must not overlap. A plan may be used
+ * by several backward and forward calls at once on different streams.
+ * Errors: INVALID_ARG (null pointer, a bad plan handle, both outputs NULL,
+ * batch outside 1..65535, channels < 1), UNSUPPORTED_DTYPE, OVERFLOW (one
+ * frame's tensor reaches 2 GiB), HIP (launch failure).
+ */
+BEVPOOL_API int bevpool_backward(const float *grad_out, const void *depth_prob,
+                     const void *cam_feat, const bevpool_plan_t *plan, float *grad_depth,
+                     float *grad_feat, int32_t batch, int32_t channels, int32_t dtype,
+                     void *hip_stream);
+
 /* Sizes of a plan. All counts are per frame. */
 typedef struct {
     int64_t n_points;     /* N*D*H*W */

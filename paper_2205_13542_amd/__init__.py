@@ -15,7 +15,7 @@ import numpy as np
 
 from . import _binding
 from ._binding import (BEVPOOL_BF16, BEVPOOL_F16, BEVPOOL_F32, BevpoolError,
-                       bevpool_forward, bevpool_forward_timed, bevpool_geometry,
+                       bevpool_backward, bevpool_forward, bevpool_forward_timed, bevpool_geometry,
                        bevpool_last_error,
                        bevpool_plan, bevpool_plan_destroy, bevpool_plan_export,
                        bevpool_plan_info_get, bevpool_version)
@@ -137,3 +137,34 @@ class Plan:
                                   out.data_ptr(), B, C, _dtype_code(cam_feat), stream.cuda_stream,
                                   start.cuda_event, stop.cuda_event)
         return out
+
+    def backward(self, grad_out, depth_prob, cam_feat, want_depth=True, want_feat=True,
+                 stream=None):
+        """Gradients of forward: grad_out fp32 [B][ny][nx][C] and the forward's
+        inputs; returns (grad_depth fp32 [B][N][D][H][W] or None,
+        grad_feat fp32 [B][N][H][W][C] or None)."""
+        torch = _torch()
+        i = self.info
+        B, C = depth_prob.shape[0], cam_feat.shape[-1]
+        if (tuple(depth_prob.shape) != (B, i.n_cams, i.n_depth, i.feat_h, i.feat_w)
+                or tuple(cam_feat.shape) != (B, i.n_cams, i.feat_h, i.feat_w, C)
+                or tuple(grad_out.shape) != (B, i.ny, i.nx, C)):
+            raise BevpoolError(_binding.BEVPOOL_ERR_SHAPE_MISMATCH,
+                               "grad_out, depth_prob or cam_feat does not match the plan")
+        if cam_feat.dtype != depth_prob.dtype or grad_out.dtype != torch.float32:
+            raise BevpoolError(_binding.BEVPOOL_ERR_UNSUPPORTED_DTYPE,
+                               "depth_prob and cam_feat must share a dtype; grad_out is fp32")
+        for t in (grad_out, depth_prob, cam_feat):
+            if not (t.is_cuda and t.is_contiguous()):
+                raise BevpoolError(_binding.BEVPOOL_ERR_INVALID_ARG,
+                                   "inputs must be contiguous device tensors")
+        dev = cam_feat.device
+        gd = torch.empty(tuple(depth_prob.shape), dtype=torch.float32, device=dev) if want_depth else None
+        gf = torch.empty(tuple(cam_feat.shape), dtype=torch.float32, device=dev) if want_feat else None
+        if stream is None:
+            stream = torch.cuda.current_stream(dev)
+        bevpool_backward(grad_out.data_ptr(), depth_prob.data_ptr(), cam_feat.data_ptr(),
+                         self.handle, gd.data_ptr() if gd is not None else 0,
+                         gf.data_ptr() if gf is not None else 0, B, C, _dtype_code(cam_feat),
+                         stream.cuda_stream)
+        return gd, gf

@@ -20,7 +20,8 @@ BEVPOOL_ERR_HIP = -6
 
 BEVPOOL_F32, BEVPOOL_BF16, BEVPOOL_F16 = 0, 1, 2
 
-EXPORTED = ("bevpool_plan", "bevpool_forward", "bevpool_forward_timed", "bevpool_plan_info_get",
+EXPORTED = ("bevpool_plan", "bevpool_forward", "bevpool_forward_timed", "bevpool_backward",
+            "bevpool_plan_info_get",
             "bevpool_plan_export", "bevpool_plan_destroy", "bevpool_last_error",
             "bevpool_version")
 
@@ -78,6 +79,8 @@ def load(path: str = LIB_PATH):
     lib.bevpool_forward.restype = ctypes.c_int
     lib.bevpool_forward_timed.argtypes = [vp, vp, vp, vp, i32, i32, i32, vp, vp, vp]
     lib.bevpool_forward_timed.restype = ctypes.c_int
+    lib.bevpool_backward.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, vp]
+    lib.bevpool_backward.restype = ctypes.c_int
     lib.bevpool_plan_info_get.argtypes = [vp, ctypes.POINTER(bevpool_plan_info)]
     lib.bevpool_plan_info_get.restype = ctypes.c_int
     lib.bevpool_plan_export.argtypes = [vp, vp, vp, vp]
@@ -137,6 +140,17 @@ def bevpool_forward_timed(depth_prob: int, cam_feat: int, plan: int, bev_out: in
                                         ctypes.c_void_p(plan), ctypes.c_void_p(bev_out),
                                         batch, channels, dtype, ctypes.c_void_p(hip_stream),
                                         ctypes.c_void_p(start_event), ctypes.c_void_p(stop_event)))
+
+
+def bevpool_backward(grad_out: int, depth_prob: int, cam_feat: int, plan: int, grad_depth: int,
+                     grad_feat: int, batch: int, channels: int, dtype: int,
+                     hip_stream: int = 0) -> None:
+    """Device addresses as ints; grad_depth or grad_feat may be 0 (skip)."""
+    _check(load().bevpool_backward(ctypes.c_void_p(grad_out), ctypes.c_void_p(depth_prob),
+                                   ctypes.c_void_p(cam_feat), ctypes.c_void_p(plan),
+                                   ctypes.c_void_p(grad_depth or None),
+                                   ctypes.c_void_p(grad_feat or None), batch, channels, dtype,
+                                   ctypes.c_void_p(hip_stream)))
 
 
 def bevpool_plan_info_get(plan: int) -> bevpool_plan_info:

@@ -1,0 +1,347 @@
+// Gradients of the per-frame BEV pooling (BEVFusion, arXiv 2205.13542,
+// Sec. III-B: the pooling is one layer of a model trained end to end). The
+// pooling is bilinear in (P, F); for G = d loss / d out:
+//   dP[b][p]      = F[b][pixel(p)] . G[b][cell(p)]   for a kept point p, else 0
+//   dF[b][pixel]  = sum over the kept points p of the pixel of P[b][p] G[b][cell(p)]
+//
+// Pixel-stationary work: a workgroup owns kBCols pixel columns x kBRows rows
+// of one camera, and its kBWaves waves take consecutive parts of the depth
+// bins. A group of 16 lanes owns one column; lane j holds the row slice
+// channels (the forward's lane layout) of the kBRows feature rows, read
+// once, and the kBRows rows' dF sums. For each depth bin the group reads one
+// gradient row when the combo (camera, depth bin, column) is clean — all its
+// kept points in one cell, which the plan records — or one per kept row
+// otherwise. dF gets P x G; dP gets the dot product F . G, reduced across the
+// 16 lanes by a transpose-reduce (8 shuffles for the 8 rows' sums). The
+// waves' dF sums are added in LDS in wave order and stored once; every dP
+// element is written by the one wave that owns its depth bin, so nothing is
+// accumulated with atomics and repeated calls give bitwise equal results.
+// Channel slices run as successive launches; slices after the first add
+// their dot products to dP.
+#include <stdint.h>
+
+#include <algorithm>
+
+#include "device.h"
+#include "internal.h"
+
+namespace bevpool {
+namespace {
+
+constexpr int kBRows = 8;                      // pixel rows per lane group
+constexpr int kBCols = 4;                      // pixel columns per workgroup (lane groups of a wave)
+constexpr int kBWaves = 4;                     // depth parts per workgroup
+constexpr int kBBlock = kBWaves * kWaveSize;
+constexpr int kBStages = 4;                    // depth bins in flight per wave
+constexpr int kBChunk = 32;                    // combo cells held in registers per pass (2 per lane)
+
+struct BwdArgs {
+    const char *P, *F;
+    const float *G;
+    float *dP, *dF;
+    const int32_t *cop, *combo_cells;
+    int32_t N, D, H, W, HW, C, c0, cn;         // channel slice [c0, c0 + cn)
+    uint32_t p_bytes, f_bytes, g_bytes, dp_bytes, df_bytes;   // per frame
+    uint32_t cop_bytes, cc_bytes;
+    int32_t items_w, items_h;                  // column blocks and row blocks per camera
+    int32_t part;                              // depth bins per wave
+    int32_t accumulate_dp, want_dp, want_df;
+};
+
+// One depth bin of a lane group: its combo's cell, each row's cell (lane j:
+// row j & 7), each row's probability, and the clean combo's gradient row.
+template <int NCH>
+struct BStage {
+    int cc, cell;
+    float pv;
+    Row<NCH> g;
+};
+
+// Sum of v[0..7] over the 16 lanes of a group, by halving rounds: after
+// them lanes j and j ^ 8 hold the total of row j & 7.
+__device__ __forceinline__ float transpose_reduce(const float (&v)[kBRows], int j) {
+    float a[4], b[2];
+    const bool h2 = (j & 4) != 0, h1 = (j & 2) != 0, h0 = (j & 1) != 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float keep = h2 ? v[4 + i] : v[i], send = h2 ? v[i] : v[4 + i];
+        a[i] = keep + __shfl_xor(send, 4, 16);
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const float keep = h1 ? a[2 + i] : a[i], send = h1 ? a[i] : a[2 + i];
+        b[i] = keep + __shfl_xor(send, 2, 16);
+    }
+    const float keep = h0 ? b[1] : b[0], send = h0 ? b[0] : b[1];
+    const float c = keep + __shfl_xor(send, 1, 16);
+    return c + __shfl_xor(c, 8, 16);
+}
+
+// acc[r] += pv_r * g and dot[r] = f[r] . g for the kBRows rows, pv_r from
+// lane r of the group.
+template <int R, int NCH>
+struct RowTerms {
+    static __device__ __forceinline__ void run(float (&acc)[kBRows][NCH], float (&dot)[kBRows],
+                                               const Row<NCH> (&f)[kBRows], const Row<NCH> &g,
+                                               float pv) {
+        const float p = row_bcast<R>(pv);
+        float s = 0.f;
+#pragma unroll
+        for (int k = 0; k < NCH; ++k) {
+            acc[R][k] = __builtin_fmaf(p, g.v[k], acc[R][k]);
+            s = __builtin_fmaf(f[R].v[k], g.v[k], s);
+        }
+        dot[R] = s;
+        RowTerms<R + 1, NCH>::run(acc, dot, f, g, pv);
+    }
+};
+template <int NCH>
+struct RowTerms<kBRows, NCH> {
+    static __device__ __forceinline__ void run(float (&)[kBRows][NCH], float (&)[kBRows],
+                                               const Row<NCH> (&)[kBRows], const Row<NCH> &, float) {}
+};
+
+// The same for a combo that is not clean: row R reads the gradient row of
+// its own cell (lane R's cell of the group), if it has one.
+template <int R, int NCH, bool VEC>
+struct RowTermsEach {
+    static __device__ __forceinline__ void run(float (&acc)[kBRows][NCH], float (&dot)[kBRows],
+                                               const Row<NCH> (&f)[kBRows], Rsrc G, uint32_t g_ch,
+                                               int C, int cell, float pv) {
+        const int c = row_bcast<R>(cell);
+        Row<NCH> g;
+        load_row<BEVPOOL_F32, NCH, VEC>(g, G, c >= 0 ? uint32_t(c) * uint32_t(C) * 4u + g_ch : kOff);
+        const float p = row_bcast<R>(pv);
+        float s = 0.f;
+#pragma unroll
+        for (int k = 0; k < NCH; ++k) {
+            acc[R][k] = __builtin_fmaf(p, g.v[k], acc[R][k]);
+            s = __builtin_fmaf(f[R].v[k], g.v[k], s);
+        }
+        dot[R] = s;
+        RowTermsEach<R + 1, NCH, VEC>::run(acc, dot, f, G, g_ch, C, cell, pv);
+    }
+};
+template <int NCH, bool VEC>
+struct RowTermsEach<kBRows, NCH, VEC> {
+    static __device__ __forceinline__ void run(float (&)[kBRows][NCH], float (&)[kBRows],
+                                               const Row<NCH> (&)[kBRows], Rsrc, uint32_t, int, int,
+                                               float) {}
+};
+
+template <int NCH>
+constexpr int bwd_stride() { return kBRows * NCH * 16 + 16; }   // one lane group's dF sums in LDS
+
+template <int DT, int NCH, bool VEC>
+__global__ __launch_bounds__(kBBlock) void k_backward(BwdArgs a) {
+    __shared__ float s_df[(kBWaves - 1) * kBCols * bwd_stride<NCH>()];
+    constexpr uint32_t ES = Elem<DT>::kBytes;
+    const int b = blockIdx.y;
+    const int rb = blockIdx.x % a.items_h;
+    const int t = blockIdx.x / a.items_h;
+    const int cb = t % a.items_w, n = t / a.items_w;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int j = lane & 15, grp = lane >> 4;
+    const int w = cb * kBCols + grp;
+    const int h0 = rb * kBRows;
+    const int jr = j & 7;                      // this lane's row for indices and probabilities
+    const bool in_w = w < a.W;
+    const bool row_ok = in_w && h0 + jr < a.H;
+    const bool tail_ok = j + 16 * (NCH - 1) < a.cn;
+
+    const Rsrc P = make_rsrc(a.P + int64_t(b) * a.p_bytes, a.p_bytes);
+    const Rsrc F = make_rsrc(a.F + int64_t(b) * a.f_bytes, a.f_bytes);
+    const Rsrc G = make_rsrc(reinterpret_cast<const char *>(a.G) + int64_t(b) * a.g_bytes, a.g_bytes);
+    const Rsrc dP = make_rsrc(reinterpret_cast<const char *>(a.dP) + int64_t(b) * a.dp_bytes, a.dp_bytes);
+    const Rsrc dF = make_rsrc(reinterpret_cast<const char *>(a.dF) + int64_t(b) * a.df_bytes, a.df_bytes);
+    const Rsrc cop = make_rsrc(a.cop, a.cop_bytes);
+    const Rsrc ccs = make_rsrc(a.combo_cells, a.cc_bytes);
+
+    // the group's feature rows, once
+    Row<NCH> f[kBRows];
+    const uint32_t f_row = uint32_t(a.W) * uint32_t(a.C) * ES;
+    const uint32_t f_col = in_w ? (uint32_t(n * a.HW + h0 * a.W + w) * uint32_t(a.C) + uint32_t(a.c0)) * ES : kOff;
+#pragma unroll
+    for (int r = 0; r < kBRows; ++r) {
+        load_row<DT, NCH, VEC>(f[r], F, h0 + r < a.H ? f_col + uint32_t(r) * f_row : kOff);
+        // the last value of a tail lane lies past the slice: it must not
+        // enter the dot products
+        if (!tail_ok) f[r].v[NCH - 1] = 0.f;
+    }
+
+    float acc[kBRows][NCH];
+#pragma unroll
+    for (int r = 0; r < kBRows; ++r)
+#pragma unroll
+        for (int k = 0; k < NCH; ++k) acc[r][k] = 0.f;
+
+    const uint32_t g_ch = uint32_t(a.c0) * 4u;
+    const uint32_t gC = uint32_t(a.C) * 4u;
+    const int d_lo = min(a.D, wave * a.part), d_hi = min(a.D, d_lo + a.part);
+    // point id of (n, d, h0 + jr, w) is pt0 + d * HW
+    const uint32_t pt0 = uint32_t((n * a.D) * a.HW + (h0 + jr) * a.W + w);
+
+    for (int dc = d_lo; dc < d_hi; dc += kBChunk) {
+        // the combo cells of this chunk's depth bins: lane j holds bins dc + j and dc + 16 + j
+        const int dn = min(kBChunk, d_hi - dc);
+        const uint32_t cc_base = uint32_t((n * a.D + dc) * a.W + w) * 4u;
+        const int cc_a = in_w && j < dn ? int(__builtin_amdgcn_raw_buffer_load_b32(ccs, int(cc_base + uint32_t(j * a.W) * 4u), 0, 0)) : -1;
+        const int cc_b = in_w && 16 + j < dn ? int(__builtin_amdgcn_raw_buffer_load_b32(ccs, int(cc_base + uint32_t((16 + j) * a.W) * 4u), 0, 0)) : -1;
+        auto load_stage = [&](BStage<NCH> &st, int i) {   // depth bin dc + i
+            const bool ok = i < dn;
+            const int cc_src = i < 16 ? cc_a : cc_b;
+            st.cc = ok ? __shfl(cc_src, (lane & 48) | (i & 15), 64) : -1;
+            const uint32_t p = pt0 + uint32_t(dc + i) * uint32_t(a.HW);
+            st.cell = ok && row_ok ? int(__builtin_amdgcn_raw_buffer_load_b32(cop, int(p * 4u), 0, 0)) : -1;
+            st.pv = Elem<DT>::load(P, ok && row_ok ? p * ES : kOff);
+            load_row<BEVPOOL_F32, NCH, VEC>(st.g, G, st.cc >= 0 ? uint32_t(st.cc) * gC + g_ch : kOff);
+        };
+        BStage<NCH> st[kBStages];
+#pragma unroll
+        for (int u = 0; u < kBStages; ++u) {
+            load_stage(st[u], u);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        for (int i0 = 0; i0 < dn; i0 += kBStages) {
+#pragma unroll
+            for (int u = 0; u < kBStages; ++u) {
+                const int i = i0 + u;
+                // a dropped row adds nothing and gets dP = 0
+                const bool kept = st[u].cell >= 0;
+                const float pv = kept ? st[u].pv : 0.f;
+                float dot[kBRows];
+                if (st[u].cc >= 0) {
+                    RowTerms<0, NCH>::run(acc, dot, f, st[u].g, pv);
+                } else if (st[u].cc == -2) {
+                    RowTermsEach<0, NCH, VEC>::run(acc, dot, f, G, g_ch, a.C, st[u].cell, pv);
+                } else {
+#pragma unroll
+                    for (int r = 0; r < kBRows; ++r) dot[r] = 0.f;
+                }
+                if (a.want_dp) {
+                    const float s = transpose_reduce(dot, j);
+                    if (j < kBRows && i < dn && row_ok) {
+                        const uint32_t off = (pt0 + uint32_t(dc + i) * uint32_t(a.HW)) * 4u;
+                        float v = kept ? s : 0.f;
+                        if (a.accumulate_dp) v += __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(dP, int(off), 0, 0));
+                        store_f32(dP, off, v);
+                    }
+                }
+                load_stage(st[u], i + kBStages);
+            }
+        }
+    }
+
+    if (!a.want_df) return;
+    // waves 1.. park their sums in LDS; wave 0 adds them in wave order
+    constexpr int BS = bwd_stride<NCH>();
+    if (wave > 0) {
+        float *slot = s_df + ((wave - 1) * kBCols + grp) * BS + j;
+#pragma unroll
+        for (int r = 0; r < kBRows; ++r)
+#pragma unroll
+            for (int k = 0; k < NCH; ++k) slot[(r * NCH + k) * 16] = acc[r][k];
+    }
+    __syncthreads();
+    if (wave > 0) return;
+    for (int v = 1; v < kBWaves; ++v) {
+        const float *slot = s_df + ((v - 1) * kBCols + grp) * BS + j;
+#pragma unroll
+        for (int r = 0; r < kBRows; ++r)
+#pragma unroll
+            for (int k = 0; k < NCH; ++k) acc[r][k] += slot[(r * NCH + k) * 16];
+    }
+    const uint32_t df_col = in_w ? (uint32_t(n * a.HW + h0 * a.W + w) * uint32_t(a.C) + uint32_t(a.c0)) * 4u : kOff;
+    const uint32_t df_row = uint32_t(a.W) * uint32_t(a.C) * 4u;
+#pragma unroll
+    for (int r = 0; r < kBRows; ++r)
+        store_row<NCH, VEC>(dF, h0 + r < a.H ? df_col + uint32_t(r) * df_row : kOff, acc[r], tail_ok);
+}
+
+template <int DT>
+void launch_bwd(const BwdArgs &a, dim3 grid, int nch, bool vec, hipStream_t s) {
+    switch (nch) {
+        case 1: hipLaunchKernelGGL((k_backward<DT, 1, false>), grid, dim3(kBBlock), 0, s, a); break;
+        case 2: hipLaunchKernelGGL((k_backward<DT, 2, false>), grid, dim3(kBBlock), 0, s, a); break;
+        case 3: hipLaunchKernelGGL((k_backward<DT, 3, false>), grid, dim3(kBBlock), 0, s, a); break;
+        case 4: hipLaunchKernelGGL((k_backward<DT, 4, false>), grid, dim3(kBBlock), 0, s, a); break;
+        default:
+            if (vec) hipLaunchKernelGGL((k_backward<DT, 5, true>), grid, dim3(kBBlock), 0, s, a);
+            else hipLaunchKernelGGL((k_backward<DT, 5, false>), grid, dim3(kBBlock), 0, s, a);
+            break;
+    }
+}
+
+}  // namespace
+}  // namespace bevpool
+
+using namespace bevpool;
+
+int bevpool_launch_backward(const float *G, const void *P, const void *F,
+                            const bevpool_plan_s *plan, float *dP, float *dF, int32_t batch,
+                            int32_t channels, int32_t dtype, hipStream_t stream) {
+    const bevpool_geometry &g = plan->geom;
+    const int64_t n_pix = int64_t(g.n_cams) * g.feat_h * g.feat_w;
+    const int64_t esize = dtype == BEVPOOL_F32 ? 4 : 2;
+    const int64_t p_bytes = plan->n_points * esize;
+    const int64_t f_bytes = n_pix * channels * esize;
+    const int64_t g_bytes = int64_t(plan->n_cells) * channels * 4;
+    const int64_t dp_bytes = plan->n_points * 4;
+    const int64_t df_bytes = n_pix * channels * 4;
+    constexpr int64_t kLimit = int64_t(1) << 31;
+    if (p_bytes >= kLimit || f_bytes >= kLimit || g_bytes >= kLimit || dp_bytes >= kLimit ||
+        df_bytes >= kLimit)
+        return bevpool_fail(BEVPOOL_ERR_OVERFLOW,
+                            "channels=%d: one frame's gradient or input tensor reaches 2 GiB",
+                            channels);
+    if (batch > 65535)
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "batch=%d exceeds 65535 frames per call", batch);
+
+    const int n_slices = (channels + kSliceChannels - 1) / kSliceChannels;
+    const int slice_c = (channels + n_slices - 1) / n_slices;
+    const int nch = (slice_c + 15) / 16;
+    const bool vec = nch == 5 && channels % 4 == 0 && slice_c % 4 == 0 &&
+                     reinterpret_cast<uintptr_t>(F) % (4 * esize) == 0 &&
+                     reinterpret_cast<uintptr_t>(G) % 16 == 0 &&
+                     (dF == nullptr || reinterpret_cast<uintptr_t>(dF) % 16 == 0);
+
+    BwdArgs a;
+    a.P = static_cast<const char *>(P);
+    a.F = static_cast<const char *>(F);
+    a.G = G;
+    a.dP = dP;
+    a.dF = dF;
+    a.cop = plan->cell_of_point;
+    a.combo_cells = plan->combo_cells;
+    a.N = g.n_cams;
+    a.D = g.n_depth;
+    a.H = g.feat_h;
+    a.W = g.feat_w;
+    a.HW = g.feat_h * g.feat_w;
+    a.C = channels;
+    a.p_bytes = uint32_t(p_bytes);
+    a.f_bytes = uint32_t(f_bytes);
+    a.g_bytes = uint32_t(g_bytes);
+    a.dp_bytes = dP ? uint32_t(dp_bytes) : 0u;
+    a.df_bytes = dF ? uint32_t(df_bytes) : 0u;
+    a.cop_bytes = uint32_t(plan->n_points * 4);
+    a.cc_bytes = uint32_t(int64_t(g.n_cams) * g.n_depth * g.feat_w * 4);
+    a.items_w = (g.feat_w + kBCols - 1) / kBCols;
+    a.items_h = (g.feat_h + kBRows - 1) / kBRows;
+    a.part = (g.n_depth + kBWaves - 1) / kBWaves;
+    a.want_dp = dP != nullptr;
+    a.want_df = dF != nullptr;
+    const dim3 grid(g.n_cams * a.items_w * a.items_h, batch);
+    for (int s = 0; s < n_slices; ++s) {
+        a.c0 = s * slice_c;
+        a.cn = std::min(slice_c, channels - a.c0);
+        a.accumulate_dp = s > 0;
+        switch (dtype) {
+            case BEVPOOL_F32: launch_bwd<BEVPOOL_F32>(a, grid, nch, vec, stream); break;
+            case BEVPOOL_BF16: launch_bwd<BEVPOOL_BF16>(a, grid, nch, vec, stream); break;
+            default: launch_bwd<BEVPOOL_F16>(a, grid, nch, vec, stream); break;
+        }
+        BEVPOOL_HIP(hipGetLastError());
+    }
+    return BEVPOOL_OK;
+}

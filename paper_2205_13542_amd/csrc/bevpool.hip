@@ -37,6 +37,7 @@ void free_plan(bevpool_plan_s *plan) {
     (void)hipFree(plan->multi_begin);
     (void)hipFree(plan->multi_cell);
     (void)hipFree(plan->multi_rows);
+    (void)hipFree(plan->combo_cells);
     if (prev >= 0 && prev != plan->device) (void)hipSetDevice(prev);
     plan->magic = 0;
     delete plan;
@@ -144,6 +145,24 @@ int bevpool_forward_timed(const void *depth_prob, const void *cam_feat, const be
                           void *hip_stream, void *start_event, void *stop_event) {
     return forward_checked(depth_prob, cam_feat, plan, bev_out, batch, channels, dtype, hip_stream,
                            start_event, stop_event);
+}
+
+int bevpool_backward(const float *grad_out, const void *depth_prob, const void *cam_feat,
+                     const bevpool_plan_t *plan, float *grad_depth, float *grad_feat,
+                     int32_t batch, int32_t channels, int32_t dtype, void *hip_stream) {
+    if (!valid_plan(plan)) return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "invalid plan handle");
+    if (!grad_out || !depth_prob || !cam_feat)
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG,
+                            "grad_out, depth_prob and cam_feat must be non-NULL");
+    if (!grad_depth && !grad_feat)
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "grad_depth and grad_feat are both NULL");
+    if (batch < 1 || channels < 1)
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "batch=%d and channels=%d must be >= 1", batch,
+                            channels);
+    if (dtype != BEVPOOL_F32 && dtype != BEVPOOL_BF16 && dtype != BEVPOOL_F16)
+        return bevpool_fail(BEVPOOL_ERR_UNSUPPORTED_DTYPE, "dtype %d is not F32, BF16 or F16", dtype);
+    return bevpool_launch_backward(grad_out, depth_prob, cam_feat, plan, grad_depth, grad_feat,
+                                   batch, channels, dtype, hipStream_t(hip_stream));
 }
 
 int bevpool_plan_info_get(const bevpool_plan_t *plan, bevpool_plan_info *info) {

@@ -84,6 +84,7 @@ struct bevpool_plan_s {
     int32_t *cell_start;     // [n_cells + 1]
     // forward work partition
     int2 *column_table;      // [N][D][W]: {cell or borrowed row or -1, h_lo | h_hi << 16 | flags}
+    int32_t *combo_cells;    // [N][D][W]: cell of a clean combo, -1 none kept, -2 not clean
     int32_t *multi_begin;    // [n_multi + 1]: first partial slot of each multi-combo cell
     int32_t *multi_cell;     // [n_multi]
     int32_t *multi_rows;     // [n_multi][kCombineInline]: borrowed rows of the first slots, or -1
@@ -108,6 +109,9 @@ int bevpool_hip_fail(hipError_t err, const char *what);
 int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
                        const bevpool_geometry &g, hipStream_t stream,
                        bevpool_plan_s *plan);
+int bevpool_launch_backward(const float *G, const void *P, const void *F,
+                            const bevpool_plan_s *plan, float *dP, float *dF, int32_t batch,
+                            int32_t channels, int32_t dtype, hipStream_t stream);
 int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *plan,
                            float *out, int32_t batch, int32_t channels,
                            int32_t dtype, hipStream_t stream, hipEvent_t start,

@@ -544,7 +544,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
     auto cleanup = [&]() {
         for (void *q : {(void *)d_calib, (void *)keys_a, (void *)keys_b, (void *)vals_a,
                         (void *)vals_b, (void *)hist, (void *)small, (void *)flag_a,
-                        (void *)flag_b, (void *)combo_cell, (void *)combo_range,
+                        (void *)flag_b, (void *)combo_range,
                         (void *)combo_flag, (void *)cell_generic, (void *)cell_ncombo,
                         (void *)head_scan, (void *)run_scan, (void *)run_begin,
                         (void *)pos_of_cell})
@@ -633,7 +633,9 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         BEVPOOL_HIP(hipGetLastError());
 
         // combos, cell classes and the column table
-        if ((rc2 = dev_alloc(&combo_cell, size_t(n_combo), "combo cells"))) return rc2;
+        // the combo cells stay with the plan (the backward pass reads them)
+        if ((rc2 = dev_alloc(&plan->combo_cells, size_t(n_combo), "combo cells"))) return rc2;
+        combo_cell = plan->combo_cells;
         if ((rc2 = dev_alloc(&combo_range, size_t(n_combo), "combo ranges"))) return rc2;
         if ((rc2 = dev_alloc(&combo_flag, size_t(n_combo) + 1, "combo flags"))) return rc2;
         if ((rc2 = dev_alloc(&cell_generic, size_t(n_cells), "cell classes"))) return rc2;

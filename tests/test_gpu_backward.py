@@ -1,0 +1,147 @@
+"""Backward pass on the GPU against the oracle's gradients (same inputs, same
+association). Bounds, per element: |dP - ref| <= 1e-4 sqrt(C) (a dot product
+of C terms of order one) and |dF - ref| <= 1e-4 sqrt(k), k the pixel's kept
+depth bins; dropped points and pixels without kept points exactly 0."""
+import numpy as np
+import pytest
+
+import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+@pytest.fixture(scope="module")
+def pkg():
+    import paper_2205_13542_amd as bp
+    bp._binding.load()
+    return bp
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def _dev(torch, a, dtype):
+    t = torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    return t.to({"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dtype]).contiguous()
+
+
+def _host_values(torch, a, dtype):
+    """The values the GPU sees: a rounded to dtype, widened back to fp32."""
+    return _dev(torch, a, dtype).float().cpu().numpy()
+
+
+def _check(torch, pkg, oracle_lib, w, G, dtype="f32", want_depth=True, want_feat=True):
+    rig = w.rig
+    P = _dev(torch, w.P, dtype)
+    F = _dev(torch, w.F, dtype)
+    Gd = torch.from_numpy(G).cuda().contiguous()
+    plan = pkg.Plan.from_rig(rig)
+    gd, gf = plan.backward(Gd, P, F, want_depth=want_depth, want_feat=want_feat)
+    torch.cuda.synchronize()
+    cop = oracle_lib.cell_map(rig)
+    refP, refF = oracle_lib.backward(rig, cop, _host_values(torch, w.P, dtype),
+                                     _host_values(torch, w.F, dtype), G)
+    C = w.channels
+    kept = cop >= 0
+    if want_depth:
+        got = gd.cpu().numpy().reshape(w.batch, -1)
+        ref = refP.reshape(w.batch, -1)
+        err = np.abs(got.astype(np.float64) - ref)
+        assert (err <= 1e-4 * np.sqrt(C)).all(), f"dP max err {err.max():.3g}"
+        assert (got[:, ~kept] == 0).all()
+    else:
+        assert gd is None
+    if want_feat:
+        got = gf.cpu().numpy().reshape(w.batch, rig.n_pixels, C)
+        ref = refF.reshape(w.batch, rig.n_pixels, C)
+        k = kept.reshape(rig.n_cams, rig.n_depth, -1).sum(axis=1).reshape(-1)
+        bound = 1e-4 * np.sqrt(np.maximum(k, 1))[None, :, None]
+        err = np.abs(got.astype(np.float64) - ref)
+        assert (err <= bound).all(), f"dF max err/bound {(err / bound).max():.3g}"
+        assert (got[:, k == 0] == 0).all()
+    else:
+        assert gf is None
+    plan.close()
+    return gd, gf
+
+
+def _grad(w, seed):
+    rng = np.random.default_rng(seed)
+    return rng.standard_normal((w.batch, w.rig.ny, w.rig.nx, w.channels)).astype(np.float32)
+
+
+@pytest.mark.parametrize("name,seed", [("tiny", 0), ("tiny_identity", 1), ("nuscenes", 2),
+                                       ("nuscenes_tilted", 3)])
+def test_backward_matches_oracle(torch_cuda, pkg, oracle_lib, name, seed):
+    """Level rig: every combo clean (one gradient row per combo); tilted rig:
+    mostly rows with cells of their own."""
+    _say(f"[backward] {name} seed={seed}")
+    w = wl.make(name, seed=seed)
+    _check(torch_cuda, pkg, oracle_lib, w, _grad(w, seed + 10))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_backward_reduced_precision_inputs(torch_cuda, pkg, oracle_lib, dtype):
+    _say(f"[backward] nuscenes {dtype}")
+    w = wl.make("nuscenes", seed=4)
+    _check(torch_cuda, pkg, oracle_lib, w, _grad(w, 14), dtype=dtype)
+
+
+@pytest.mark.parametrize("channels", [1, 5, 17, 64, 81, 160, 260])
+def test_backward_channel_counts(torch_cuda, pkg, oracle_lib, channels):
+    """Every lane-chunk count, 4-element lanes (160), and channel slices
+    (81, 160, 260: dP adds the slices' dot products)."""
+    _say(f"[backward] nuscenes_tilted C={channels}")
+    w = wl.make("nuscenes_tilted", seed=5, channels=channels)
+    _check(torch_cuda, pkg, oracle_lib, w, _grad(w, channels))
+
+
+def test_backward_batch_and_single_outputs(torch_cuda, pkg, oracle_lib):
+    _say("[backward] batch 2, one output at a time")
+    w = wl.make("nuscenes", seed=6, batch=2)
+    G = _grad(w, 16)
+    gd, gf = _check(torch_cuda, pkg, oracle_lib, w, G)
+    gd1, _ = _check(torch_cuda, pkg, oracle_lib, w, G, want_feat=False)
+    _, gf1 = _check(torch_cuda, pkg, oracle_lib, w, G, want_depth=False)
+    assert torch_cuda.equal(gd, gd1) and torch_cuda.equal(gf, gf1)
+
+
+def test_backward_deterministic(torch_cuda, pkg):
+    torch = torch_cuda
+    w = wl.make("nuscenes_tilted", seed=7)
+    plan = pkg.Plan.from_rig(w.rig)
+    P, F = _dev(torch, w.P, "f32"), _dev(torch, w.F, "f32")
+    G = torch.from_numpy(_grad(w, 17)).cuda()
+    a = plan.backward(G, P, F)
+    b = plan.backward(G, P, F)
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+    plan.close()
+
+
+def test_backward_adjoint_on_gpu(torch_cuda, pkg):
+    """<G, forward(P, F)> = <P, dP> = <F, dF> with the GPU's own forward and
+    backward, in double on the host."""
+    torch = torch_cuda
+    w = wl.make("nuscenes", seed=8)
+    plan = pkg.Plan.from_rig(w.rig)
+    P, F = _dev(torch, w.P, "f32"), _dev(torch, w.F, "f32")
+    G = torch.from_numpy(_grad(w, 18)).cuda()
+    out = plan.forward(P, F)
+    gd, gf = plan.backward(G, P, F)
+    torch.cuda.synchronize()
+    d = lambda x: x.double().cpu()
+    lhs = float((d(G) * d(out)).sum())
+    via_p = float((d(P) * d(gd)).sum())
+    via_f = float((d(F) * d(gf)).sum())
+    scale = float((d(G).abs() * d(out).abs()).sum())
+    assert abs(lhs - via_p) <= 1e-5 * scale and abs(lhs - via_f) <= 1e-5 * scale
+    plan.close()
