@@ -42,6 +42,7 @@ FLUSH_BYTES = 1 << 30
 PLAN_REBUILDS = 4               # plan builds timed after the first
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "forward_traffic.json")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2205_13542_amd", "csrc", "forward.hip")
+BWD_SOURCE = os.path.join(ROOT, "paper_2205_13542_amd", "csrc", "backward.hip")
 
 WORKLOAD_TEXT = {
     "nuscenes": "nuScenes-shaped frame: 6 cams x 118 depth bins x 32x88, C=80 fp32 -> 360x360 BEV at 0.3 m",
@@ -62,6 +63,9 @@ def parse_args():
                     help="skip the oracle timing on the host cores")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU time budget of the oracle sample")
+    ap.add_argument("--backward", action="store_true",
+                    help="time bevpool_backward (gradients of P and F) instead of the forward; "
+                         "prints its own JSON line")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device-to-device copy of 256 MiB five times (the "
                          "reference kernel for scaling the FETCH_SIZE / WRITE_SIZE counters)")
@@ -97,8 +101,8 @@ def algorithmic_bytes(w) -> int:
     return p + f + o
 
 
-def kernel_hash() -> str:
-    with open(KERNEL_SOURCE, "rb") as fh:
+def kernel_hash(path: str = KERNEL_SOURCE) -> str:
+    with open(path, "rb") as fh:
         return hashlib.sha256(fh.read()).hexdigest()[:16]
 
 
@@ -153,6 +157,92 @@ def cpu_baseline(w, nbytes: int, budget_s: float):
     }
 
 
+BWD_METRIC = ("BEV-pool backward ms + HBM GB/s (gradients of P and F), 6cam×118D×32×88×C80"
+              "→360×360 BEV, 1 GPU")
+
+
+def backward_bench(args):
+    """bevpool_backward on the workload: P, F and a standard-normal gradient
+    of the BEV map resident in HBM; each timed call after a cache-evicting
+    read, timed by events recorded as stream entries around the call.
+    Algorithmic bytes: P, F and the gradient rows of the non-empty cells
+    read, dP and dF written (the plan's cell map is reported beside them)."""
+    import numpy as np
+    import torch
+    import workloads as wl
+    import paper_2205_13542_amd as bp
+    import oracle
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = wl.make(args.workload, seed=0)
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[w.dtype]
+    P = torch.from_numpy(w.P).to(dev).to(tdt).contiguous()
+    F = torch.from_numpy(w.F).to(dev).to(tdt).contiguous()
+    rng = np.random.default_rng(1)
+    G_host = rng.standard_normal((w.batch, w.rig.ny, w.rig.nx, w.channels)).astype(np.float32)
+    G = torch.from_numpy(G_host).to(dev)
+    flush = torch.zeros(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
+    flush_out = torch.zeros((), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    plan = bp.Plan.from_rig(w.rig, stream=stream)
+    info = plan.info
+    for _ in range(args.warmup):
+        torch.sum(flush, dim=0, out=flush_out)
+        plan.backward(G, P, F, stream=stream)
+    torch.cuda.synchronize()
+    ms = []
+    for _ in range(args.steps):
+        torch.sum(flush, dim=0, out=flush_out)
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0.record(stream)
+        plan.backward(G, P, F, stream=stream)
+        s1.record(stream)
+        torch.cuda.synchronize()
+        ms.append(s0.elapsed_time(s1))
+    ms = np.array(ms)
+    esize = 4 if w.dtype == "f32" else 2
+    per_frame = (w.rig.n_points * esize + w.rig.n_pixels * w.channels * esize
+                 + info.n_nonempty * w.channels * 4
+                 + w.rig.n_points * 4 + w.rig.n_pixels * w.channels * 4)
+    nbytes = per_frame * w.batch
+    mean_ms = float(ms.mean())
+    gbs = nbytes / (mean_ms * 1e-3) / 1e9
+    rec = {
+        "metric": BWD_METRIC, "value": round(gbs, 2), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(mean_ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": WORKLOAD_TEXT[args.workload], "name": args.workload,
+                   "batch": w.batch, "outputs": "dP and dF"},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None},
+        "backward_us": {"mean": round(mean_ms * 1e3, 2),
+                        "median": round(float(np.median(ms)) * 1e3, 2),
+                        "min": round(float(ms.min()) * 1e3, 2)},
+        "algorithmic_bytes": nbytes,
+        "plan_bytes_read": w.rig.n_points * 4 + w.rig.n_cams * w.rig.n_depth * w.rig.feat_w * 4,
+        "kernel_sha256_16": kernel_hash(BWD_SOURCE),
+    }
+    if not args.no_cpu_baseline:
+        cop = oracle.cell_map(w.rig)
+        frames, spent = 0, 0.0
+        while frames == 0 or (spent < args.cpu_seconds / 2 and frames < 16):
+            b = frames % w.batch
+            t0 = time.perf_counter()
+            oracle.backward(w.rig, cop, w.P[b:b + 1], w.F[b:b + 1], G_host[b:b + 1])
+            spent += time.perf_counter() - t0
+            frames += 1
+        rec["cpu_baseline"] = {
+            "value": round(per_frame * frames / spent / 1e9, 4), "unit": "GB/s",
+            "cores": oracle.max_threads(), "kind": "oracle",
+            "sample": f"{frames} whole frame(s) of the same workload, {spent:.1f} s "
+                      f"({spent / frames * 1e3:.0f} ms/frame); host CPU {cpu_model()}, "
+                      f"os.cpu_count()={os.cpu_count()}"}
+    plan.close()
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -162,6 +252,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.backward:
+        backward_bench(args)
         return
 
     import numpy as np
