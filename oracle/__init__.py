@@ -19,6 +19,10 @@ Functions and the passages they follow:
   "Interval Reduction": a cell's points are then consecutive).
 - ``pool``: per-cell sums of P * F ("Interval Reduction": sum is one of the
   symmetric aggregations; "Takeaways": exact, no approximation).
+- ``pool_reduce``: per-cell mean or max of P * F ("Interval Reduction": mean
+  and max are the other symmetric aggregations it names); 0 for empty cells.
+- ``pool_slabs``: several z slabs, each pooled on its own, concatenated
+  along channels (Sec. III-B: flattening along z).
 - ``backward``: the gradients of ``pool`` with respect to P and F for a given
   gradient of the BEV map (the pooling is one differentiable layer of a
   model trained end to end): dP[p] = F[pixel(p)] . G[cell(p)] and
@@ -31,13 +35,18 @@ product, the count test, mass conservation, and permutation, linearity and
 boundary cases; for the gradients, the adjoint identities
 <G, pool(P, F)> = <P, dP> = <F, dF> against ``pool``, a dense Jacobian of
 ``pool`` built column by column on the tiny rig, and all-ones cases with
-integer answers. Values at the nuScenes-shaped sizes are pinned only by these
+integer answers; for mean and max, numpy's ``add.at``/``bincount`` and
+``maximum.at`` over the cell map, the golden cell maps of the tiny rig
+(point-id probabilities give each cell's largest point id), and ordering
+invariants; for slabs, the union of dyadic slabs against one slab of the
+union's height. Values at the nuScenes-shaped sizes are pinned only by these
 properties: the paper prints no pooled value (parity unpinned by the paper,
 pinned by the invariants).
 """
 from __future__ import annotations
 
 import ctypes
+import dataclasses
 import os
 import subprocess
 
@@ -91,6 +100,9 @@ def _load():
     lib.oracle_backward.argtypes = [P, P, P, P, ctypes.POINTER(_Geom), ctypes.c_int32,
                                     ctypes.c_int32, P, P]
     lib.oracle_backward.restype = None
+    lib.oracle_pool_reduce.argtypes = [P, P, P, ctypes.POINTER(_Geom), ctypes.c_int32,
+                                       ctypes.c_int32, ctypes.c_int32, P]
+    lib.oracle_pool_reduce.restype = None
     lib.oracle_max_threads.argtypes = []
     lib.oracle_max_threads.restype = ctypes.c_int
     _lib = lib
@@ -164,6 +176,49 @@ def pool(rig, cell_of_point: np.ndarray, P: np.ndarray, F: np.ndarray,
     if want_abs:
         res.append(a64)
     return res[0] if len(res) == 1 else tuple(res)
+
+
+REDUCE_MODES = {"mean": 1, "max": 2}
+
+
+def pool_reduce(rig, cell_of_point: np.ndarray, P: np.ndarray, F: np.ndarray, mode: str):
+    """Mean or max pooling ("Interval Reduction": mean and max are the other
+    symmetric aggregations it names). Returns float64 [B][ny][nx][C]: per
+    cell the mean, or the max, of P * F over its kept points; 0 for a cell
+    without points."""
+    lib = _load()
+    P = np.ascontiguousarray(P, dtype=np.float32)
+    F = np.ascontiguousarray(F, dtype=np.float32)
+    B = P.shape[0]
+    C = F.shape[-1]
+    assert P.size == B * rig.n_points and F.size == B * rig.n_pixels * C
+    cop = np.ascontiguousarray(cell_of_point, dtype=np.int32)
+    out = np.empty((B, rig.ny, rig.nx, C), dtype=np.float64)
+    g = _geom(rig)
+    lib.oracle_pool_reduce(_ptr(P), _ptr(F), _ptr(cop), ctypes.byref(g), B, C,
+                           REDUCE_MODES[mode], _ptr(out))
+    return out
+
+
+def slab_rig(rig, iz: int):
+    """The rig restricted to z slab iz: [z_min + iz z_cell, z_min + (iz+1) z_cell)."""
+    return dataclasses.replace(rig, z_min=rig.z_min + iz * rig.z_cell)
+
+
+def pool_slabs(rig, nz: int, P: np.ndarray, F: np.ndarray, mode: str = "sum"):
+    """Pooling over nz stacked z slabs, flattened along z by concatenating
+    the slabs' channels (Sec. III-B: the features are flattened along the
+    z-axis): out[b][iy][ix][iz * C + c] is the pooled value of slab iz.
+    Returns float64 [B][ny][nx][nz * C]."""
+    parts = []
+    for iz in range(nz):
+        r = slab_rig(rig, iz)
+        cop = cell_map(r)
+        if mode == "sum":
+            parts.append(pool(r, cop, P, F, want_f64=True)[1])
+        else:
+            parts.append(pool_reduce(r, cop, P, F, mode))
+    return np.concatenate(parts, axis=-1)
 
 
 def backward(rig, cell_of_point: np.ndarray, P: np.ndarray, F: np.ndarray, G: np.ndarray):

@@ -21,7 +21,7 @@
  *     points of one cell are consecutive ("Interval Reduction" paragraph).
  *   - Pooling by sum, one of the symmetric functions the "Interval Reduction"
  *     paragraph allows, with no approximation ("Takeaways" paragraph: the
- *     method is exact).
+ *     method is exact); and by mean and max, the other two it names.
  *
  * Readings where the paper is silent (each one is also listed with the design
  * notes of the GPU library, which implements the same readings independently):
@@ -194,6 +194,75 @@ void oracle_pool(const float *P, const float *F, const int32_t *cell_of_point,
         free(acc);
         free(aacc);
     }
+}
+
+/*
+ * Mean and max pooling: the other two symmetric functions the "Interval
+ * Reduction" paragraph names for aggregating a cell's points.
+ *   mode 1 (mean): out = (sum over the cell's kept points of P * F) divided
+ *                  by the number of those points, in double;
+ *   mode 2 (max):  out = the largest P * F over those points, per channel;
+ *                  each product is exact in double (a float times a float
+ *                  has at most 48 significant bits).
+ * A cell without points gets 0 in both modes. P, F and the layouts are those
+ * of oracle_pool; out64: [B][ny][nx][C] double. Channels are split across
+ * threads as in oracle_pool.
+ */
+void oracle_pool_reduce(const float *P, const float *F, const int32_t *cell_of_point,
+                        const oracle_geometry *g, int32_t batch, int32_t channels,
+                        int32_t mode, double *out64) {
+    const int64_t NP = n_points_of(g);
+    const int64_t HW = (int64_t)g->feat_h * g->feat_w;
+    const int64_t DHW = (int64_t)g->n_depth * HW;
+    const int64_t n_pix = (int64_t)g->n_cams * HW;
+    const int64_t n_cells = (int64_t)g->nx * g->ny;
+    const int64_t C = channels;
+    int64_t *count = (int64_t *)calloc((size_t)n_cells, sizeof(int64_t));
+    for (int64_t p = 0; p < NP; ++p) {
+        if (cell_of_point[p] >= 0) ++count[cell_of_point[p]];
+    }
+    for (int32_t b = 0; b < batch; ++b) {
+        const float *Pb = P + (size_t)b * NP;
+        const float *Fb = F + (size_t)b * n_pix * C;
+        double *acc = out64 + (size_t)b * n_cells * C;
+        const double init = mode == 2 ? -INFINITY : 0.0;
+        for (int64_t i = 0; i < n_cells * C; ++i) acc[i] = init;
+#pragma omp parallel
+        {
+            int64_t c0 = 0, c1 = C;
+#ifdef _OPENMP
+            const int64_t nt = omp_get_num_threads(), t = omp_get_thread_num();
+            const int64_t slice = (C + nt - 1) / nt;
+            c0 = t * slice < C ? t * slice : C;
+            c1 = c0 + slice < C ? c0 + slice : C;
+#endif
+            for (int64_t p = 0; p < NP && c0 < c1; ++p) {
+                const int32_t cell = cell_of_point[p];
+                if (cell < 0) continue;
+                const int64_t n = p / DHW;
+                const int64_t hw = p % HW;
+                const double prob = (double)Pb[p];
+                const float *feat = Fb + (n * HW + hw) * C;
+                double *a = acc + (int64_t)cell * C;
+                for (int64_t c = c0; c < c1; ++c) {
+                    const double term = prob * (double)feat[c];
+                    if (mode == 2) {
+                        if (term > a[c]) a[c] = term;
+                    } else {
+                        a[c] += term;
+                    }
+                }
+            }
+        }
+        for (int64_t cell = 0; cell < n_cells; ++cell) {
+            double *a = acc + cell * C;
+            for (int64_t c = 0; c < C; ++c) {
+                if (count[cell] == 0) a[c] = 0.0;
+                else if (mode == 1) a[c] = a[c] / (double)count[cell];
+            }
+        }
+    }
+    free(count);
 }
 
 /*

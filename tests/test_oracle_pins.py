@@ -388,3 +388,141 @@ def test_backward_all_ones(oracle_lib):
     assert (dP.reshape(-1) == np.where(cop >= 0, C, 0)).all()
     kept = (cop.reshape(rig.n_cams, rig.n_depth, rig.feat_h * rig.feat_w) >= 0).sum(axis=1)
     assert (dF.reshape(rig.n_pixels, C) == kept.reshape(-1)[:, None]).all()
+
+
+# ------------------------------------------------------------------ mean / max pins
+
+def _terms(w, cop):
+    """(kept cells, exact double P * F of every kept point)."""
+    rig = w.rig
+    kept = cop >= 0
+    p = np.arange(rig.n_points)[kept]
+    terms = w.P[0].reshape(-1)[kept, None].astype(np.float64) * \
+        w.F[0].reshape(rig.n_pixels, -1)[_pixel_of(rig, p)].astype(np.float64)
+    return cop[kept], terms
+
+
+@pytest.mark.parametrize("name,channels", [("tiny", None), ("tiny_identity", None),
+                                           ("nuscenes_tilted", 6)])
+def test_mean_max_numpy_ufunc_route(oracle_lib, name, channels):
+    """Mean through numpy's add.at and bincount, max through maximum.at, over
+    the cell map: library routines, no loop of ours. The max is exact (the
+    same exact products), the mean agrees to double rounding."""
+    w = wl.make(name, seed=5, channels=channels)
+    rig = w.rig
+    cop = oracle_lib.cell_map(rig)
+    cells, terms = _terms(w, cop)
+    C = terms.shape[1]
+    cnt = np.bincount(cells, minlength=rig.n_cells)
+    s = np.zeros((rig.n_cells, C))
+    np.add.at(s, cells, terms)
+    a = np.zeros((rig.n_cells, C))
+    np.add.at(a, cells, np.abs(terms))
+    m = np.full((rig.n_cells, C), -np.inf)
+    np.maximum.at(m, cells, terms)
+    has = cnt[:, None] > 0
+    mean_ref = np.where(has, s / np.maximum(cnt, 1)[:, None], 0.0)
+    max_ref = np.where(has, m, 0.0)
+    mean = oracle_lib.pool_reduce(rig, cop, w.P, w.F, "mean")[0].reshape(rig.n_cells, C)
+    mx = oracle_lib.pool_reduce(rig, cop, w.P, w.F, "max")[0].reshape(rig.n_cells, C)
+    assert (mx == max_ref).all()
+    scale = a / np.maximum(cnt, 1)[:, None] + 1e-300
+    assert (np.abs(mean - mean_ref) <= 1e-13 * scale).all()
+    assert (mean[~has[:, 0]] == 0).all() and (mx[~has[:, 0]] == 0).all()
+
+
+def test_mean_max_tiny_golden():
+    """Tiny rig, C = 1, F = 1 and P = (point id + 1) / 1024 (exact dyadics):
+    each cell's max is its largest point id and its mean the mean id, both
+    computed here from the hand-derived cell map in the golden file (a cell
+    (ix, iy) holds the points with depth d = ix - 8 and any row h whose
+    column w has iy in the table)."""
+    import oracle
+    rig = wl.tiny_rig()
+    g = _read_golden("tiny_rig_closed_form.txt")
+    H, W = rig.feat_h, rig.feat_w
+    members = {}
+    for dd in range(1, 8):
+        iys = [int(v) for v in g[f"iy d={dd}"]]
+        for wcol in range(W):
+            cell = iys[wcol] * 16 + (dd + 8)
+            for h in range(H):
+                members.setdefault(cell, []).append(((dd - 1) * H + h) * W + wcol)
+    exp_max = np.zeros(rig.n_cells)
+    exp_mean = np.zeros(rig.n_cells)
+    for cell, ids in members.items():
+        exp_max[cell] = (max(ids) + 1) / 1024.0
+        exp_mean[cell] = (sum(ids) + len(ids)) / len(ids) / 1024.0
+    P = ((np.arange(rig.n_points) + 1) / 1024.0).astype(np.float32)[None]
+    F = np.ones((1, rig.n_pixels, 1), dtype=np.float32)
+    cop = oracle.cell_map(rig)
+    mx = oracle.pool_reduce(rig, cop, P, F, "max").reshape(-1)
+    mean = oracle.pool_reduce(rig, cop, P, F, "mean").reshape(-1)
+    assert (mx == exp_max).all()
+    assert np.allclose(mean, exp_mean, rtol=1e-15, atol=0)
+    assert len(members) == int(g["nonempty"][0])
+
+
+def test_min_mean_max_order(oracle_lib):
+    """Per non-empty cell and channel: min <= mean <= max, with the min taken
+    as -max of P * (-F)."""
+    w = wl.make("nuscenes_tilted", seed=6, channels=4)
+    cop = oracle_lib.cell_map(w.rig)
+    mx = oracle_lib.pool_reduce(w.rig, cop, w.P, w.F, "max")
+    mn = -oracle_lib.pool_reduce(w.rig, cop, w.P, -w.F, "max")
+    mean = oracle_lib.pool_reduce(w.rig, cop, w.P, w.F, "mean")
+    has = np.bincount(cop[cop >= 0], minlength=w.rig.n_cells).reshape(1, w.rig.ny, w.rig.nx, 1) > 0
+    tol = 1e-12 * (np.abs(mx) + np.abs(mn))
+    assert ((mn <= mean + tol) | ~has).all() and ((mean <= mx + tol) | ~has).all()
+    assert (mn[has[..., 0]] < mx[has[..., 0]]).mean() > 0.5
+
+
+# ------------------------------------------------------------------ z slab pins
+
+def test_slabs_identity_rig_union():
+    """Identity rig (z = d exactly): slabs of 2 m from z = 0 partition the
+    points of the single 8 m slab [0, 8); every kept point keeps its (x, y)
+    cell, and the slabs' sums add up to the sum over the 8 m slab."""
+    import oracle
+    w = wl.make("tiny_identity", seed=7)
+    base = dataclasses.replace(w.rig, z_min=0.0, z_cell=2.0)
+    union = dataclasses.replace(w.rig, z_min=0.0, z_cell=8.0)
+    cu = oracle.cell_map(union)
+    hits = np.zeros(base.n_points, dtype=np.int64)
+    for iz in range(4):
+        c = oracle.cell_map(oracle.slab_rig(base, iz))
+        hits += c >= 0
+        assert (c[c >= 0] == cu[c >= 0]).all()
+    assert ((hits == 1) == (cu >= 0)).all() and hits.max() <= 1
+    _, k, _, _ = _decode(base, np.arange(base.n_points))
+    assert ((cu >= 0) == (k + 1 < 8)).all()
+    cat = oracle.pool_slabs(base, 4, w.P, w.F)
+    C = w.channels
+    total = sum(cat[..., iz * C:(iz + 1) * C] for iz in range(4))
+    _, ref = oracle.pool(union, cu, w.P, w.F, want_f64=True)
+    _, a64 = oracle.pool(union, cu, np.abs(w.P), np.abs(w.F), want_f64=True)
+    assert (np.abs(total - ref) <= 1e-13 * (a64 + 1e-300)).all()
+
+
+def test_slabs_ring_rig_union():
+    """nuScenes-shaped rig, four 4 m slabs from z = -8 m against the 16 m slab
+    [-8, 8): the same partition of the kept points at full size."""
+    import oracle
+    rig = dataclasses.replace(wl.ring_rig(), z_min=-8.0, z_cell=4.0)
+    cu = oracle.cell_map(dataclasses.replace(rig, z_cell=16.0))
+    hits = np.zeros(rig.n_points, dtype=np.int64)
+    for iz in range(4):
+        c = oracle.cell_map(oracle.slab_rig(rig, iz))
+        hits += c >= 0
+        assert (c[c >= 0] == cu[c >= 0]).all()
+    assert ((hits == 1) == (cu >= 0)).all()
+    assert 0.2 < (cu >= 0).mean() < 1.0
+
+
+def test_one_slab_is_pool(oracle_lib):
+    w = wl.make("tiny", seed=8)
+    cop = oracle_lib.cell_map(w.rig)
+    _, ref = oracle_lib.pool(w.rig, cop, w.P, w.F, want_f64=True)
+    assert (oracle_lib.pool_slabs(w.rig, 1, w.P, w.F) == ref).all()
+    ref_max = oracle_lib.pool_reduce(w.rig, cop, w.P, w.F, "max")
+    assert (oracle_lib.pool_slabs(w.rig, 1, w.P, w.F, "max") == ref_max).all()
