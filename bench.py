@@ -63,6 +63,10 @@ def parse_args():
                     help="skip the oracle timing on the host cores")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU time budget of the oracle sample")
+    ap.add_argument("--reduce", default="sum", choices=["sum", "mean", "max"],
+                    help="aggregation (mean/max, and --slabs, are timed by reduce_bench)")
+    ap.add_argument("--slabs", type=int, default=1,
+                    help="z slabs of 4 m from z = -8 m, flattened by channel concatenation")
     ap.add_argument("--backward", action="store_true",
                     help="time bevpool_backward (gradients of P and F) instead of the forward; "
                          "prints its own JSON line")
@@ -243,6 +247,93 @@ def backward_bench(args):
     print(json.dumps(rec), flush=True)
 
 
+def reduce_bench(args):
+    """bevpool_forward_ex with --reduce mean/max, or --slabs nz z slabs
+    (one plan per slab, each writing its channel block of one map): timed by
+    events recorded as stream entries around the call, each call after a
+    cache-evicting read. Algorithmic bytes: P and F read once, the map
+    (nz x C channels per cell) written once; each slab's call reads P and F
+    again, which the figure does not credit."""
+    import dataclasses
+    import numpy as np
+    import torch
+    import workloads as wl
+    import paper_2205_13542_amd as bp
+    import oracle
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = wl.make(args.workload, seed=0)
+    nz = args.slabs
+    rig = w.rig if nz == 1 else dataclasses.replace(w.rig, z_min=-8.0, z_cell=4.0)
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[w.dtype]
+    P = torch.from_numpy(w.P).to(dev).to(tdt).contiguous()
+    F = torch.from_numpy(w.F).to(dev).to(tdt).contiguous()
+    flush = torch.zeros(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
+    flush_out = torch.zeros((), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    sp = bp.SlabPlan.from_rig(rig, nz, stream=stream)
+    out = torch.empty((w.batch, rig.ny, rig.nx, nz * w.channels), dtype=torch.float32, device=dev)
+    for _ in range(args.warmup):
+        torch.sum(flush, dim=0, out=flush_out)
+        sp.forward(P, F, out=out, stream=stream, reduce=args.reduce)
+    torch.cuda.synchronize()
+    ms = []
+    for _ in range(args.steps):
+        torch.sum(flush, dim=0, out=flush_out)
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0.record(stream)
+        sp.forward(P, F, out=out, stream=stream, reduce=args.reduce)
+        s1.record(stream)
+        torch.cuda.synchronize()
+        ms.append(s0.elapsed_time(s1))
+    ms = np.array(ms)
+    esize = 4 if w.dtype == "f32" else 2
+    per_frame = (rig.n_points * esize + rig.n_pixels * w.channels * esize
+                 + rig.n_cells * nz * w.channels * 4)
+    nbytes = per_frame * w.batch
+    mean_ms = float(ms.mean())
+    gbs = nbytes / (mean_ms * 1e-3) / 1e9
+    what = f"{args.reduce}" + (f", {nz} z slabs of 4 m from -8 m (C x {nz} channels)" if nz > 1 else "")
+    rec = {
+        "metric": f"BEV-pool forward ({what}) ms + HBM GB/s, 1 GPU", "value": round(gbs, 2),
+        "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(mean_ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": WORKLOAD_TEXT[args.workload], "name": args.workload,
+                   "batch": w.batch, "reduce": args.reduce, "slabs": nz},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None},
+        "forward_us": {"mean": round(mean_ms * 1e3, 2),
+                       "median": round(float(np.median(ms)) * 1e3, 2),
+                       "min": round(float(ms.min()) * 1e3, 2)},
+        "algorithmic_bytes": nbytes,
+        "kernel_sha256_16": kernel_hash(),
+    }
+    if not args.no_cpu_baseline:
+        frames, spent = 0, 0.0
+        cops = [oracle.cell_map(oracle.slab_rig(rig, iz)) for iz in range(nz)]
+        while frames == 0 or (spent < args.cpu_seconds / 2 and frames < 16):
+            b = frames % w.batch
+            t0 = time.perf_counter()
+            for iz in range(nz):
+                r = oracle.slab_rig(rig, iz)
+                if args.reduce == "sum":
+                    oracle.pool(r, cops[iz], w.P[b:b + 1], w.F[b:b + 1])
+                else:
+                    oracle.pool_reduce(r, cops[iz], w.P[b:b + 1], w.F[b:b + 1], args.reduce)
+            spent += time.perf_counter() - t0
+            frames += 1
+        rec["cpu_baseline"] = {
+            "value": round(per_frame * frames / spent / 1e9, 4), "unit": "GB/s",
+            "cores": oracle.max_threads(), "kind": "oracle",
+            "sample": f"{frames} whole frame(s) of the same workload, {spent:.1f} s "
+                      f"({spent / frames * 1e3:.0f} ms/frame); host CPU {cpu_model()}, "
+                      f"os.cpu_count()={os.cpu_count()}"}
+    sp.close()
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -255,6 +346,9 @@ def main():
         return
     if args.backward:
         backward_bench(args)
+        return
+    if args.reduce != "sum" or args.slabs != 1:
+        reduce_bench(args)
         return
 
     import numpy as np

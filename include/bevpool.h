@@ -5,8 +5,9 @@
  * Sec. III-B). Each camera feature pixel is lifted to D points along its
  * camera ray, and each point carries its depth probability times the pixel's
  * feature vector. The points are quantised to an r x r BEV grid and flattened
- * along z (first paragraph). All points of a cell are summed (the "Interval
- * Reduction" paragraph allows sum, mean or max; this library sums).
+ * along z (first paragraph). All points of a cell are summed, or averaged,
+ * or their maximum is taken (the "Interval Reduction" paragraph names sum,
+ * mean and max; bevpool_forward sums, bevpool_forward_ex does all three).
  *
  * The point-to-cell association depends only on the calibration, so it is
  * computed once per rig ("Precomputation" paragraph). That is bevpool_plan.
@@ -52,6 +53,11 @@ extern "C" {
 
 /* Element type of depth_prob and cam_feat. Accumulation and output are fp32. */
 typedef enum { BEVPOOL_F32 = 0, BEVPOOL_BF16 = 1, BEVPOOL_F16 = 2 } bevpool_dtype;
+
+/* Aggregation of a cell's points (the "Interval Reduction" paragraph of
+ * Sec. III-B names mean, max and sum as symmetric functions to use). A cell
+ * without points gets 0 in every mode. */
+typedef enum { BEVPOOL_SUM = 0, BEVPOOL_MEAN = 1, BEVPOOL_MAX = 2 } bevpool_reduce;
 
 /*
  * Frustum and BEV grid (Sec. III-B, first paragraph: N cameras, an H x W
@@ -146,6 +152,32 @@ BEVPOOL_API int bevpool_forward(const void *depth_prob, const void *cam_feat,
                     const bevpool_plan_t *plan, float *bev_out,
                     int32_t batch, int32_t channels, int32_t dtype,
                     void *hip_stream);
+
+/*
+ * bevpool_forward with a choice of aggregation and a strided output.
+ *  reduce:         a bevpool_reduce. SUM is bevpool_forward's sum. MEAN
+ *                  divides each cell's fp32 sum by its number of kept points.
+ *                  MAX takes, per channel, the largest fp32 product P * F over
+ *                  the cell's kept points (exact: no sum is involved).
+ *  out_row_stride: floats from one cell's row of bev_out to the next
+ *                  (>= channels). The call writes floats [0, channels) of
+ *                  each row and no other element of bev_out, so several
+ *                  calls can fill disjoint channel ranges of one map: with
+ *                  nz z slabs (one plan per slab, each slab's z_min raised by
+ *                  z_cell), slab iz writes at bev_out + iz * channels with
+ *                  out_row_stride = nz * channels, which flattens the slabs
+ *                  along z by concatenating their channels (Sec. III-B, first
+ *                  paragraph). Frame b starts at bev_out + b * ny * nx *
+ *                  out_row_stride.
+ * Other arguments, ownership, asynchrony and determinism are those of
+ * bevpool_forward. Errors: those of bevpool_forward, and INVALID_ARG for an
+ * unknown reduce or out_row_stride < channels; OVERFLOW when ny * nx *
+ * out_row_stride floats reach 2 GiB.
+ */
+BEVPOOL_API int bevpool_forward_ex(const void *depth_prob, const void *cam_feat,
+                       const bevpool_plan_t *plan, float *bev_out, int64_t out_row_stride,
+                       int32_t batch, int32_t channels, int32_t dtype, int32_t reduce,
+                       void *hip_stream);
 
 /*
  * bevpool_forward with kernel-boundary timing, for measurement: start_event

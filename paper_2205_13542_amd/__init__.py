@@ -14,14 +14,17 @@ from __future__ import annotations
 import numpy as np
 
 from . import _binding
-from ._binding import (BEVPOOL_BF16, BEVPOOL_F16, BEVPOOL_F32, BevpoolError,
-                       bevpool_backward, bevpool_forward, bevpool_forward_timed, bevpool_geometry,
+from ._binding import (BEVPOOL_BF16, BEVPOOL_F16, BEVPOOL_F32, BEVPOOL_MAX, BEVPOOL_MEAN,
+                       BEVPOOL_SUM, BevpoolError,
+                       bevpool_backward, bevpool_forward, bevpool_forward_ex,
+                       bevpool_forward_timed, bevpool_geometry,
                        bevpool_last_error,
                        bevpool_plan, bevpool_plan_destroy, bevpool_plan_export,
                        bevpool_plan_info_get, bevpool_version)
 
 __all__ = [
-    "Plan", "BevpoolError", "bevpool_plan", "bevpool_forward", "bevpool_forward_timed",
+    "Plan", "SlabPlan", "BevpoolError", "bevpool_plan", "bevpool_forward", "bevpool_forward_ex",
+    "bevpool_forward_timed", "bevpool_backward", "BEVPOOL_SUM", "BEVPOOL_MEAN", "BEVPOOL_MAX",
     "bevpool_plan_info_get",
     "bevpool_plan_export", "bevpool_plan_destroy", "bevpool_last_error", "bevpool_version",
     "bevpool_geometry", "geometry_of", "BEVPOOL_F32", "BEVPOOL_BF16", "BEVPOOL_F16",
@@ -39,6 +42,9 @@ def geometry_of(rig) -> bevpool_geometry:
 def _torch():
     import torch
     return torch
+
+
+_REDUCE = {"sum": BEVPOOL_SUM, "mean": BEVPOOL_MEAN, "max": BEVPOOL_MAX}
 
 
 def _dtype_code(t) -> int:
@@ -92,12 +98,16 @@ class Plan:
         bevpool_plan_export(self.handle, cop, sp, cs)
         return cop, sp, cs
 
-    def forward(self, depth_prob, cam_feat, out=None, stream=None, events=None):
+    def forward(self, depth_prob, cam_feat, out=None, stream=None, events=None, reduce="sum"):
         """depth_prob [B][N][D][H][W], cam_feat [B][N][H][W][C] device tensors
         of one dtype (fp32, bf16 or fp16); returns fp32 [B][ny][nx][C].
+        reduce: "sum", "mean" or "max" (bevpool_forward_ex for the last two).
+        out: optional fp32 [B][ny][nx][C] device tensor, contiguous or a
+        channel slice of a wider map (rows out.stride(2) floats apart, the
+        call then writes only that slice).
         events: optional (start, stop) pair of timing-enabled torch.cuda.Event,
         recorded by the forward's own first and last kernel dispatch
-        (bevpool_forward_timed)."""
+        (bevpool_forward_timed; sum only)."""
         torch = _torch()
         i = self.info
         if depth_prob.dim() != 5 or cam_feat.dim() != 5:
@@ -117,15 +127,27 @@ class Plan:
             raise BevpoolError(_binding.BEVPOOL_ERR_INVALID_ARG, "inputs must be device tensors")
         if not (depth_prob.is_contiguous() and cam_feat.is_contiguous()):
             raise BevpoolError(_binding.BEVPOOL_ERR_INVALID_ARG, "inputs must be contiguous")
+        if reduce not in _REDUCE:
+            raise BevpoolError(_binding.BEVPOOL_ERR_INVALID_ARG, f"reduce {reduce!r}")
         if out is None:
             out = torch.empty((B, i.ny, i.nx, C), dtype=torch.float32, device=cam_feat.device)
-        elif (tuple(out.shape) != (B, i.ny, i.nx, C) or out.dtype != torch.float32
-              or not out.is_contiguous() or not out.is_cuda):
+        ldo = out.stride(2) if out.dim() == 4 else -1
+        if (tuple(out.shape) != (B, i.ny, i.nx, C) or out.dtype != torch.float32
+                or not out.is_cuda or out.stride(3) != 1 or ldo < C
+                or out.stride(1) != i.nx * ldo or out.stride(0) != i.ny * i.nx * ldo):
             raise BevpoolError(_binding.BEVPOOL_ERR_SHAPE_MISMATCH,
-                               "out must be a contiguous fp32 device tensor [B][ny][nx][C]")
+                               "out must be an fp32 device tensor [B][ny][nx][C] whose rows are "
+                               "evenly spaced (contiguous, or a channel slice of a wider map)")
         if stream is None:
             stream = torch.cuda.current_stream(cam_feat.device)
-        if events is None:
+        if reduce != "sum" or ldo != C:
+            if events is not None:
+                raise BevpoolError(_binding.BEVPOOL_ERR_INVALID_ARG,
+                                   "timing events go with a plain sum into a contiguous map")
+            bevpool_forward_ex(depth_prob.data_ptr(), cam_feat.data_ptr(), self.handle,
+                               out.data_ptr(), ldo, B, C, _dtype_code(cam_feat), _REDUCE[reduce],
+                               stream.cuda_stream)
+        elif events is None:
             bevpool_forward(depth_prob.data_ptr(), cam_feat.data_ptr(), self.handle,
                             out.data_ptr(), B, C, _dtype_code(cam_feat), stream.cuda_stream)
         else:
@@ -168,3 +190,48 @@ class Plan:
                          gf.data_ptr() if gf is not None else 0, B, C, _dtype_code(cam_feat),
                          stream.cuda_stream)
         return gd, gf
+
+
+class SlabPlan:
+    """Several z slabs flattened along z by concatenating their channels
+    (Sec. III-B, first paragraph: the pooled features are flattened along
+    the z-axis). Slab iz is [z_min + iz z_cell, z_min + (iz+1) z_cell) and
+    has a plan of its own; forward writes slab iz's C channels at channel
+    offset iz * C of one [B][ny][nx][nz * C] map (bevpool_forward_ex with
+    out_row_stride = nz * C), one call per slab."""
+
+    def __init__(self, intrinsics, extrinsics, geometry, nz: int, stream=None):
+        if nz < 1:
+            raise BevpoolError(_binding.BEVPOOL_ERR_INVALID_ARG, f"nz={nz} must be >= 1")
+        base = geometry_of(geometry)
+        self.nz = nz
+        self.plans = []
+        for iz in range(nz):
+            g = bevpool_geometry(*[getattr(base, f) for f in _GEOM_FIELDS])
+            g.z_min = base.z_min + iz * base.z_cell
+            self.plans.append(Plan(intrinsics, extrinsics, g, stream))
+
+    @classmethod
+    def from_rig(cls, rig, nz: int, stream=None) -> "SlabPlan":
+        return cls(rig.intrinsics, rig.extrinsics, rig, nz, stream)
+
+    def forward(self, depth_prob, cam_feat, out=None, stream=None, reduce="sum"):
+        """Returns fp32 [B][ny][nx][nz * C]: channel iz * C + c is channel c
+        of slab iz."""
+        torch = _torch()
+        i = self.plans[0].info
+        B, C = depth_prob.shape[0], cam_feat.shape[-1]
+        if out is None:
+            out = torch.empty((B, i.ny, i.nx, self.nz * C), dtype=torch.float32,
+                              device=cam_feat.device)
+        elif tuple(out.shape) != (B, i.ny, i.nx, self.nz * C) or not out.is_contiguous():
+            raise BevpoolError(_binding.BEVPOOL_ERR_SHAPE_MISMATCH,
+                               "out must be a contiguous fp32 tensor [B][ny][nx][nz * C]")
+        for iz, plan in enumerate(self.plans):
+            plan.forward(depth_prob, cam_feat, out=out[..., iz * C:(iz + 1) * C], stream=stream,
+                         reduce=reduce)
+        return out
+
+    def close(self) -> None:
+        for p in self.plans:
+            p.close()

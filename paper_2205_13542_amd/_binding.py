@@ -19,8 +19,10 @@ BEVPOOL_ERR_OOM = -5
 BEVPOOL_ERR_HIP = -6
 
 BEVPOOL_F32, BEVPOOL_BF16, BEVPOOL_F16 = 0, 1, 2
+BEVPOOL_SUM, BEVPOOL_MEAN, BEVPOOL_MAX = 0, 1, 2
 
-EXPORTED = ("bevpool_plan", "bevpool_forward", "bevpool_forward_timed", "bevpool_backward",
+EXPORTED = ("bevpool_plan", "bevpool_forward", "bevpool_forward_ex", "bevpool_forward_timed",
+            "bevpool_backward",
             "bevpool_plan_info_get",
             "bevpool_plan_export", "bevpool_plan_destroy", "bevpool_last_error",
             "bevpool_version")
@@ -77,6 +79,8 @@ def load(path: str = LIB_PATH):
     lib.bevpool_plan.restype = ctypes.c_int
     lib.bevpool_forward.argtypes = [vp, vp, vp, vp, i32, i32, i32, vp]
     lib.bevpool_forward.restype = ctypes.c_int
+    lib.bevpool_forward_ex.argtypes = [vp, vp, vp, vp, ctypes.c_int64, i32, i32, i32, i32, vp]
+    lib.bevpool_forward_ex.restype = ctypes.c_int
     lib.bevpool_forward_timed.argtypes = [vp, vp, vp, vp, i32, i32, i32, vp, vp, vp]
     lib.bevpool_forward_timed.restype = ctypes.c_int
     lib.bevpool_backward.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, vp]
@@ -129,6 +133,17 @@ def bevpool_forward(depth_prob: int, cam_feat: int, plan: int, bev_out: int,
     _check(load().bevpool_forward(ctypes.c_void_p(depth_prob), ctypes.c_void_p(cam_feat),
                                   ctypes.c_void_p(plan), ctypes.c_void_p(bev_out),
                                   batch, channels, dtype, ctypes.c_void_p(hip_stream)))
+
+
+def bevpool_forward_ex(depth_prob: int, cam_feat: int, plan: int, bev_out: int,
+                       out_row_stride: int, batch: int, channels: int, dtype: int, reduce: int,
+                       hip_stream: int = 0) -> None:
+    """bevpool_forward with an aggregation (BEVPOOL_SUM, _MEAN, _MAX) and an
+    output row stride in floats; device addresses as ints."""
+    _check(load().bevpool_forward_ex(ctypes.c_void_p(depth_prob), ctypes.c_void_p(cam_feat),
+                                     ctypes.c_void_p(plan), ctypes.c_void_p(bev_out),
+                                     out_row_stride, batch, channels, dtype, reduce,
+                                     ctypes.c_void_p(hip_stream)))
 
 
 def bevpool_forward_timed(depth_prob: int, cam_feat: int, plan: int, bev_out: int, batch: int,

@@ -61,7 +61,7 @@ extern "C" {
 
 const char *bevpool_last_error(void) { return g_last_error; }
 
-int32_t bevpool_version(void) { return 100; }  // 0.1.0
+int32_t bevpool_version(void) { return 200; }  // 0.2.0: bevpool_forward_ex
 
 int bevpool_plan(const double *intrinsics, const double *extrinsics, const bevpool_geometry *geom,
                  void *hip_stream, bevpool_plan_t **out_plan) {
@@ -116,8 +116,9 @@ int bevpool_plan(const double *intrinsics, const double *extrinsics, const bevpo
 
 namespace {
 int forward_checked(const void *depth_prob, const void *cam_feat, const bevpool_plan_t *plan,
-                    float *bev_out, int32_t batch, int32_t channels, int32_t dtype,
-                    void *hip_stream, void *start_event, void *stop_event) {
+                    float *bev_out, int64_t out_row_stride, int32_t batch, int32_t channels,
+                    int32_t dtype, int32_t reduce, void *hip_stream, void *start_event,
+                    void *stop_event) {
     if (!valid_plan(plan)) return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "invalid plan handle");
     if (!depth_prob || !cam_feat || !bev_out)
         return bevpool_fail(BEVPOOL_ERR_INVALID_ARG,
@@ -127,24 +128,36 @@ int forward_checked(const void *depth_prob, const void *cam_feat, const bevpool_
                             channels);
     if (dtype != BEVPOOL_F32 && dtype != BEVPOOL_BF16 && dtype != BEVPOOL_F16)
         return bevpool_fail(BEVPOOL_ERR_UNSUPPORTED_DTYPE, "dtype %d is not F32, BF16 or F16", dtype);
-    return bevpool_launch_forward(depth_prob, cam_feat, plan, bev_out, batch, channels, dtype,
-                                  hipStream_t(hip_stream), hipEvent_t(start_event),
-                                  hipEvent_t(stop_event));
+    if (reduce != BEVPOOL_SUM && reduce != BEVPOOL_MEAN && reduce != BEVPOOL_MAX)
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "reduce %d is not SUM, MEAN or MAX", reduce);
+    if (out_row_stride < channels)
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "out_row_stride=%lld is below channels=%d",
+                            (long long)out_row_stride, channels);
+    return bevpool_launch_forward(depth_prob, cam_feat, plan, bev_out, out_row_stride, batch,
+                                  channels, dtype, reduce, hipStream_t(hip_stream),
+                                  hipEvent_t(start_event), hipEvent_t(stop_event));
 }
 }  // namespace
 
 int bevpool_forward(const void *depth_prob, const void *cam_feat, const bevpool_plan_t *plan,
                     float *bev_out, int32_t batch, int32_t channels, int32_t dtype,
                     void *hip_stream) {
-    return forward_checked(depth_prob, cam_feat, plan, bev_out, batch, channels, dtype, hip_stream,
-                           nullptr, nullptr);
+    return forward_checked(depth_prob, cam_feat, plan, bev_out, channels, batch, channels, dtype,
+                           BEVPOOL_SUM, hip_stream, nullptr, nullptr);
+}
+
+int bevpool_forward_ex(const void *depth_prob, const void *cam_feat, const bevpool_plan_t *plan,
+                       float *bev_out, int64_t out_row_stride, int32_t batch, int32_t channels,
+                       int32_t dtype, int32_t reduce, void *hip_stream) {
+    return forward_checked(depth_prob, cam_feat, plan, bev_out, out_row_stride, batch, channels,
+                           dtype, reduce, hip_stream, nullptr, nullptr);
 }
 
 int bevpool_forward_timed(const void *depth_prob, const void *cam_feat, const bevpool_plan_t *plan,
                           float *bev_out, int32_t batch, int32_t channels, int32_t dtype,
                           void *hip_stream, void *start_event, void *stop_event) {
-    return forward_checked(depth_prob, cam_feat, plan, bev_out, batch, channels, dtype, hip_stream,
-                           start_event, stop_event);
+    return forward_checked(depth_prob, cam_feat, plan, bev_out, channels, batch, channels, dtype,
+                           BEVPOOL_SUM, hip_stream, start_event, stop_event);
 }
 
 int bevpool_backward(const float *grad_out, const void *depth_prob, const void *cam_feat,

@@ -42,6 +42,15 @@
 // end of its buffer: the hardware range check then returns 0 for a load and
 // drops a store, so the hot loops carry no branches for bounds or masks.
 //
+// The same kernels take the mean and the max (the "Interval Reduction"
+// paragraph names both besides the sum). Mean: sums as above, each final
+// value divided by its cell's point count where it is stored (a single
+// combo's count is its row range; other cells read the interval table).
+// Max (template flag MAXR): the FMAs become max(acc, p * f) from -inf, a
+// masked row carries a NaN probability that fmaxf ignores, and partial slots
+// are combined by max. Rows of the map are ldo floats apart (ldo >= C), so a
+// call can fill one channel block of a wider map, e.g. one z slab.
+//
 // Each output row gets its final value from one plain store (a borrowed row
 // holds a partial sum before it is zeroed), and every sum runs in an order
 // fixed by the plan, so results are deterministic. The per-row products are
@@ -64,9 +73,10 @@ namespace {
 struct ZeroArgs {
     float *out;
     const int32_t *empty_cells;
-    int32_t n_cells, C;
+    int32_t n_cells, ldo;               // output rows are ldo floats apart
     int32_t zero_begin, zero_end;
     int32_t zero_vec, zero_units;       // float4 units (or floats) per row
+    int32_t row_units;                  // the same units from one row to the next
     FastDiv div_units;
 };
 
@@ -78,6 +88,8 @@ struct FwdArgs {
     const int4 *gen_runs;
     int32_t N, D, H, W, HW;
     int32_t n_cells, C, slice_c;
+    int32_t ldo, mean;                  // output row stride (floats); divide sums by counts
+    const int32_t *cell_start;          // interval table: point counts of the cells
     uint32_t p_bytes, f_bytes, o_bytes, run_bytes;   // per frame (runs: whole table)
     int32_t items_d, items_w, n_items;
     int32_t n_heavy, n_light;
@@ -132,42 +144,62 @@ struct Stage {
 // acc[J] += pb[J] * f for the kColDepth depth bins of one row: pb holds the
 // row's probabilities of this lane group's column, read back from LDS as
 // broadcasts (a DPP broadcast operand would halve the FMA issue rate).
-template <int NCH>
+// With MAXR, acc[J] = max(acc[J], pb[J] * f) instead: a masked-off row
+// carries a NaN probability, and fmaxf ignores the NaN product.
+template <int NCH, bool MAXR>
 __device__ __forceinline__ void apply_row(float (&acc)[kColDepth][NCH], const float4 &lo,
                                           const float4 &hi, const Row<NCH> &f) {
     const float pb[kColDepth] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
 #pragma unroll
     for (int J = 0; J < kColDepth; ++J)
 #pragma unroll
-        for (int k = 0; k < NCH; ++k) acc[J][k] = __builtin_fmaf(pb[J], f.v[k], acc[J][k]);
+        for (int k = 0; k < NCH; ++k) {
+            if constexpr (MAXR)
+                acc[J][k] = fmaxf(acc[J][k], pb[J] * f.v[k]);
+            else
+                acc[J][k] = __builtin_fmaf(pb[J], f.v[k], acc[J][k]);
+        }
 }
 
 // After the row loop: each depth bin's sums go to the BEV row named by its
 // table entry: its single-combo cell, or the borrowed empty-cell row that
 // holds the partial sum of its combo. Lane J of the group holds the entry of
-// depth bin J.
+// depth bin J. For the mean, a single-combo cell's sum is divided by its
+// point count, the combo's row range; partial sums are divided later.
 template <int J, int NCH, bool VEC>
 struct Emit {
-    static __device__ __forceinline__ void run(const float (&acc)[kColDepth][NCH], int ex,
-                                               uint32_t dm, Rsrc out, uint32_t ch_off, int C,
-                                               bool tail_ok) {
+    static __device__ __forceinline__ void run(const float (&acc)[kColDepth][NCH], int ex, int ey,
+                                               uint32_t dm, Rsrc out, uint32_t ch_off, int ldo,
+                                               bool mean, bool tail_ok) {
         if (dm & (1u << J)) {
             const int x = row_bcast<J>(ex);
-            store_row<NCH, VEC>(out, x >= 0 ? uint32_t(x) * uint32_t(C) * 4u + ch_off : kOff, acc[J],
+            float v[NCH];
+#pragma unroll
+            for (int k = 0; k < NCH; ++k) v[k] = acc[J][k];
+            if (mean) {
+                const uint32_t y = uint32_t(row_bcast<J>(ey));
+                if (!(y & kComboMulti)) {
+                    const float cnt = float(int((y >> 16) & 0x3FFFu) - int(y & 0xFFFFu));
+#pragma unroll
+                    for (int k = 0; k < NCH; ++k) v[k] = v[k] / cnt;
+                }
+            }
+            store_row<NCH, VEC>(out, x >= 0 ? uint32_t(x) * uint32_t(ldo) * 4u + ch_off : kOff, v,
                            tail_ok);
         }
-        Emit<J + 1, NCH, VEC>::run(acc, ex, dm, out, ch_off, C, tail_ok);
+        Emit<J + 1, NCH, VEC>::run(acc, ex, ey, dm, out, ch_off, ldo, mean, tail_ok);
     }
 };
 template <int NCH, bool VEC>
 struct Emit<kColDepth, NCH, VEC> {
-    static __device__ __forceinline__ void run(const float (&)[kColDepth][NCH], int, uint32_t, Rsrc,
-                                               uint32_t, int, bool) {}
+    static __device__ __forceinline__ void run(const float (&)[kColDepth][NCH], int, int, uint32_t,
+                                               Rsrc, uint32_t, int, bool, bool) {}
 };
 
 // Zeroing workgroup zb of BS threads: the rows of BS listed empty cells of
 // frame b, from entry z.zero_begin + zb * BS on, written as one flat
-// sequence of 16-byte (or 4-byte) units: unit f is unit f % U of row f / U.
+// sequence of 16-byte (or 4-byte) units: unit f is unit f % U of row f / U
+// (a row's first U units; rows are row_units apart).
 // Rows of consecutive cells are adjacent in memory, so runs of empty cells
 // become contiguous stores. The cell ids are staged in LDS first, so no
 // store waits on a load.
@@ -179,17 +211,18 @@ __device__ void zero_rows(const ZeroArgs &z, int zb, int b, int *s_cell) {
     __syncthreads();
     const int U = z.zero_units;
     const int total = ne * U;
+    const int RU = z.row_units;
     if (z.zero_vec) {
-        float4 *o = reinterpret_cast<float4 *>(z.out + int64_t(b) * z.n_cells * z.C);
+        float4 *o = reinterpret_cast<float4 *>(z.out + int64_t(b) * z.n_cells * z.ldo);
         for (int f = threadIdx.x; f < total; f += BS) {
             const int r = int(fdiv(uint32_t(f), z.div_units));
-            o[int64_t(s_cell[r]) * U + (f - r * U)] = make_float4(0.f, 0.f, 0.f, 0.f);
+            o[int64_t(s_cell[r]) * RU + (f - r * U)] = make_float4(0.f, 0.f, 0.f, 0.f);
         }
     } else {
-        float *o = z.out + int64_t(b) * z.n_cells * z.C;
+        float *o = z.out + int64_t(b) * z.n_cells * z.ldo;
         for (int f = threadIdx.x; f < total; f += BS) {
             const int r = int(fdiv(uint32_t(f), z.div_units));
-            o[int64_t(s_cell[r]) * U + (f - r * U)] = 0.f;
+            o[int64_t(s_cell[r]) * RU + (f - r * U)] = 0.f;
         }
     }
 }
@@ -198,7 +231,7 @@ __device__ void zero_rows(const ZeroArgs &z, int zb, int b, int *s_cell) {
 template <int BS>
 int zero_blocks(const ZeroArgs &z) { return (z.zero_end - z.zero_begin + BS - 1) / BS; }
 
-template <int DT, int NCH, bool VEC>
+template <int DT, int NCH, bool VEC, bool MAXR>
 __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0, int cn,
                             float *s_pb) {
     constexpr uint32_t ES = Elem<DT>::kBytes;
@@ -255,7 +288,8 @@ __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0,
 #pragma unroll
     for (int q = 0; q < kColDepth; ++q)
 #pragma unroll
-        for (int k = 0; k < NCH; ++k) acc[q][k] = 0.f;
+        for (int k = 0; k < NCH; ++k) acc[q][k] = MAXR ? -INFINITY : 0.f;
+    const float masked = MAXR ? __builtin_nanf("") : 0.f;   // probability of a row outside the combo
 
     if (dm != 0) {
         // A ring of kStages stages of two rows: while one stage is applied,
@@ -271,28 +305,32 @@ __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0,
             for (int u = 0; u < kStages; ++u) {
                 const int hs = h + 2 * u;
                 const int hp = hs + hsel;
-                pq[j] = (hp >= hlo && hp < hhi) ? st[u].pv : 0.f;
+                pq[j] = (hp >= hlo && hp < hhi) ? st[u].pv : masked;
                 __builtin_amdgcn_wave_barrier();
                 const float4 r0a = *reinterpret_cast<const float4 *>(pq);
                 const float4 r0b = *reinterpret_cast<const float4 *>(pq + 4);
                 const float4 r1a = *reinterpret_cast<const float4 *>(pq + 8);
                 const float4 r1b = *reinterpret_cast<const float4 *>(pq + 12);
                 __builtin_amdgcn_wave_barrier();
-                apply_row<NCH>(acc, r0a, r0b, st[u].f0);
-                apply_row<NCH>(acc, r1a, r1b, st[u].f1);
+                apply_row<NCH, MAXR>(acc, r0a, r0b, st[u].f0);
+                apply_row<NCH, MAXR>(acc, r1a, r1b, st[u].f1);
                 load_stage(st[u], hs + 2 * kStages);
             }
         }
     }
 
-    Emit<0, NCH, VEC>::run(acc, e.x, dm, fr.O, uint32_t(c0) * 4u, a.C, tail_ok);
+    Emit<0, NCH, VEC>::run(acc, e.x, e.y, dm, fr.O, uint32_t(c0) * 4u, a.ldo, !MAXR && a.mean != 0,
+                           tail_ok);
 }
 
 // A generic cell's runs in chunks of 64: lane i loads run i of the chunk and
 // sums its depth probabilities; then the four lane groups take the runs
 // round-robin, four at a time, each run costing one feature row. A group's
-// runs are added in a fixed order.
-template <int DT, int NCH, bool VEC>
+// runs are added in a fixed order. With MAXR a run's points share one
+// feature row f, so their largest product per channel is f times the run's
+// largest probability where f >= 0 and f times its smallest otherwise; a
+// run past the chunk carries NaN probabilities, which fmaxf ignores.
+template <int DT, int NCH, bool VEC, bool MAXR>
 __device__ __forceinline__ void generic_runs(float (&acc)[NCH], const FwdArgs &a, const Frame &fr,
                                              int4 hdr, int c0, int first_chunk, int chunk_step) {
     constexpr uint32_t ES = Elem<DT>::kBytes;
@@ -304,15 +342,26 @@ __device__ __forceinline__ void generic_runs(float (&acc)[NCH], const FwdArgs &a
         const uint32_t roff = lane < nr ? uint32_t(hdr.y + ch * 64 + lane) * 16u : kOff;
         const auto rv = __builtin_amdgcn_raw_buffer_load_b128(runs, int(roff), 0, 0);
         const int p0 = int(rv[0]), pix = int(rv[1]), len = int(rv[2]);
-        float ps = 0.f;
-        for (int q = 0; q < len; ++q) ps += Elem<DT>::load(fr.P, uint32_t(p0 + q * a.HW) * ES);
+        float ps = 0.f, pmin = INFINITY;   // sum (max with MAXR) and min of the run's probabilities
+        if constexpr (MAXR) ps = -INFINITY;
+        for (int q = 0; q < len; ++q) {
+            const float pq = Elem<DT>::load(fr.P, uint32_t(p0 + q * a.HW) * ES);
+            if constexpr (MAXR) {
+                ps = fmaxf(ps, pq);
+                pmin = fminf(pmin, pq);
+            } else {
+                ps += pq;
+            }
+        }
         for (int i0 = 0; i0 < nr; i0 += 16) {
-            float pr[4];
+            float pr[4], pm[4];
             Row<NCH> f[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int i = i0 + 4 * u + grp;
                 pr[u] = __shfl(ps, i & 63);
+                pm[u] = __shfl(pmin, i & 63);
+                if (MAXR && i >= nr) pr[u] = pm[u] = __builtin_nanf("");
                 const int px = __shfl(pix, i & 63);
                 load_row<DT, NCH, VEC>(f[u], fr.F,
                                   i < nr ? (uint32_t(px) * uint32_t(a.C) + uint32_t(c0)) * ES : kOff);
@@ -320,31 +369,50 @@ __device__ __forceinline__ void generic_runs(float (&acc)[NCH], const FwdArgs &a
 #pragma unroll
             for (int u = 0; u < 4; ++u)
 #pragma unroll
-                for (int k = 0; k < NCH; ++k) acc[k] = __builtin_fmaf(pr[u], f[u].v[k], acc[k]);
+                for (int k = 0; k < NCH; ++k) {
+                    if constexpr (MAXR)
+                        acc[k] = fmaxf(acc[k], (f[u].v[k] >= 0.f ? pr[u] : pm[u]) * f[u].v[k]);
+                    else
+                        acc[k] = __builtin_fmaf(pr[u], f[u].v[k], acc[k]);
+                }
         }
     }
 }
 
-template <int DT, int NCH, bool VEC>
+// Mean: a generic cell's total divided by its point count.
+template <int NCH>
+__device__ __forceinline__ void divide_by_count(float (&v)[NCH], const FwdArgs &a, int cell) {
+    const float cnt = float(a.cell_start[cell + 1] - a.cell_start[cell]);
+#pragma unroll
+    for (int q = 0; q < NCH; ++q) v[q] = v[q] / cnt;
+}
+
+template <int DT, int NCH, bool VEC, bool MAXR>
 __device__ void light_generic(const FwdArgs &a, const Frame &fr, int k, int c0, int cn) {
     const int lane = threadIdx.x & 63;
     const int j = lane & 15, grp = lane >> 4;
     const int4 hdr = a.gen_hdr[a.n_heavy + k];
     float acc[NCH];
 #pragma unroll
-    for (int q = 0; q < NCH; ++q) acc[q] = 0.f;
-    generic_runs<DT, NCH, VEC>(acc, a, fr, hdr, c0, 0, 1);
+    for (int q = 0; q < NCH; ++q) acc[q] = MAXR ? -INFINITY : 0.f;
+    generic_runs<DT, NCH, VEC, MAXR>(acc, a, fr, hdr, c0, 0, 1);
     // (g0 + g1) + (g2 + g3), the same in every lane of the wave
 #pragma unroll
     for (int q = 0; q < NCH; ++q) {
-        const float s = acc[q] + __shfl_xor(acc[q], 16);
-        acc[q] = s + __shfl_xor(s, 32);
+        if constexpr (MAXR) {
+            const float s = fmaxf(acc[q], __shfl_xor(acc[q], 16));
+            acc[q] = fmaxf(s, __shfl_xor(s, 32));
+        } else {
+            const float s = acc[q] + __shfl_xor(acc[q], 16);
+            acc[q] = s + __shfl_xor(s, 32);
+        }
     }
-    store_row<NCH, VEC>(fr.O, grp == 0 ? (uint32_t(hdr.x) * uint32_t(a.C) + uint32_t(c0)) * 4u : kOff,
+    if (!MAXR && a.mean) divide_by_count<NCH>(acc, a, hdr.x);
+    store_row<NCH, VEC>(fr.O, grp == 0 ? (uint32_t(hdr.x) * uint32_t(a.ldo) + uint32_t(c0)) * 4u : kOff,
                    acc, j + 16 * (NCH - 1) < cn);
 }
 
-template <int DT, int NCH, bool VEC>
+template <int DT, int NCH, bool VEC, bool MAXR>
 __device__ void heavy_generic(const FwdArgs &a, const Frame &fr, int k, int c0, int cn,
                               float *s_part) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -354,24 +422,30 @@ __device__ void heavy_generic(const FwdArgs &a, const Frame &fr, int k, int c0, 
     const int4 hdr = a.gen_hdr[k];
     float acc[NCH];
 #pragma unroll
-    for (int q = 0; q < NCH; ++q) acc[q] = 0.f;
-    generic_runs<DT, NCH, VEC>(acc, a, fr, hdr, c0, wave, kFwdWaves);
+    for (int q = 0; q < NCH; ++q) acc[q] = MAXR ? -INFINITY : 0.f;
+    generic_runs<DT, NCH, VEC, MAXR>(acc, a, fr, hdr, c0, wave, kFwdWaves);
 #pragma unroll
     for (int q = 0; q < NCH; ++q) s_part[wl * SS + j + 16 * q] = acc[q];
     __syncthreads();
     if (wl == 0) {
         float sum[NCH];
 #pragma unroll
-        for (int q = 0; q < NCH; ++q) sum[q] = 0.f;
+        for (int q = 0; q < NCH; ++q) sum[q] = MAXR ? -INFINITY : 0.f;
         for (int g = 0; g < kColWidth; ++g)
 #pragma unroll
-            for (int q = 0; q < NCH; ++q) sum[q] += s_part[g * SS + j + 16 * q];
-        store_row<NCH, VEC>(fr.O, (uint32_t(hdr.x) * uint32_t(a.C) + uint32_t(c0)) * 4u, sum,
+            for (int q = 0; q < NCH; ++q) {
+                if constexpr (MAXR)
+                    sum[q] = fmaxf(sum[q], s_part[g * SS + j + 16 * q]);
+                else
+                    sum[q] += s_part[g * SS + j + 16 * q];
+            }
+        if (!MAXR && a.mean) divide_by_count<NCH>(sum, a, hdr.x);
+        store_row<NCH, VEC>(fr.O, (uint32_t(hdr.x) * uint32_t(a.ldo) + uint32_t(c0)) * 4u, sum,
                        j + 16 * (NCH - 1) < cn);
     }
 }
 
-template <int DT, int NCH, bool VEC>
+template <int DT, int NCH, bool VEC, bool MAXR>
 __global__ __launch_bounds__(kFwdBlock) void k_forward(FwdArgs a) {
     __shared__ float s_part[kColWidth * slot_stride<NCH>()];   // heavy cells: group partials
     __shared__ int s_cell[kFwdBlock];                          // zero rows: cell ids
@@ -380,18 +454,18 @@ __global__ __launch_bounds__(kFwdBlock) void k_forward(FwdArgs a) {
     const int c0 = blockIdx.z * a.slice_c;
     const int cn = min(a.slice_c, a.C - c0);
     if (bx < a.n_heavy) {
-        heavy_generic<DT, NCH, VEC>(a, Frame(a, b), bx, c0, cn, s_part);
+        heavy_generic<DT, NCH, VEC, MAXR>(a, Frame(a, b), bx, c0, cn, s_part);
     } else if (bx < a.base_col) {
         return;  // padding: column items start on a multiple of 8
     } else if (bx < a.base_col + a.n_items) {
-        column_item<DT, NCH, VEC>(a, Frame(a, b), xcd_remap(bx - a.base_col, a.n_items), c0, cn, s_pb);
+        column_item<DT, NCH, VEC, MAXR>(a, Frame(a, b), xcd_remap(bx - a.base_col, a.n_items), c0, cn, s_pb);
     } else if (bx < a.base_zero) {
         return;
     } else if (bx < a.base_light) {
         if (blockIdx.z == 0) zero_rows<kFwdBlock>(a.zero, bx - a.base_zero, b, s_cell);   // whole rows
     } else {
         const int k = (bx - a.base_light) * kFwdWaves + int(threadIdx.x >> 6);
-        if (k < a.n_light) light_generic<DT, NCH, VEC>(a, Frame(a, b), k, c0, cn);
+        if (k < a.n_light) light_generic<DT, NCH, VEC, MAXR>(a, Frame(a, b), k, c0, cn);
     }
 }
 
@@ -411,7 +485,8 @@ static_assert(kCombineInline <= 16, "inline rows come from one lane each of a 16
 struct CombineArgs {
     float *out;
     const int32_t *multi_begin, *multi_cell, *multi_rows, *empty_cells;
-    int32_t n_multi, C, n_zblocks;
+    const int32_t *cell_start;
+    int32_t n_multi, C, ldo, mean, n_zblocks;
     uint32_t o_bytes;
     ZeroArgs zero;
 };
@@ -436,6 +511,9 @@ struct SlotRows<kCombineInline> {
     static __device__ __forceinline__ void run(uint32_t *, int, int, int, uint32_t) {}
 };
 
+// With MAXR the slots' largest value is taken instead of their sum; for the
+// mean the sum is divided by the cell's point count.
+template <bool MAXR>
 __global__ __launch_bounds__(kBlock) void k_combine(CombineArgs a) {
     __shared__ int s_cell[kBlock];
     const int b = blockIdx.y;
@@ -452,15 +530,17 @@ __global__ __launch_bounds__(kBlock) void k_combine(CombineArgs a) {
     const int r_inline = a.multi_rows[int64_t(k) * kCombineInline + ji];
     const int s0 = a.multi_begin[k];
     const int n = a.multi_begin[k + 1] - s0;
-    const uint32_t row = uint32_t(a.C) * 4u;
-    const uint32_t obase = uint32_t(a.multi_cell[k]) * row;
+    const uint32_t row = uint32_t(a.ldo) * 4u;
+    const int cell = a.multi_cell[k];
+    const uint32_t obase = uint32_t(cell) * row;
+    const float cnt = (!MAXR && a.mean) ? float(a.cell_start[cell + 1] - a.cell_start[cell]) : 1.f;
     // every lane of the group runs every pass (the slot rows are exchanged
     // between its lanes); channels past C are masked
     for (int cb = 0; cb < a.C; cb += kCombineChunks * 16) {
         const int c = cb + j;
         float sum[kCombineChunks];
 #pragma unroll
-        for (int q = 0; q < kCombineChunks; ++q) sum[q] = 0.f;
+        for (int q = 0; q < kCombineChunks; ++q) sum[q] = MAXR ? -INFINITY : 0.f;
         // kCombineInline slots' loads in flight at a time, added in slot order
         for (int sl = 0; sl < n; sl += kCombineInline) {
             const int r = sl == 0 ? r_inline : (sl + ji < n ? a.empty_cells[s0 + sl + ji] : 0);
@@ -477,7 +557,7 @@ __global__ __launch_bounds__(kBlock) void k_combine(CombineArgs a) {
             for (int u = 0; u < kCombineInline; ++u)
 #pragma unroll
                 for (int q = 0; q < kCombineChunks; ++q)
-                    if (sl + u < n) sum[q] += v[u][q];
+                    if (sl + u < n) sum[q] = MAXR ? fmaxf(sum[q], v[u][q]) : sum[q] + v[u][q];
 #pragma unroll
             for (int u = 0; u < kCombineInline; ++u)
 #pragma unroll
@@ -486,24 +566,36 @@ __global__ __launch_bounds__(kBlock) void k_combine(CombineArgs a) {
         }
 #pragma unroll
         for (int q = 0; q < kCombineChunks; ++q)
-            store_f32(O, c + 16 * q < a.C ? obase + uint32_t(c + 16 * q) * 4u : kOff, sum[q]);
+            store_f32(O, c + 16 * q < a.C ? obase + uint32_t(c + 16 * q) * 4u : kOff,
+                      (!MAXR && a.mean) ? sum[q] / cnt : sum[q]);
     }
 }
 
 // Kernel-boundary events (either may be null): they take the timestamps of
 // the dispatch itself rather than of separate queue entries.
-template <int DT>
+template <int DT, bool MAXR>
 void launch_dtype(const FwdArgs &a, dim3 grid, int nch, bool vec, hipStream_t s, hipEvent_t e0,
                   hipEvent_t e1) {
+    const dim3 block(kFwdBlock);
     switch (nch) {
-        case 1: hipExtLaunchKernelGGL((k_forward<DT, 1, false>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a); break;
-        case 2: hipExtLaunchKernelGGL((k_forward<DT, 2, false>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a); break;
-        case 3: hipExtLaunchKernelGGL((k_forward<DT, 3, false>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a); break;
-        case 4: hipExtLaunchKernelGGL((k_forward<DT, 4, false>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a); break;
+        case 1: hipExtLaunchKernelGGL((k_forward<DT, 1, false, MAXR>), grid, block, 0, s, e0, e1, 0, a); break;
+        case 2: hipExtLaunchKernelGGL((k_forward<DT, 2, false, MAXR>), grid, block, 0, s, e0, e1, 0, a); break;
+        case 3: hipExtLaunchKernelGGL((k_forward<DT, 3, false, MAXR>), grid, block, 0, s, e0, e1, 0, a); break;
+        case 4: hipExtLaunchKernelGGL((k_forward<DT, 4, false, MAXR>), grid, block, 0, s, e0, e1, 0, a); break;
         default:
-            if (vec) hipExtLaunchKernelGGL((k_forward<DT, 5, true>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a);
-            else hipExtLaunchKernelGGL((k_forward<DT, 5, false>), grid, dim3(kFwdBlock), 0, s, e0, e1, 0, a);
+            if (vec) hipExtLaunchKernelGGL((k_forward<DT, 5, true, MAXR>), grid, block, 0, s, e0, e1, 0, a);
+            else hipExtLaunchKernelGGL((k_forward<DT, 5, false, MAXR>), grid, block, 0, s, e0, e1, 0, a);
             break;
+    }
+}
+
+template <bool MAXR>
+void launch_forward(const FwdArgs &a, int dtype, dim3 grid, int nch, bool vec, hipStream_t s,
+                    hipEvent_t e0, hipEvent_t e1) {
+    switch (dtype) {
+        case BEVPOOL_F32: launch_dtype<BEVPOOL_F32, MAXR>(a, grid, nch, vec, s, e0, e1); break;
+        case BEVPOOL_BF16: launch_dtype<BEVPOOL_BF16, MAXR>(a, grid, nch, vec, s, e0, e1); break;
+        default: launch_dtype<BEVPOOL_F16, MAXR>(a, grid, nch, vec, s, e0, e1); break;
     }
 }
 
@@ -518,21 +610,22 @@ constexpr int kZeroLate = 8;
 using namespace bevpool;
 
 int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *plan, float *out,
-                           int32_t batch, int32_t channels, int32_t dtype, hipStream_t stream,
-                           hipEvent_t start, hipEvent_t stop) {
+                           int64_t ldo, int32_t batch, int32_t channels, int32_t dtype,
+                           int32_t reduce, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
     const bevpool_geometry &g = plan->geom;
     const int64_t n_pix = int64_t(g.n_cams) * g.feat_h * g.feat_w;
     const int64_t esize = dtype == BEVPOOL_F32 ? 4 : 2;
     const int64_t p_bytes = plan->n_points * esize;
     const int64_t f_bytes = n_pix * channels * esize;
-    const int64_t o_bytes = int64_t(plan->n_cells) * channels * 4;
+    const int64_t o_bytes = int64_t(plan->n_cells) * ldo * 4;
     const int64_t run_bytes = int64_t(plan->n_runs) * 16;
     constexpr int64_t kLimit = int64_t(1) << 31;
     if (p_bytes >= kLimit || f_bytes >= kLimit || o_bytes >= kLimit || run_bytes >= kLimit)
         return bevpool_fail(BEVPOOL_ERR_OVERFLOW,
-                            "channels=%d: one frame's depth (%lld B), feature (%lld B) or BEV "
-                            "(%lld B) tensor reaches 2 GiB", channels, (long long)p_bytes,
-                            (long long)f_bytes, (long long)o_bytes);
+                            "channels=%d, row stride %lld: one frame's depth (%lld B), feature "
+                            "(%lld B) or BEV (%lld B) tensor reaches 2 GiB", channels,
+                            (long long)ldo, (long long)p_bytes, (long long)f_bytes,
+                            (long long)o_bytes);
     if (batch > 65535)
         return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "batch=%d exceeds 65535 frames per call", batch);
 
@@ -555,6 +648,9 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
     a.n_cells = plan->n_cells;
     a.C = channels;
     a.slice_c = slice_c;
+    a.ldo = int32_t(ldo);
+    a.mean = reduce == BEVPOOL_MEAN ? 1 : 0;
+    a.cell_start = plan->cell_start;
     a.p_bytes = uint32_t(p_bytes);
     a.f_bytes = uint32_t(f_bytes);
     a.o_bytes = uint32_t(o_bytes);
@@ -573,9 +669,10 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
     z.out = out;
     z.empty_cells = plan->empty_cells;
     z.n_cells = plan->n_cells;
-    z.C = channels;
-    z.zero_vec = (channels % 4 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0) ? 1 : 0;
+    z.ldo = int32_t(ldo);
+    z.zero_vec = (channels % 4 == 0 && ldo % 4 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0) ? 1 : 0;
     z.zero_units = z.zero_vec ? channels / 4 : channels;
+    z.row_units = z.zero_vec ? int32_t(ldo / 4) : int32_t(ldo);
     z.div_units = make_fastdiv(uint32_t(z.zero_units));
     const int n_free = plan->n_empty - plan->n_partials;
     const int n_late = combine ? int(int64_t(n_free) * kZeroLate / 8) : 0;
@@ -591,14 +688,12 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
     const dim3 grid(n_blocks, batch, n_slices);
     // 4-element lanes: every row slice of F (elements) and of the output
     // (fp32) starts on a 4-element boundary of an aligned buffer
-    const bool vec = nch == 5 && channels % 4 == 0 && slice_c % 4 == 0 &&
+    const bool vec = nch == 5 && channels % 4 == 0 && slice_c % 4 == 0 && ldo % 4 == 0 &&
                      reinterpret_cast<uintptr_t>(F) % (4 * esize) == 0 &&
                      reinterpret_cast<uintptr_t>(out) % 16 == 0;
-    switch (dtype) {
-        case BEVPOOL_F32: launch_dtype<BEVPOOL_F32>(a, grid, nch, vec, stream, start, combine ? nullptr : stop); break;
-        case BEVPOOL_BF16: launch_dtype<BEVPOOL_BF16>(a, grid, nch, vec, stream, start, combine ? nullptr : stop); break;
-        default: launch_dtype<BEVPOOL_F16>(a, grid, nch, vec, stream, start, combine ? nullptr : stop); break;
-    }
+    const bool maxr = reduce == BEVPOOL_MAX;
+    if (maxr) launch_forward<true>(a, dtype, grid, nch, vec, stream, start, combine ? nullptr : stop);
+    else launch_forward<false>(a, dtype, grid, nch, vec, stream, start, combine ? nullptr : stop);
     BEVPOOL_HIP(hipGetLastError());
     if (combine) {
         CombineArgs ca;
@@ -607,16 +702,20 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
         ca.multi_cell = plan->multi_cell;
         ca.multi_rows = plan->multi_rows;
         ca.empty_cells = plan->empty_cells;
+        ca.cell_start = plan->cell_start;
         ca.n_multi = plan->n_multi;
         ca.C = channels;
+        ca.ldo = int32_t(ldo);
+        ca.mean = a.mean;
         ca.o_bytes = uint32_t(o_bytes);
         ca.zero = z;
         ca.zero.zero_begin = plan->n_empty - n_late;
         ca.zero.zero_end = plan->n_empty;
         ca.n_zblocks = zero_blocks<kBlock>(ca.zero);
         const int n_cblocks = (plan->n_multi + kCombineGroups - 1) / kCombineGroups;
-        hipExtLaunchKernelGGL(k_combine, dim3(ca.n_zblocks + n_cblocks, batch),
-                              dim3(kBlock), 0, stream, nullptr, stop, 0, ca);
+        const dim3 cgrid(ca.n_zblocks + n_cblocks, batch);
+        if (maxr) hipExtLaunchKernelGGL(k_combine<true>, cgrid, dim3(kBlock), 0, stream, nullptr, stop, 0, ca);
+        else hipExtLaunchKernelGGL(k_combine<false>, cgrid, dim3(kBlock), 0, stream, nullptr, stop, 0, ca);
         BEVPOOL_HIP(hipGetLastError());
     }
     return BEVPOOL_OK;

@@ -113,6 +113,6 @@ int bevpool_launch_backward(const float *G, const void *P, const void *F,
                             const bevpool_plan_s *plan, float *dP, float *dF, int32_t batch,
                             int32_t channels, int32_t dtype, hipStream_t stream);
 int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *plan,
-                           float *out, int32_t batch, int32_t channels,
-                           int32_t dtype, hipStream_t stream, hipEvent_t start,
-                           hipEvent_t stop);
+                           float *out, int64_t ldo, int32_t batch, int32_t channels,
+                           int32_t dtype, int32_t reduce, hipStream_t stream,
+                           hipEvent_t start, hipEvent_t stop);

@@ -30,7 +30,7 @@ def _declared_functions():
 def test_header_declares_the_boundary():
     names = _declared_functions()
     assert {"bevpool_plan", "bevpool_forward", "bevpool_forward_timed"} <= set(names)
-    assert len(names) == 9
+    assert len(names) == 10
 
 
 def test_library_exports_every_declared_symbol(binding):
@@ -111,6 +111,10 @@ def test_forward_rejects_bad_handles_before_device_work(binding):
     assert lib.bevpool_plan_export(None, None, None, None) == -1
     lib.bevpool_plan_destroy(None)            # NULL-safe
     lib.bevpool_plan_destroy(ctypes.cast(fake, vp))   # bad magic: ignored
+    # forward_ex: bad handle
+    assert lib.bevpool_forward_ex(vp(1), vp(1), None, vp(1), 8, 1, 8, 0, 0, None) == -1
+    assert lib.bevpool_forward_ex(vp(1), vp(1), ctypes.cast(fake, vp), vp(1), 8, 1, 8, 0, 2,
+                                  None) == -1
     # backward: bad handle, and no output at all
     assert lib.bevpool_backward(vp(1), vp(1), vp(1), None, vp(1), vp(1), 1, 8, 0, None) == -1
     assert lib.bevpool_backward(vp(1), vp(1), vp(1), ctypes.cast(fake, vp), vp(1), vp(1), 1, 8, 0,

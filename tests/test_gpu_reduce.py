@@ -1,0 +1,237 @@
+"""Mean and max pooling, strided outputs and z slabs on the GPU (through the
+C ABI's bevpool_forward_ex) against the oracle, on the same seeded inputs.
+
+Bounds, per element:
+- max: equal in value to the oracle's max, which is exact in double and
+  rounded once to fp32. Both sides see the same products: a float times a
+  float (or a widened bf16/fp16 value) rounded once, and rounding is
+  monotonic, so the largest rounded product is the rounded largest product.
+- mean: |gpu - ref| <= 1e-4 / sqrt(n) + 1e-6 |ref| with n the cell's point
+  count: the sum's bound 1e-4 sqrt(n) divided by n, plus the rounding of the
+  division.
+- sum into a strided map: the forward's bound, 1e-4 sqrt(n).
+Cells without points are exactly 0 in every mode; floats of the map outside
+the written channels keep their previous contents.
+"""
+import dataclasses
+import sys
+
+import numpy as np
+import pytest
+
+import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+@pytest.fixture(scope="module")
+def pkg(torch_cuda):
+    import paper_2205_13542_amd as pkg
+    pkg._binding.load()
+    return pkg
+
+
+def _coarse(rig):
+    return dataclasses.replace(rig, nx=36, ny=36, cell_x=3.0, cell_y=3.0)
+
+
+RIGS = {
+    "tiny": wl.tiny_rig,
+    "nuscenes": wl.ring_rig,                                   # column items + combine
+    "nuscenes_tilted": lambda: wl.tilt_rig(wl.ring_rig()),     # generic cells, light and heavy
+    "coarse": lambda: _coarse(wl.ring_rig()),                  # many slots per cell
+    "coarse_tilted": lambda: _coarse(wl.tilt_rig(wl.ring_rig())),
+    "empty": lambda: dataclasses.replace(wl.tiny_rig(), x_min=100.0),
+}
+
+_TDT = {"f32": "float32", "bf16": "bfloat16", "f16": "float16"}
+
+
+def _inputs(torch, rig, C, seed, dtype="f32", batch=1):
+    P, F = wl.frames(rig, C, batch, "peaked", seed=seed, dtype=dtype)
+    dt = getattr(torch, _TDT[dtype])
+    Pd = torch.from_numpy(P).cuda().to(dt).contiguous()
+    Fd = torch.from_numpy(F).cuda().to(dt).contiguous()
+    # the values the GPU reads, widened exactly to fp32
+    return Pd, Fd, Pd.float().cpu().numpy(), Fd.float().cpu().numpy()
+
+
+def _counts(oracle_lib, rig, cop):
+    return np.bincount(cop[cop >= 0], minlength=rig.n_cells).reshape(rig.ny, rig.nx)
+
+
+def _check_reduce(got, ref, n, mode):
+    """got fp32 [B][ny][nx][C], ref float64, n int [ny][nx]."""
+    n4 = n[None, :, :, None]
+    if mode == "max":
+        assert np.array_equal(got, ref.astype(np.float32)), \
+            f"max: {np.sum(got != ref.astype(np.float32))} elements differ"
+    else:
+        bound = 1e-4 / np.sqrt(np.maximum(n4, 1)) + 1e-6 * np.abs(ref)
+        err = np.abs(got.astype(np.float64) - ref)
+        assert (err <= bound).all(), f"mean: max err/bound {(err / bound).max():.3g}"
+    assert (got[:, n == 0] == 0).all()
+
+
+@pytest.mark.parametrize("mode", ["mean", "max"])
+@pytest.mark.parametrize("name,C", [("tiny", 8), ("nuscenes", 80), ("nuscenes_tilted", 80),
+                                    ("coarse", 16), ("coarse_tilted", 16), ("empty", 8)])
+def test_reduce_matches_oracle(torch_cuda, pkg, oracle_lib, name, C, mode):
+    _say(f"[reduce] {name} C={C} {mode}")
+    torch = torch_cuda
+    rig = RIGS[name]()
+    Pd, Fd, Ph, Fh = _inputs(torch, rig, C, seed=11)
+    plan = pkg.Plan.from_rig(rig)
+    out = torch.full((1, rig.ny, rig.nx, C), float("nan"), device="cuda")
+    plan.forward(Pd, Fd, out=out, reduce=mode)
+    torch.cuda.synchronize()
+    cop = oracle_lib.cell_map(rig)
+    ref = oracle_lib.pool_reduce(rig, cop, Ph, Fh, mode)
+    _check_reduce(out.cpu().numpy(), ref, _counts(oracle_lib, rig, cop), mode)
+    plan.close()
+
+
+@pytest.mark.parametrize("mode", ["mean", "max"])
+@pytest.mark.parametrize("C", [1, 5, 17, 81, 160])
+def test_reduce_channel_counts(torch_cuda, pkg, oracle_lib, C, mode):
+    """Every lane-chunk count, and channel slices (81, 160)."""
+    _say(f"[reduce] nuscenes_tilted C={C} {mode}")
+    torch = torch_cuda
+    rig = RIGS["nuscenes_tilted"]()
+    Pd, Fd, Ph, Fh = _inputs(torch, rig, C, seed=C)
+    plan = pkg.Plan.from_rig(rig)
+    out = plan.forward(Pd, Fd, reduce=mode)
+    torch.cuda.synchronize()
+    cop = oracle_lib.cell_map(rig)
+    ref = oracle_lib.pool_reduce(rig, cop, Ph, Fh, mode)
+    _check_reduce(out.cpu().numpy(), ref, _counts(oracle_lib, rig, cop), mode)
+    plan.close()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_reduce_reduced_precision_batch(torch_cuda, pkg, oracle_lib, dtype):
+    """bf16 / fp16 inputs, two frames in one call, both modes."""
+    _say(f"[reduce] nuscenes {dtype} batch 2")
+    torch = torch_cuda
+    rig = RIGS["nuscenes"]()
+    Pd, Fd, Ph, Fh = _inputs(torch, rig, 80, seed=21, dtype=dtype, batch=2)
+    plan = pkg.Plan.from_rig(rig)
+    cop = oracle_lib.cell_map(rig)
+    n = _counts(oracle_lib, rig, cop)
+    for mode in ("mean", "max"):
+        out = plan.forward(Pd, Fd, reduce=mode)
+        torch.cuda.synchronize()
+        _check_reduce(out.cpu().numpy(), oracle_lib.pool_reduce(rig, cop, Ph, Fh, mode), n, mode)
+    plan.close()
+
+
+def test_reduce_deterministic_and_sum_unchanged(torch_cuda, pkg):
+    """Repeated mean/max calls are bitwise equal; reduce="sum" through
+    bevpool_forward_ex equals bevpool_forward bitwise."""
+    torch = torch_cuda
+    rig = RIGS["nuscenes_tilted"]()
+    Pd, Fd, _, _ = _inputs(torch, rig, 80, seed=31)
+    plan = pkg.Plan.from_rig(rig)
+    for mode in ("mean", "max"):
+        a = plan.forward(Pd, Fd, reduce=mode)
+        b = plan.forward(Pd, Fd, reduce=mode)
+        assert torch.equal(a, b)
+    s0 = plan.forward(Pd, Fd)
+    s1 = torch.empty_like(s0)
+    pkg.bevpool_forward_ex(Pd.data_ptr(), Fd.data_ptr(), plan.handle, s1.data_ptr(), 80, 1, 80,
+                           pkg.BEVPOOL_F32, pkg.BEVPOOL_SUM,
+                           torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert torch.equal(s0, s1)
+    plan.close()
+
+
+@pytest.mark.parametrize("name,C,ldo,off", [("nuscenes", 80, 96, 16), ("nuscenes", 80, 83, 3),
+                                            ("nuscenes_tilted", 80, 160, 80),
+                                            ("coarse", 16, 40, 24), ("nuscenes_tilted", 81, 90, 9)])
+def test_strided_output(torch_cuda, pkg, oracle_lib, name, C, ldo, off):
+    """Sum into channels [off, off + C) of rows ldo floats apart (aligned and
+    unaligned strides); the other floats of the map keep their sentinel."""
+    _say(f"[strided] {name} C={C} ldo={ldo} off={off}")
+    torch = torch_cuda
+    rig = RIGS[name]()
+    Pd, Fd, Ph, Fh = _inputs(torch, rig, C, seed=41, batch=2)
+    plan = pkg.Plan.from_rig(rig)
+    big = torch.full((2, rig.ny, rig.nx, ldo), -7.0, device="cuda")
+    plan.forward(Pd, Fd, out=big[..., off:off + C])
+    torch.cuda.synchronize()
+    got = big.cpu().numpy()
+    cop = oracle_lib.cell_map(rig)
+    _, ref = oracle_lib.pool(rig, cop, Ph, Fh, want_f64=True)
+    n = _counts(oracle_lib, rig, cop)[None, :, :, None]
+    err = np.abs(got[..., off:off + C].astype(np.float64) - ref)
+    assert (err <= 1e-4 * np.sqrt(np.maximum(n, 1))).all()
+    assert (got[..., :off] == -7.0).all() and (got[..., off + C:] == -7.0).all()
+    plan.close()
+
+
+@pytest.mark.parametrize("name", ["nuscenes", "nuscenes_tilted"])
+@pytest.mark.parametrize("mode", ["sum", "mean", "max"])
+def test_z_slabs(torch_cuda, pkg, oracle_lib, name, mode):
+    """Four 4 m slabs from z = -8 m, flattened by channel concatenation,
+    against the oracle's per-slab pooling."""
+    _say(f"[slabs] {name} {mode}")
+    torch = torch_cuda
+    rig = dataclasses.replace(RIGS[name](), z_min=-8.0, z_cell=4.0)
+    C, nz = 16, 4
+    Pd, Fd, Ph, Fh = _inputs(torch, rig, C, seed=51)
+    sp = pkg.SlabPlan.from_rig(rig, nz)
+    got = sp.forward(Pd, Fd, reduce=mode).cpu().numpy()
+    ref = oracle_lib.pool_slabs(rig, nz, Ph, Fh, mode)
+    for iz in range(nz):
+        r = oracle_lib.slab_rig(rig, iz)
+        cop = oracle_lib.cell_map(r)
+        n = _counts(oracle_lib, r, cop)
+        g = got[..., iz * C:(iz + 1) * C]
+        e = ref[..., iz * C:(iz + 1) * C]
+        if mode == "sum":
+            n4 = n[None, :, :, None]
+            assert (np.abs(g.astype(np.float64) - e) <= 1e-4 * np.sqrt(np.maximum(n4, 1))).all()
+            assert (g[:, n == 0] == 0).all()
+        else:
+            _check_reduce(g, e, n, mode)
+        assert n.sum() > 0
+    sp.close()
+
+
+def test_reduce_argument_errors(torch_cuda, pkg):
+    torch = torch_cuda
+    rig = RIGS["tiny"]()
+    Pd, Fd, _, _ = _inputs(torch, rig, 8, seed=61)
+    plan = pkg.Plan.from_rig(rig)
+    out = torch.empty((1, rig.ny, rig.nx, 8), device="cuda")
+    lib = pkg._binding.load()
+    import ctypes
+    vp = ctypes.c_void_p
+    s = torch.cuda.current_stream().cuda_stream
+    args = (vp(Pd.data_ptr()), vp(Fd.data_ptr()), vp(plan.handle), vp(out.data_ptr()))
+    assert lib.bevpool_forward_ex(*args, 7, 1, 8, 0, 0, vp(s)) == pkg._binding.BEVPOOL_ERR_INVALID_ARG
+    assert lib.bevpool_forward_ex(*args, 8, 1, 8, 0, 3, vp(s)) == pkg._binding.BEVPOOL_ERR_INVALID_ARG
+    assert lib.bevpool_forward_ex(*args, 8, 1, 8, 0, -1, vp(s)) == pkg._binding.BEVPOOL_ERR_INVALID_ARG
+    assert lib.bevpool_forward_ex(*args, 1 << 40, 1, 8, 0, 0, vp(s)) == pkg._binding.BEVPOOL_ERR_OVERFLOW
+    assert lib.bevpool_forward_ex(*args, 8, 1, 8, 0, 2, vp(s)) == 0
+    with pytest.raises(pkg.BevpoolError):
+        plan.forward(Pd, Fd, reduce="median")
+    with pytest.raises(pkg.BevpoolError):
+        plan.forward(Pd, Fd, reduce="max", events=(torch.cuda.Event(enable_timing=True),
+                                                   torch.cuda.Event(enable_timing=True)))
+    torch.cuda.synchronize()
+    plan.close()
