@@ -67,6 +67,8 @@ def parse_args():
                     help="aggregation (mean/max, and --slabs, are timed by reduce_bench)")
     ap.add_argument("--slabs", type=int, default=1,
                     help="z slabs of 4 m from z = -8 m, flattened by channel concatenation")
+    ap.add_argument("--nchw", action="store_true",
+                    help="time the channel-major copy of the pooled map (bevpool_to_nchw)")
     ap.add_argument("--backward", action="store_true",
                     help="time bevpool_backward (gradients of P and F) instead of the forward; "
                          "prints its own JSON line")
@@ -334,6 +336,59 @@ def reduce_bench(args):
     print(json.dumps(rec), flush=True)
 
 
+def nchw_bench(args):
+    """bevpool_to_nchw of the workload's pooled map, alone: [B][ny][nx][C]
+    rows to [B][C][ny][nx] planes, each call after a cache-evicting read,
+    timed by events around the call. Algorithmic bytes: the map read once
+    and written once."""
+    import numpy as np
+    import torch
+    import workloads as wl
+    import paper_2205_13542_amd as bp
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = wl.make(args.workload, seed=0)
+    stream = torch.cuda.current_stream(dev)
+    plan = bp.Plan.from_rig(w.rig, stream=stream)
+    bev = plan.forward(torch.from_numpy(w.P).to(dev), torch.from_numpy(w.F).to(dev), stream=stream)
+    out = torch.empty((w.batch, w.channels, w.rig.ny, w.rig.nx), dtype=torch.float32, device=dev)
+    flush = torch.zeros(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
+    flush_out = torch.zeros((), dtype=torch.float32, device=dev)
+    for _ in range(args.warmup):
+        torch.sum(flush, dim=0, out=flush_out)
+        bp.to_nchw(bev, out=out, stream=stream)
+    torch.cuda.synchronize()
+    ms = []
+    for _ in range(args.steps):
+        torch.sum(flush, dim=0, out=flush_out)
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0.record(stream)
+        bp.to_nchw(bev, out=out, stream=stream)
+        s1.record(stream)
+        torch.cuda.synchronize()
+        ms.append(s0.elapsed_time(s1))
+    ms = np.array(ms)
+    nbytes = 2 * bev.numel() * 4
+    mean_ms = float(ms.mean())
+    gbs = nbytes / (mean_ms * 1e-3) / 1e9
+    rec = {
+        "metric": "BEV map NHWC->NCHW copy ms + HBM GB/s, 1 GPU", "value": round(gbs, 2),
+        "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(mean_ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": WORKLOAD_TEXT[args.workload], "name": args.workload,
+                   "batch": w.batch, "map": [w.batch, w.rig.ny, w.rig.nx, w.channels]},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None},
+        "copy_us": {"mean": round(mean_ms * 1e3, 2), "median": round(float(np.median(ms)) * 1e3, 2),
+                    "min": round(float(ms.min()) * 1e3, 2)},
+        "algorithmic_bytes": nbytes,
+    }
+    plan.close()
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -346,6 +401,9 @@ def main():
         return
     if args.backward:
         backward_bench(args)
+        return
+    if args.nchw:
+        nchw_bench(args)
         return
     if args.reduce != "sum" or args.slabs != 1:
         reduce_bench(args)

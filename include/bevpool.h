@@ -220,6 +220,23 @@ BEVPOOL_API int bevpool_backward(const float *grad_out, const void *depth_prob,
                      float *grad_feat, int32_t batch, int32_t channels, int32_t dtype,
                      void *hip_stream);
 
+/*
+ * Channel-major copy of a BEV map, for a convolutional BEV encoder that reads
+ * [B][C][ny][nx] planes (Sec. III-C: the fused BEV features go through a
+ * convolutional encoder, and the fusion concatenates channel planes).
+ *  bev_nhwc:  device float, frame b's cell (iy, ix) row at
+ *             bev_nhwc + (b * ny * nx + iy * nx + ix) * in_row_stride;
+ *             channels [0, channels) of each row are read.
+ *  bev_nchw:  device float [batch][channels][ny][nx], overwritten.
+ * Needs no plan. Asynchronous on hip_stream; the buffers must not overlap.
+ * Errors: INVALID_ARG (null pointer, a size below 1, in_row_stride <
+ * channels, batch above 65535, more than 65535 tiles of 128 channels),
+ * OVERFLOW (in_row_stride or ny * nx reaches 2^31), HIP (launch failure).
+ */
+BEVPOOL_API int bevpool_to_nchw(const float *bev_nhwc, int64_t in_row_stride, float *bev_nchw,
+                    int32_t batch, int32_t ny, int32_t nx, int32_t channels,
+                    void *hip_stream);
+
 /* Sizes of a plan. All counts are per frame. */
 typedef struct {
     int64_t n_points;     /* N*D*H*W */

@@ -17,14 +17,15 @@ from . import _binding
 from ._binding import (BEVPOOL_BF16, BEVPOOL_F16, BEVPOOL_F32, BEVPOOL_MAX, BEVPOOL_MEAN,
                        BEVPOOL_SUM, BevpoolError,
                        bevpool_backward, bevpool_forward, bevpool_forward_ex,
-                       bevpool_forward_timed, bevpool_geometry,
+                       bevpool_forward_timed, bevpool_geometry, bevpool_to_nchw,
                        bevpool_last_error,
                        bevpool_plan, bevpool_plan_destroy, bevpool_plan_export,
                        bevpool_plan_info_get, bevpool_version)
 
 __all__ = [
     "Plan", "SlabPlan", "BevpoolError", "bevpool_plan", "bevpool_forward", "bevpool_forward_ex",
-    "bevpool_forward_timed", "bevpool_backward", "BEVPOOL_SUM", "BEVPOOL_MEAN", "BEVPOOL_MAX",
+    "bevpool_forward_timed", "bevpool_backward", "bevpool_to_nchw", "to_nchw",
+    "BEVPOOL_SUM", "BEVPOOL_MEAN", "BEVPOOL_MAX",
     "bevpool_plan_info_get",
     "bevpool_plan_export", "bevpool_plan_destroy", "bevpool_last_error", "bevpool_version",
     "bevpool_geometry", "geometry_of", "BEVPOOL_F32", "BEVPOOL_BF16", "BEVPOOL_F16",
@@ -53,6 +54,28 @@ def _dtype_code(t) -> int:
     if t.dtype not in codes:
         raise BevpoolError(_binding.BEVPOOL_ERR_UNSUPPORTED_DTYPE, f"dtype {t.dtype}")
     return codes[t.dtype]
+
+
+def to_nchw(bev, out=None, stream=None):
+    """fp32 device map [B][ny][nx][C] (contiguous, or a channel slice of a
+    wider map) -> [B][C][ny][nx] (bevpool_to_nchw)."""
+    torch = _torch()
+    if bev.dim() != 4 or bev.dtype != torch.float32 or not bev.is_cuda or bev.stride(3) != 1:
+        raise BevpoolError(_binding.BEVPOOL_ERR_INVALID_ARG,
+                           "bev must be an fp32 device tensor [B][ny][nx][C] with unit channel stride")
+    B, ny, nx, C = bev.shape
+    ldi = bev.stride(2)
+    if bev.stride(1) != nx * ldi or bev.stride(0) != ny * nx * ldi:
+        raise BevpoolError(_binding.BEVPOOL_ERR_INVALID_ARG, "rows of bev must be evenly spaced")
+    if out is None:
+        out = torch.empty((B, C, ny, nx), dtype=torch.float32, device=bev.device)
+    elif tuple(out.shape) != (B, C, ny, nx) or not out.is_contiguous() or out.dtype != torch.float32:
+        raise BevpoolError(_binding.BEVPOOL_ERR_SHAPE_MISMATCH,
+                           "out must be a contiguous fp32 tensor [B][C][ny][nx]")
+    if stream is None:
+        stream = torch.cuda.current_stream(bev.device)
+    bevpool_to_nchw(bev.data_ptr(), ldi, out.data_ptr(), B, ny, nx, C, stream.cuda_stream)
+    return out
 
 
 class Plan:

@@ -22,7 +22,7 @@ BEVPOOL_F32, BEVPOOL_BF16, BEVPOOL_F16 = 0, 1, 2
 BEVPOOL_SUM, BEVPOOL_MEAN, BEVPOOL_MAX = 0, 1, 2
 
 EXPORTED = ("bevpool_plan", "bevpool_forward", "bevpool_forward_ex", "bevpool_forward_timed",
-            "bevpool_backward",
+            "bevpool_backward", "bevpool_to_nchw",
             "bevpool_plan_info_get",
             "bevpool_plan_export", "bevpool_plan_destroy", "bevpool_last_error",
             "bevpool_version")
@@ -81,6 +81,8 @@ def load(path: str = LIB_PATH):
     lib.bevpool_forward.restype = ctypes.c_int
     lib.bevpool_forward_ex.argtypes = [vp, vp, vp, vp, ctypes.c_int64, i32, i32, i32, i32, vp]
     lib.bevpool_forward_ex.restype = ctypes.c_int
+    lib.bevpool_to_nchw.argtypes = [vp, ctypes.c_int64, vp, i32, i32, i32, i32, vp]
+    lib.bevpool_to_nchw.restype = ctypes.c_int
     lib.bevpool_forward_timed.argtypes = [vp, vp, vp, vp, i32, i32, i32, vp, vp, vp]
     lib.bevpool_forward_timed.restype = ctypes.c_int
     lib.bevpool_backward.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, vp]
@@ -144,6 +146,15 @@ def bevpool_forward_ex(depth_prob: int, cam_feat: int, plan: int, bev_out: int,
                                      ctypes.c_void_p(plan), ctypes.c_void_p(bev_out),
                                      out_row_stride, batch, channels, dtype, reduce,
                                      ctypes.c_void_p(hip_stream)))
+
+
+def bevpool_to_nchw(bev_nhwc: int, in_row_stride: int, bev_nchw: int, batch: int, ny: int,
+                    nx: int, channels: int, hip_stream: int = 0) -> None:
+    """Rows [B][ny*nx] (in_row_stride floats apart) to planes [B][C][ny][nx];
+    device addresses as ints."""
+    _check(load().bevpool_to_nchw(ctypes.c_void_p(bev_nhwc), in_row_stride,
+                                  ctypes.c_void_p(bev_nchw), batch, ny, nx, channels,
+                                  ctypes.c_void_p(hip_stream)))
 
 
 def bevpool_forward_timed(depth_prob: int, cam_feat: int, plan: int, bev_out: int, batch: int,

@@ -14,7 +14,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(HERE, "libbevpool.so")
-SOURCES = ["bevpool.hip", "plan.hip", "forward.hip", "backward.hip"]
+SOURCES = ["bevpool.hip", "plan.hip", "forward.hip", "backward.hip", "layout.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -178,6 +178,21 @@ int bevpool_backward(const float *grad_out, const void *depth_prob, const void *
                                    batch, channels, dtype, hipStream_t(hip_stream));
 }
 
+int bevpool_to_nchw(const float *bev_nhwc, int64_t in_row_stride, float *bev_nchw, int32_t batch,
+                    int32_t ny, int32_t nx, int32_t channels, void *hip_stream) {
+    if (!bev_nhwc || !bev_nchw)
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "bev_nhwc and bev_nchw must be non-NULL");
+    if (batch < 1 || ny < 1 || nx < 1 || channels < 1)
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG,
+                            "batch=%d, ny=%d, nx=%d and channels=%d must be >= 1", batch, ny, nx,
+                            channels);
+    if (in_row_stride < channels)
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "in_row_stride=%lld is below channels=%d",
+                            (long long)in_row_stride, channels);
+    return bevpool_launch_to_nchw(bev_nhwc, in_row_stride, bev_nchw, batch, ny, nx, channels,
+                                  hipStream_t(hip_stream));
+}
+
 int bevpool_plan_info_get(const bevpool_plan_t *plan, bevpool_plan_info *info) {
     if (!valid_plan(plan)) return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "invalid plan handle");
     if (!info) return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "info is NULL");

@@ -112,6 +112,8 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
 int bevpool_launch_backward(const float *G, const void *P, const void *F,
                             const bevpool_plan_s *plan, float *dP, float *dF, int32_t batch,
                             int32_t channels, int32_t dtype, hipStream_t stream);
+int bevpool_launch_to_nchw(const float *in, int64_t in_row_stride, float *out, int32_t batch,
+                           int32_t ny, int32_t nx, int32_t channels, hipStream_t stream);
 int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *plan,
                            float *out, int64_t ldo, int32_t batch, int32_t channels,
                            int32_t dtype, int32_t reduce, hipStream_t stream,
