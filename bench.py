@@ -67,6 +67,8 @@ def parse_args():
                     help="aggregation (mean/max, and --slabs, are timed by reduce_bench)")
     ap.add_argument("--slabs", type=int, default=1,
                     help="z slabs of 4 m from z = -8 m, flattened by channel concatenation")
+    ap.add_argument("--cumsum", action="store_true",
+                    help="time the prior-art prefix-sum pooling beside the forward (speed ratio)")
     ap.add_argument("--nchw", action="store_true",
                     help="time the channel-major copy of the pooled map (bevpool_to_nchw)")
     ap.add_argument("--backward", action="store_true",
@@ -336,6 +338,107 @@ def reduce_bench(args):
     print(json.dumps(rec), flush=True)
 
 
+def cumsum_trick_pool(P, F, sorted_point, cell_start, rig, C, inner_scan=False):
+    """The prior art the paper compares against (Sec. III-B, "Interval
+    Reduction"): lift every kept point in cell order into a K x C array,
+    take the prefix sum over all points, and subtract the prefix at each
+    cell's interval boundaries. Written with PyTorch tensor ops on the GPU,
+    as that implementation is; it reuses the plan's association (the sort
+    is not timed), so only the aggregation is compared. P [1][N][D][H][W],
+    F [1][N][H][W][C] fp32 device tensors; sorted_point, cell_start int64
+    device tensors. Returns fp32 [1][ny][nx][C]. inner_scan: run the prefix
+    sum along the innermost dimension of a transposed copy (PyTorch's
+    parallel scan) instead of along the points dimension as laid out."""
+    import torch
+    HW = rig.feat_h * rig.feat_w
+    DHW = rig.n_depth * HW
+    pix = (sorted_point // DHW) * HW + sorted_point % HW
+    x = P.reshape(-1)[sorted_point].unsqueeze(1) * F.reshape(-1, C)[pix]
+    if inner_scan:
+        prefix = torch.cumsum(x.t().contiguous(), dim=1).t()
+    else:
+        prefix = torch.cumsum(x, dim=0)
+    counts = cell_start[1:] - cell_start[:-1]
+    nonempty = torch.nonzero(counts > 0).squeeze(1)
+    ends = prefix[cell_start[1:][nonempty] - 1]
+    sums = torch.cat((ends[:1], ends[1:] - ends[:-1]))
+    out = torch.zeros((rig.n_cells, C), dtype=torch.float32, device=P.device)
+    out[nonempty] = sums
+    return out.view(1, rig.ny, rig.nx, C)
+
+
+def cumsum_bench(args):
+    """The prefix-sum pooling and the forward on the same frame (cold caches,
+    events around each call): the speed ratio the paper reports between the
+    two (500 ms -> 2 ms on its GPU) measured on MI355X."""
+    import numpy as np
+    import torch
+    import workloads as wl
+    import paper_2205_13542_amd as bp
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = wl.make(args.workload, seed=0)
+    assert w.batch == 1 and w.dtype == "f32"
+    stream = torch.cuda.current_stream(dev)
+    plan = bp.Plan.from_rig(w.rig, stream=stream)
+    _, sp, cs = plan.export()
+    spd = torch.from_numpy(sp.astype(np.int64)).to(dev)
+    csd = torch.from_numpy(cs.astype(np.int64)).to(dev)
+    P = torch.from_numpy(w.P).to(dev)
+    F = torch.from_numpy(w.F).to(dev)
+    flush = torch.zeros(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
+    flush_out = torch.zeros((), dtype=torch.float32, device=dev)
+
+    def timed(fn, steps):
+        ms = []
+        for _ in range(steps):
+            torch.sum(flush, dim=0, out=flush_out)
+            s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s0.record(stream)
+            fn()
+            s1.record(stream)
+            torch.cuda.synchronize()
+            ms.append(s0.elapsed_time(s1))
+        return np.array(ms)
+
+    run_cs = lambda: cumsum_trick_pool(P, F, spd, csd, w.rig, w.channels)
+    run_ci = lambda: cumsum_trick_pool(P, F, spd, csd, w.rig, w.channels, inner_scan=True)
+    run_fw = lambda: plan.forward(P, F, stream=stream)
+    timed(run_cs, args.warmup)
+    timed(run_ci, args.warmup)
+    timed(run_fw, args.warmup)
+    cs_ms = timed(run_cs, max(5, args.steps // 5))
+    ci_ms = timed(run_ci, args.steps)
+    fw_ms = timed(run_fw, args.steps)
+    a, ai, b = run_cs(), run_ci(), run_fw()
+    torch.cuda.synchronize()
+    diff = float((a - b).abs().max())
+    diff_i = float((ai - b).abs().max())
+    K = int(cs[-1])
+    rec = {
+        "metric": "BEV-pool aggregation: prefix-sum pooling vs interval forward, ms, 1 GPU",
+        "value": round(float(cs_ms.mean()) / float(fw_ms.mean()), 1), "unit": "x (speed ratio)",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(float(fw_ms.mean()), 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": WORKLOAD_TEXT[args.workload], "name": args.workload,
+                   "kept_points": K, "lifted_bytes": K * w.channels * 4},
+        "prefix_sum_ms": {"mean": round(float(cs_ms.mean()), 4),
+                          "median": round(float(np.median(cs_ms)), 4)},
+        "prefix_sum_inner_scan_ms": {"mean": round(float(ci_ms.mean()), 4),
+                                     "median": round(float(np.median(ci_ms)), 4),
+                                     "ratio_to_forward": round(float(ci_ms.mean()) / float(fw_ms.mean()), 1),
+                                     "max_abs_difference": diff_i},
+        "forward_ms": {"mean": round(float(fw_ms.mean()), 5),
+                       "median": round(float(np.median(fw_ms)), 5)},
+        "max_abs_difference": diff,
+        "paper": "500 ms -> 2 ms (250x) on an RTX 3090, Sec. III-B",
+    }
+    plan.close()
+    print(json.dumps(rec), flush=True)
+
+
 def nchw_bench(args):
     """bevpool_to_nchw of the workload's pooled map, alone: [B][ny][nx][C]
     rows to [B][C][ny][nx] planes, each call after a cache-evicting read,
@@ -404,6 +507,9 @@ def main():
         return
     if args.nchw:
         nchw_bench(args)
+        return
+    if args.cumsum:
+        cumsum_bench(args)
         return
     if args.reduce != "sum" or args.slabs != 1:
         reduce_bench(args)
