@@ -512,8 +512,11 @@ struct SlotRows<kCombineInline> {
 };
 
 // With MAXR the slots' largest value is taken instead of their sum; for the
-// mean the sum is divided by the cell's point count.
-template <bool MAXR>
+// mean the sum is divided by the cell's point count. With VEC (every
+// 80-channel pass of the row holds 65..80 channels, rows on 16-byte
+// boundaries) a lane moves channels 4j..4j+3 as one 16-byte access and
+// channel 64 + j as one 4-byte access; otherwise channels j + 16k.
+template <bool MAXR, bool VEC>
 __global__ __launch_bounds__(kBlock) void k_combine(CombineArgs a) {
     __shared__ int s_cell[kBlock];
     const int b = blockIdx.y;
@@ -537,37 +540,56 @@ __global__ __launch_bounds__(kBlock) void k_combine(CombineArgs a) {
     // every lane of the group runs every pass (the slot rows are exchanged
     // between its lanes); channels past C are masked
     for (int cb = 0; cb < a.C; cb += kCombineChunks * 16) {
-        const int c = cb + j;
-        float sum[kCombineChunks];
+        const int cn = min(kCombineChunks * 16, a.C - cb);
+        const uint32_t cboff = uint32_t(cb) * 4u;
+        Row<kCombineChunks> sum;
 #pragma unroll
-        for (int q = 0; q < kCombineChunks; ++q) sum[q] = MAXR ? -INFINITY : 0.f;
+        for (int q = 0; q < kCombineChunks; ++q) sum.v[q] = MAXR ? -INFINITY : 0.f;
         // kCombineInline slots' loads in flight at a time, added in slot order
         for (int sl = 0; sl < n; sl += kCombineInline) {
             const int r = sl == 0 ? r_inline : (sl + ji < n ? a.empty_cells[s0 + sl + ji] : 0);
             uint32_t rb[kCombineInline];
             SlotRows<0>::run(rb, r, sl, n, row);
-            float v[kCombineInline][kCombineChunks];
+            Row<kCombineChunks> v[kCombineInline];
+#pragma unroll
+            for (int u = 0; u < kCombineInline; ++u) {
+                if constexpr (VEC) {
+                    load_row<BEVPOOL_F32, kCombineChunks, true>(v[u], O, rb[u] + cboff);
+                } else {
+#pragma unroll
+                    for (int q = 0; q < kCombineChunks; ++q)
+                        v[u].v[q] = Elem<BEVPOOL_F32>::load(
+                            O, j + 16 * q < cn ? rb[u] + cboff + uint32_t(j + 16 * q) * 4u : kOff);
+                }
+            }
 #pragma unroll
             for (int u = 0; u < kCombineInline; ++u)
 #pragma unroll
                 for (int q = 0; q < kCombineChunks; ++q)
-                    v[u][q] = Elem<BEVPOOL_F32>::load(
-                        O, c + 16 * q < a.C ? rb[u] + uint32_t(c + 16 * q) * 4u : kOff);
+                    if (sl + u < n) sum.v[q] = MAXR ? fmaxf(sum.v[q], v[u].v[q]) : sum.v[q] + v[u].v[q];
+            const float zero[kCombineChunks] = {0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int u = 0; u < kCombineInline; ++u)
+            for (int u = 0; u < kCombineInline; ++u) {
+                if constexpr (VEC) {
+                    store_row<kCombineChunks, true>(O, rb[u] + cboff, zero, 64 + j < cn);
+                } else {
 #pragma unroll
-                for (int q = 0; q < kCombineChunks; ++q)
-                    if (sl + u < n) sum[q] = MAXR ? fmaxf(sum[q], v[u][q]) : sum[q] + v[u][q];
-#pragma unroll
-            for (int u = 0; u < kCombineInline; ++u)
-#pragma unroll
-                for (int q = 0; q < kCombineChunks; ++q)
-                    store_f32(O, c + 16 * q < a.C ? rb[u] + uint32_t(c + 16 * q) * 4u : kOff, 0.f);
+                    for (int q = 0; q < kCombineChunks; ++q)
+                        store_f32(O, j + 16 * q < cn ? rb[u] + cboff + uint32_t(j + 16 * q) * 4u : kOff, 0.f);
+                }
+            }
         }
+        if (!MAXR && a.mean) {
 #pragma unroll
-        for (int q = 0; q < kCombineChunks; ++q)
-            store_f32(O, c + 16 * q < a.C ? obase + uint32_t(c + 16 * q) * 4u : kOff,
-                      (!MAXR && a.mean) ? sum[q] / cnt : sum[q]);
+            for (int q = 0; q < kCombineChunks; ++q) sum.v[q] = sum.v[q] / cnt;
+        }
+        if constexpr (VEC) {
+            store_row<kCombineChunks, true>(O, obase + cboff, sum.v, 64 + j < cn);
+        } else {
+#pragma unroll
+            for (int q = 0; q < kCombineChunks; ++q)
+                store_f32(O, j + 16 * q < cn ? obase + cboff + uint32_t(j + 16 * q) * 4u : kOff, sum.v[q]);
+        }
     }
 }
 
@@ -714,8 +736,15 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
         ca.n_zblocks = zero_blocks<kBlock>(ca.zero);
         const int n_cblocks = (plan->n_multi + kCombineGroups - 1) / kCombineGroups;
         const dim3 cgrid(ca.n_zblocks + n_cblocks, batch);
-        if (maxr) hipExtLaunchKernelGGL(k_combine<true>, cgrid, dim3(kBlock), 0, stream, nullptr, stop, 0, ca);
-        else hipExtLaunchKernelGGL(k_combine<false>, cgrid, dim3(kBlock), 0, stream, nullptr, stop, 0, ca);
+        // 4-element lanes when every 80-channel pass holds 65..80 channels
+        // on 16-byte boundaries
+        const int tail = channels % (kCombineChunks * 16);
+        const bool cvec = channels % 4 == 0 && ldo % 4 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0 &&
+                          (tail == 0 || tail > 64);
+        if (maxr && cvec) hipExtLaunchKernelGGL((k_combine<true, true>), cgrid, dim3(kBlock), 0, stream, nullptr, stop, 0, ca);
+        else if (maxr) hipExtLaunchKernelGGL((k_combine<true, false>), cgrid, dim3(kBlock), 0, stream, nullptr, stop, 0, ca);
+        else if (cvec) hipExtLaunchKernelGGL((k_combine<false, true>), cgrid, dim3(kBlock), 0, stream, nullptr, stop, 0, ca);
+        else hipExtLaunchKernelGGL((k_combine<false, false>), cgrid, dim3(kBlock), 0, stream, nullptr, stop, 0, ca);
         BEVPOOL_HIP(hipGetLastError());
     }
     return BEVPOOL_OK;
