@@ -137,8 +137,11 @@ __global__ __launch_bounds__(kBBlock) void k_backward(BwdArgs a) {
     __shared__ float s_df[(kBWaves - 1) * kBCols * bwd_stride<NCH>()];
     constexpr uint32_t ES = Elem<DT>::kBytes;
     const int b = blockIdx.y;
-    const int rb = blockIdx.x % a.items_h;
-    const int t = blockIdx.x / a.items_h;
+    // the row blocks of one column block share its gradient rows: placed on
+    // one XCD, two at a time on one CU
+    const int item = xcd_cu_remap<2>(blockIdx.x, gridDim.x);
+    const int rb = item % a.items_h;
+    const int t = item / a.items_h;
     const int cb = t % a.items_w, n = t / a.items_w;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int j = lane & 15, grp = lane >> 4;

@@ -80,6 +80,25 @@ __device__ __forceinline__ float row_bcast(float v) {
     return __int_as_float(row_bcast<J>(__float_as_int(v)));
 }
 
+// Work order for a grid of G workgroups whose consecutive items share
+// data. Workgroups are dealt to the 8 XCDs round-robin (block b runs on XCD
+// b % 8), so item ranges are given to XCDs in contiguous eighths: adjacent
+// items meet in one L2. Within an XCD the dispatcher deals workgroups to
+// its 32 CUs in turn, so the XCD's workgroups k, k + 32, ... land on one CU
+// while every CU has room (measured on MI355X): the first ROUNDS * 32 of
+// them get ROUNDS consecutive items per CU, which then also meet in that
+// CU's L1. Placement only affects speed; the map is a permutation of
+// 0..G-1 for any G.
+constexpr int kCusPerXcd = 32;
+template <int ROUNDS>
+__device__ __forceinline__ int xcd_cu_remap(int b, int G) {
+    const int q = G >> 3, r = G & 7, x = b & 7, k0 = b >> 3;
+    constexpr int kSpan = ROUNDS * kCusPerXcd;
+    // a permutation of the XCD's first kSpan workgroups (it has >= q)
+    const int k = (q >= kSpan && k0 < kSpan) ? ROUNDS * (k0 % kCusPerXcd) + k0 / kCusPerXcd : k0;
+    return x < r ? x * (q + 1) + k : r * (q + 1) + (x - r) * q + k;
+}
+
 template <int NCH>
 struct Row {
     float v[NCH];

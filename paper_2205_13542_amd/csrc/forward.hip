@@ -114,23 +114,10 @@ template <int NCH>
 constexpr int slot_stride() { return 16 * NCH + ((NCH % 2 == 0) ? 16 : 0); }
 
 
-// Item order with consecutive depth blocks of one column block adjacent,
-// and adjacent items placed on the same XCD (workgroups are dealt to the 8
-// XCDs round-robin), so the feature rows they share meet in one L2. Within
-// an XCD the dispatcher deals workgroups to its 32 CUs in turn, so the
-// XCD's workgroups k, k + 32 and k + 64 land on one CU when every CU has
-// room (measured on MI355X): they get three consecutive items, whose
-// feature rows then also meet in that CU's L1. Placement only affects
-// speed; any placement gives the same result.
-constexpr int kCusPerXcd = 32;
+// Column items in (camera, column block, depth block) order are placed so
+// that consecutive depth blocks of one column block share an XCD's L2 and,
+// three at a time, a CU's L1 (xcd_cu_remap in device.h).
 constexpr int kCuRounds = 3;
-__device__ __forceinline__ int xcd_remap(int b, int G) {
-    const int q = G >> 3, r = G & 7, x = b & 7, k0 = b >> 3;
-    constexpr int kSpan = kCuRounds * kCusPerXcd;
-    // a permutation of the XCD's first kSpan workgroups (it has >= q)
-    const int k = (q >= kSpan && k0 < kSpan) ? kCuRounds * (k0 % kCusPerXcd) + k0 / kCusPerXcd : k0;
-    return x < r ? x * (q + 1) + k : r * (q + 1) + (x - r) * q + k;
-}
 
 
 // Two feature rows of a column and the lane's depth probability for them.
@@ -458,7 +445,8 @@ __global__ __launch_bounds__(kFwdBlock) void k_forward(FwdArgs a) {
     } else if (bx < a.base_col) {
         return;  // padding: column items start on a multiple of 8
     } else if (bx < a.base_col + a.n_items) {
-        column_item<DT, NCH, VEC, MAXR>(a, Frame(a, b), xcd_remap(bx - a.base_col, a.n_items), c0, cn, s_pb);
+        column_item<DT, NCH, VEC, MAXR>(a, Frame(a, b), xcd_cu_remap<kCuRounds>(bx - a.base_col, a.n_items),
+                                        c0, cn, s_pb);
     } else if (bx < a.base_zero) {
         return;
     } else if (bx < a.base_light) {
