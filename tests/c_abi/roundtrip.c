@@ -5,6 +5,10 @@
  *  - the plan's cell of every point equals the oracle's cell map exactly;
  *  - the pooled map is within 1e-4 * sqrt(points in the cell) of the
  *    oracle's fp64 sums, and empty cells are exactly 0;
+ *  - bevpool_forward_ex's max into channels [4, 4 + C) of rows C + 8 floats
+ *    apart equals the oracle's max rounded to float, and the other floats
+ *    of the map keep their contents;
+ *  - bevpool_to_nchw gives the planes of the summed map exactly;
  *  - bad arguments return the documented error codes with a message.
  * Exit status 0 when every check passes; the first failure is printed.
  */
@@ -32,6 +36,9 @@ int64_t oracle_cell_map(const double *intrinsics, const double *extrinsics,
 void oracle_pool(const float *P, const float *F, const int32_t *cell_of_point,
                  const oracle_geometry *g, int32_t batch, int32_t channels, float *out,
                  double *out64, double *abs64);
+void oracle_pool_reduce(const float *P, const float *F, const int32_t *cell_of_point,
+                        const oracle_geometry *g, int32_t batch, int32_t channels,
+                        int32_t mode, double *out64);
 
 #define FAIL(...)                          \
     do {                                   \
@@ -154,12 +161,58 @@ int main(void) {
         }
     }
 
+    /* max into a channel block of a wider map (sentinel 7.0 elsewhere) */
+    enum { LD = C + 8, OFF = 4 };
+    float *wide = malloc(sizeof(float) * B * n_cells * LD);
+    double *max64 = malloc(sizeof(double) * B * n_cells * C);
+    float *planes = malloc(sizeof(float) * B * n_cells * C);
+    if (!wide || !max64 || !planes) FAIL("host allocation");
+    void *dW, *dN;
+    HIP_OK(hipMalloc(&dW, sizeof(float) * B * n_cells * LD));
+    HIP_OK(hipMalloc(&dN, sizeof(float) * B * n_cells * C));
+    for (int64_t i = 0; i < B * n_cells * LD; ++i) wide[i] = 7.0f;
+    HIP_OK(hipMemcpy(dW, wide, sizeof(float) * B * n_cells * LD, hipMemcpyHostToDevice));
+    if (bevpool_forward_ex(dP, dF, plan, (float *)dW + OFF, LD, B, C, BEVPOOL_F32, BEVPOOL_MAX,
+                           stream) != BEVPOOL_OK)
+        FAIL("bevpool_forward_ex: %s", bevpool_last_error());
+    HIP_OK(hipStreamSynchronize(stream));
+    HIP_OK(hipMemcpy(wide, dW, sizeof(float) * B * n_cells * LD, hipMemcpyDeviceToHost));
+    oracle_pool_reduce(P, F, cop_ref, &og, B, C, 2, max64);
+    for (int64_t r = 0; r < B * n_cells; ++r) {
+        for (int k = 0; k < LD; ++k) {
+            const float v = wide[r * LD + k];
+            if (k < OFF || k >= OFF + C) {
+                if (v != 7.0f) FAIL("row %lld float %d outside the block changed to %.9g", (long long)r, k, v);
+            } else if (v != (float)max64[r * C + (k - OFF)]) {
+                FAIL("max row %lld channel %d: %.9g, oracle %.9g", (long long)r, k - OFF, v,
+                     max64[r * C + (k - OFF)]);
+            }
+        }
+    }
+
+    /* channel planes of the summed map: a copy, so exact */
+    if (bevpool_to_nchw((const float *)dO, C, (float *)dN, B, NY, NX, C, stream) != BEVPOOL_OK)
+        FAIL("bevpool_to_nchw: %s", bevpool_last_error());
+    HIP_OK(hipStreamSynchronize(stream));
+    HIP_OK(hipMemcpy(planes, dN, sizeof(float) * B * n_cells * C, hipMemcpyDeviceToHost));
+    for (int64_t b = 0; b < B; ++b)
+        for (int k = 0; k < C; ++k)
+            for (int64_t c = 0; c < n_cells; ++c)
+                if (planes[(b * C + k) * n_cells + c] != got[(b * n_cells + c) * C + k])
+                    FAIL("plane %d of frame %lld, cell %lld differs", k, (long long)b, (long long)c);
+
     /* documented errors */
     if (bevpool_forward(dP, dF, plan, (float *)dO, 0, C, BEVPOOL_F32, stream) != BEVPOOL_ERR_INVALID_ARG ||
         bevpool_last_error()[0] == '\0')
         FAIL("batch 0 must be INVALID_ARG with a message");
     if (bevpool_forward(dP, dF, plan, (float *)dO, B, C, 7, stream) != BEVPOOL_ERR_UNSUPPORTED_DTYPE)
         FAIL("dtype 7 must be UNSUPPORTED_DTYPE");
+    if (bevpool_forward_ex(dP, dF, plan, (float *)dO, C - 1, B, C, BEVPOOL_F32, BEVPOOL_SUM, stream) !=
+        BEVPOOL_ERR_INVALID_ARG)
+        FAIL("a row stride below the channel count must be INVALID_ARG");
+    if (bevpool_forward_ex(dP, dF, plan, (float *)dO, C, B, C, BEVPOOL_F32, 9, stream) !=
+        BEVPOOL_ERR_INVALID_ARG)
+        FAIL("reduce 9 must be INVALID_ARG");
     if (bevpool_forward(NULL, dF, plan, (float *)dO, B, C, BEVPOOL_F32, stream) != BEVPOOL_ERR_INVALID_ARG)
         FAIL("a null input must be INVALID_ARG");
     bevpool_plan_t *bad = NULL;
@@ -170,10 +223,12 @@ int main(void) {
     HIP_OK(hipFree(dP));
     HIP_OK(hipFree(dF));
     HIP_OK(hipFree(dO));
+    HIP_OK(hipFree(dW));
+    HIP_OK(hipFree(dN));
     HIP_OK(hipStreamDestroy(stream));
     printf("PASS: %lld kept points, %d non-empty cells, %d frames x %d channels\n",
            (long long)kept, info.n_nonempty, B, C);
     free(P); free(F); free(got); free(ref); free(ref64); free(abs64);
-    free(cop_lib); free(cop_ref); free(count);
+    free(cop_lib); free(cop_ref); free(count); free(wide); free(max64); free(planes);
     return 0;
 }
