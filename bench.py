@@ -646,6 +646,10 @@ def main():
         "plan_bytes_read": 8 * info.n_cams * info.n_depth * info.feat_w + 16 * info.n_generic
                            + 16 * info.n_runs + 4 * info.n_empty
                            + 4 * (info.n_multi * (10 + 8) + 1),
+        "frames_per_s": round(w.batch / (mean_ms * 1e-3), 1),
+        # a plan is built once per calibration; this many frames' forward
+        # time equals one rebuild
+        "plan_rebuild_in_frames": round(float(np.median(plan_ms[1:])) / (mean_ms / w.batch), 1),
         "plan_build_ms": round(plan_ms[0], 2),
         "plan": {"build_ms_first": round(plan_ms[0], 2),
                  "build_ms_median": round(float(np.median(plan_ms[1:])), 2),
