@@ -6,8 +6,9 @@
 // Kernels, in launch order:
 //   k_project      one thread per point: camera ray -> ego frame -> cell id
 //   k_radix_hist   } stable LSD radix sort of (cell, point id), 8-bit digits;
-//   k_scan         } input in id order, so ties stay in id order
-//   k_radix_scatter}
+//   k_scan...      } input in id order, so ties stay in id order (scans:
+//   k_radix_scatter} one workgroup for a short array, else chunk sums,
+//                    their scan and per-chunk scans from the offsets)
 //   k_cell_start   interval table from the sorted keys
 //   k_cell_stats   non-empty cells and the largest interval
 //   k_combo_walk ... k_generic_runs   work partition of the forward pass:
@@ -36,6 +37,7 @@ constexpr int kSortTile = kBlock * kSortItems;      // 2048 keys per workgroup
 constexpr int kWaveItems = kWaveSize * kSortItems;  // 512 keys per wave
 constexpr int kScanBlock = 1024;
 constexpr int kScanItems = 4;
+constexpr int kScanChunk = kScanBlock * kScanItems;  // elements per workgroup of a multi-block scan
 static_assert(kBlock == 256, "one radix digit per thread");
 
 struct ProjectArgs {
@@ -138,6 +140,41 @@ __global__ __launch_bounds__(kScanBlock) void k_scan(int32_t *data, int64_t n, i
         carry += blocksum;
     }
     if (threadIdx.x == 0) *total = carry;
+}
+
+// Multi-block exclusive scan, for arrays longer than one chunk: each
+// workgroup sums its chunk, one workgroup scans the chunk sums (k_scan),
+// and each workgroup scans its chunk again from its offset.
+__global__ __launch_bounds__(kScanBlock) void k_scan_sums(const int32_t *data, int64_t n,
+                                                          int32_t *sums) {
+    __shared__ int lds[kScanBlock / kWaveSize];
+    const int64_t i0 = int64_t(blockIdx.x) * kScanChunk + int64_t(threadIdx.x) * kScanItems;
+    int local = 0;
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k) local += (i0 + k < n) ? data[i0 + k] : 0;
+    int total;
+    (void)block_exclusive_scan<kScanBlock>(local, lds, &total);
+    if (threadIdx.x == 0) sums[blockIdx.x] = total;
+}
+
+__global__ __launch_bounds__(kScanBlock) void k_scan_apply(int32_t *data, int64_t n,
+                                                           const int32_t *offsets) {
+    __shared__ int lds[kScanBlock / kWaveSize];
+    const int64_t i0 = int64_t(blockIdx.x) * kScanChunk + int64_t(threadIdx.x) * kScanItems;
+    int v[kScanItems];
+    int local = 0;
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k) {
+        v[k] = (i0 + k < n) ? data[i0 + k] : 0;
+        local += v[k];
+    }
+    int total;
+    int run = offsets[blockIdx.x] + block_exclusive_scan<kScanBlock>(local, lds, &total);
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k) {
+        if (i0 + k < n) data[i0 + k] = run;
+        run += v[k];
+    }
 }
 
 // ---------------------------------------------------------------- radix sort
@@ -503,10 +540,20 @@ int dev_alloc(T **p, size_t count, const char *what) {
     return BEVPOOL_OK;
 }
 
-// Exclusive scan of data[0..n] in place; data[n] must be 0 on entry and
-// holds the total afterwards.
-void scan_with_total(int32_t *data, int64_t n, int32_t *scratch_total, hipStream_t stream) {
-    hipLaunchKernelGGL(k_scan, dim3(1), dim3(kScanBlock), 0, stream, data, n + 1, scratch_total);
+// Chunk sums a multi-block scan of n elements needs.
+int64_t scan_sums_needed(int64_t n) { return (n + kScanChunk - 1) / kScanChunk; }
+
+// Exclusive scan of data[0..n) in place; *total receives the sum. sums:
+// scratch of scan_sums_needed(n) ints (unused for a single chunk).
+void device_scan(int32_t *data, int64_t n, int32_t *total, int32_t *sums, hipStream_t stream) {
+    const int64_t nb = scan_sums_needed(n);
+    if (nb <= 1) {
+        hipLaunchKernelGGL(k_scan, dim3(1), dim3(kScanBlock), 0, stream, data, n, total);
+        return;
+    }
+    hipLaunchKernelGGL(k_scan_sums, dim3(uint32_t(nb)), dim3(kScanBlock), 0, stream, data, n, sums);
+    hipLaunchKernelGGL(k_scan, dim3(1), dim3(kScanBlock), 0, stream, sums, nb, total);
+    hipLaunchKernelGGL(k_scan_apply, dim3(uint32_t(nb)), dim3(kScanBlock), 0, stream, data, n, sums);
 }
 
 }  // namespace
@@ -537,13 +584,14 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
     double *d_calib = nullptr;
     uint32_t *keys_a = nullptr, *keys_b = nullptr;
     int32_t *vals_a = nullptr, *vals_b = nullptr, *hist = nullptr, *small = nullptr;
+    int32_t *scan_sums = nullptr;
     int32_t *flag_a = nullptr, *flag_b = nullptr;
     int32_t *combo_cell = nullptr, *combo_range = nullptr, *combo_flag = nullptr;
     int32_t *cell_generic = nullptr, *cell_ncombo = nullptr, *head_scan = nullptr;
     int32_t *run_scan = nullptr, *run_begin = nullptr, *pos_of_cell = nullptr;
     auto cleanup = [&]() {
         for (void *q : {(void *)d_calib, (void *)keys_a, (void *)keys_b, (void *)vals_a,
-                        (void *)vals_b, (void *)hist, (void *)small, (void *)flag_a,
+                        (void *)vals_b, (void *)hist, (void *)small, (void *)scan_sums, (void *)flag_a,
                         (void *)flag_b, (void *)combo_range,
                         (void *)combo_flag, (void *)cell_generic, (void *)cell_ncombo,
                         (void *)head_scan, (void *)run_scan, (void *)run_begin,
@@ -562,8 +610,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         for (int pass = 0; pass < passes; ++pass) {
             const int shift = 8 * pass;
             hipLaunchKernelGGL(k_radix_hist, dim3(tiles), dim3(kBlock), 0, stream, kin, n, shift, hist);
-            hipLaunchKernelGGL(k_scan, dim3(1), dim3(kScanBlock), 0, stream, hist,
-                               int64_t(tiles) * 256, small + 3);
+            device_scan(hist, int64_t(tiles) * 256, small + 3, scan_sums, stream);
             hipLaunchKernelGGL(k_radix_scatter, dim3(tiles), dim3(kBlock), 0, stream, kin, vin, n,
                                shift, hist, kout, vout);
             BEVPOOL_HIP(hipGetLastError());
@@ -600,6 +647,10 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         if ((rc2 = dev_alloc(&vals_b, size_t(sort_cap), "sort values"))) return rc2;
         if ((rc2 = dev_alloc(&hist, size_t(sort_tiles_cap) * 256, "radix histogram"))) return rc2;
         if ((rc2 = dev_alloc(&small, 8, "plan counters"))) return rc2;
+        // the longest scan is over sort_cap + 1 elements (radix histograms
+        // are shorter)
+        if ((rc2 = dev_alloc(&scan_sums, size_t(scan_sums_needed(sort_cap + 1)), "scan chunk sums")))
+            return rc2;
         if ((rc2 = dev_alloc(&flag_a, size_t(n_cells) + 1, "flags"))) return rc2;
         if ((rc2 = dev_alloc(&flag_b, size_t(n_cells) + 1, "flags"))) return rc2;
 
@@ -664,9 +715,9 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
                                plan->cell_start, n_cells, flag_a, flag_b, small + 4);
             hipLaunchKernelGGL(k_combo_table, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream,
                                ca, plan->column_table, combo_flag);
-            scan_with_total(flag_a, n_cells, small + 3, stream);       // generic cells
-            scan_with_total(flag_b, n_cells, small + 3, stream);       // empty cells
-            scan_with_total(combo_flag, n_combo, small + 3, stream);   // combos of multi cells
+            device_scan(flag_a, int64_t(n_cells) + 1, small + 3, scan_sums, stream);       // generic cells
+            device_scan(flag_b, int64_t(n_cells) + 1, small + 3, scan_sums, stream);       // empty cells
+            device_scan(combo_flag, n_combo + 1, small + 3, scan_sums, stream);   // combos of multi cells
             BEVPOOL_HIP(hipGetLastError());
             BEVPOOL_HIP(hipMemcpyAsync(stats, small, sizeof(stats), hipMemcpyDeviceToHost, stream));
             BEVPOOL_HIP(hipMemcpyAsync(counters, small + 4, sizeof(counters),
@@ -711,7 +762,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
                                keys_a, vals_a, n_part, plan->empty_cells, plan->column_table,
                                head_scan);
         }
-        scan_with_total(head_scan, n_part, small + 3, stream);
+        device_scan(head_scan, int64_t(n_part) + 1, small + 3, scan_sums, stream);
         BEVPOOL_HIP(hipGetLastError());
         int32_t n_multi;
         if ((rc2 = to_host(&n_multi, head_scan + n_part))) return rc2;
@@ -752,11 +803,11 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
             hipLaunchKernelGGL(k_run_flags, dim3(blocks_for(kept)), dim3(kBlock), 0, stream,
                                plan->sorted_point, kept, plan->cell_of_point, flag_a, HW, div_hw,
                                div_d, D, run_scan);
-        scan_with_total(run_scan, kept, small + 3, stream);
+        device_scan(run_scan, int64_t(kept) + 1, small + 3, scan_sums, stream);
         if (n_gen > 0)
             hipLaunchKernelGGL(k_generic_counts, dim3(blocks_for(n_gen)), dim3(kBlock), 0, stream,
                                gen_cell, n_gen, plan->cell_start, run_scan, run_begin, pos_of_cell);
-        scan_with_total(run_begin, n_gen, small + 3, stream);
+        device_scan(run_begin, int64_t(n_gen) + 1, small + 3, scan_sums, stream);
         if (n_gen > 0)
             hipLaunchKernelGGL(k_generic_hdr, dim3(blocks_for(n_gen)), dim3(kBlock), 0, stream,
                                gen_cell, n_gen, plan->cell_start, run_begin, plan->generic_hdr);
