@@ -23,7 +23,7 @@ from ._binding import (BEVPOOL_BF16, BEVPOOL_F16, BEVPOOL_F32, BEVPOOL_MAX, BEVP
                        bevpool_plan_info_get, bevpool_version)
 
 __all__ = [
-    "Plan", "SlabPlan", "BevpoolError", "bevpool_plan", "bevpool_forward", "bevpool_forward_ex",
+    "Plan", "SlabPlan", "bev_pool", "BevpoolError", "bevpool_plan", "bevpool_forward", "bevpool_forward_ex",
     "bevpool_forward_timed", "bevpool_backward", "bevpool_to_nchw", "to_nchw",
     "BEVPOOL_SUM", "BEVPOOL_MEAN", "BEVPOOL_MAX",
     "bevpool_plan_info_get",
@@ -258,3 +258,43 @@ class SlabPlan:
     def close(self) -> None:
         for p in self.plans:
             p.close()
+
+
+def _autograd_function():
+    torch = _torch()
+
+    class _BevPool(torch.autograd.Function):
+        """Sum pooling with its gradients (bevpool_forward, bevpool_backward)."""
+
+        @staticmethod
+        def forward(ctx, depth_prob, cam_feat, plan):
+            ctx.plan = plan
+            ctx.save_for_backward(depth_prob, cam_feat)
+            return plan.forward(depth_prob, cam_feat)
+
+        @staticmethod
+        def backward(ctx, grad_out):
+            depth_prob, cam_feat = ctx.saved_tensors
+            gd, gf = ctx.plan.backward(grad_out.contiguous(), depth_prob, cam_feat,
+                                       want_depth=ctx.needs_input_grad[0],
+                                       want_feat=ctx.needs_input_grad[1])
+            if gd is not None and gd.dtype != depth_prob.dtype:
+                gd = gd.to(depth_prob.dtype)
+            if gf is not None and gf.dtype != cam_feat.dtype:
+                gf = gf.to(cam_feat.dtype)
+            return gd, gf, None
+
+    return _BevPool
+
+
+_BEVPOOL_FN = None
+
+
+def bev_pool(depth_prob, cam_feat, plan):
+    """Differentiable sum pooling for training: the BEV map [B][ny][nx][C]
+    fp32 of ``plan.forward``, whose gradients with respect to depth_prob and
+    cam_feat come from ``plan.backward`` (returned in the inputs' dtypes)."""
+    global _BEVPOOL_FN
+    if _BEVPOOL_FN is None:
+        _BEVPOOL_FN = _autograd_function()
+    return _BEVPOOL_FN.apply(depth_prob, cam_feat, plan)

@@ -145,3 +145,27 @@ def test_backward_adjoint_on_gpu(torch_cuda, pkg):
     scale = float((d(G).abs() * d(out).abs()).sum())
     assert abs(lhs - via_p) <= 1e-5 * scale and abs(lhs - via_f) <= 1e-5 * scale
     plan.close()
+
+
+def test_autograd_function_matches_oracle(torch_cuda, pkg, oracle_lib):
+    """bev_pool under autograd: a scalar loss sum(out * G) gives the oracle's
+    gradients for G (and the same tensors as calling backward directly)."""
+    torch = torch_cuda
+    w = wl.make("nuscenes_tilted", seed=19)
+    plan = pkg.Plan.from_rig(w.rig)
+    P = torch.from_numpy(w.P).cuda().requires_grad_(True)
+    F = torch.from_numpy(w.F).cuda().requires_grad_(True)
+    G = torch.from_numpy(_grad(w, 29)).cuda()
+    out = pkg.bev_pool(P, F, plan)
+    (out * G).sum().backward()
+    torch.cuda.synchronize()
+    gd, gf = plan.backward(G, P.detach(), F.detach())
+    assert torch.equal(P.grad, gd) and torch.equal(F.grad, gf)
+    cop = oracle_lib.cell_map(w.rig)
+    refP, refF = oracle_lib.backward(w.rig, cop, w.P, w.F, _grad(w, 29))
+    assert (np.abs(P.grad.cpu().numpy().astype(np.float64) - refP) <= 1e-4 * np.sqrt(w.channels)).all()
+    k = (cop >= 0).reshape(w.rig.n_cams, w.rig.n_depth, -1).sum(axis=1).reshape(-1)
+    bound = 1e-4 * np.sqrt(np.maximum(k, 1))[None, :, None]
+    got = F.grad.cpu().numpy().reshape(w.batch, w.rig.n_pixels, w.channels)
+    assert (np.abs(got - refF.reshape(got.shape)) <= bound).all()
+    plan.close()
