@@ -272,6 +272,32 @@ def test_deterministic(torch_cuda, pkg):
     assert np.array_equal(a, b)
 
 
+def test_one_plan_on_two_streams(torch_cuda, pkg):
+    """The plan is read-only during a forward: two streams pool different
+    frames with it at once (each into its own map), several times over, and
+    every map equals the one pooled alone."""
+    torch = torch_cuda
+    w = wl.make("nuscenes", seed=12, batch=2)
+    plan = pkg.Plan.from_rig(w.rig)
+    P = _to_device(torch, w.P, "f32")
+    F = _to_device(torch, w.F, "f32")
+    ref = [plan.forward(P[b:b + 1].contiguous(), F[b:b + 1].contiguous()) for b in range(2)]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    ins = [(P[b:b + 1].contiguous(), F[b:b + 1].contiguous()) for b in range(2)]
+    torch.cuda.synchronize()
+    outs = [[], []]
+    for _ in range(4):
+        for b, s in enumerate(streams):
+            with torch.cuda.stream(s):
+                outs[b].append(plan.forward(*ins[b], stream=s))
+    torch.cuda.synchronize()
+    for b in range(2):
+        for o in outs[b]:
+            assert torch.equal(o, ref[b])
+    plan.close()
+
+
 def test_plan_reuse_and_shape_checks(torch_cuda, pkg):
     torch = torch_cuda
     rig = wl.tiny_rig()
