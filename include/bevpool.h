@@ -264,6 +264,21 @@ BEVPOOL_API int bevpool_plan_info_get(const bevpool_plan_t *plan, bevpool_plan_i
 BEVPOOL_API int bevpool_plan_export(const bevpool_plan_t *plan, int32_t *cell_of_point,
                         int32_t *sorted_point, int32_t *cell_start);
 
+/*
+ * A plan from a stored association, for callers that keep it (the
+ * "Precomputation" paragraph of Sec. III-B: the association depends only on
+ * the calibration, so it is computed once and reused). cell_of_point is
+ * host int32 [n_points] as bevpool_plan_export writes it: the cell of every
+ * point in point-id order, -1 for a dropped one. geom gives the sizes (the
+ * projection parameters are not used). The sort, the interval table and the
+ * work partition are rebuilt on the device; for a map exported from a plan
+ * with the same sizes the result equals that plan. Synchronises hip_stream.
+ * Errors: INVALID_ARG (null pointer, bad sizes, an entry outside
+ * [-1, nx*ny)), OVERFLOW, OOM, HIP.
+ */
+BEVPOOL_API int bevpool_plan_import(const int32_t *cell_of_point, const bevpool_geometry *geom,
+                        void *hip_stream, bevpool_plan_t **out_plan);
+
 /* Free a plan and its device memory. NULL-safe. The plan must not be in use
  * by work still queued on a stream. */
 BEVPOOL_API void bevpool_plan_destroy(bevpool_plan_t *plan);

@@ -20,6 +20,7 @@ from ._binding import (BEVPOOL_BF16, BEVPOOL_F16, BEVPOOL_F32, BEVPOOL_MAX, BEVP
                        bevpool_forward_timed, bevpool_geometry, bevpool_to_nchw,
                        bevpool_last_error,
                        bevpool_plan, bevpool_plan_destroy, bevpool_plan_export,
+                       bevpool_plan_import,
                        bevpool_plan_info_get, bevpool_version)
 
 __all__ = [
@@ -27,7 +28,7 @@ __all__ = [
     "bevpool_forward_timed", "bevpool_backward", "bevpool_to_nchw", "to_nchw",
     "BEVPOOL_SUM", "BEVPOOL_MEAN", "BEVPOOL_MAX",
     "bevpool_plan_info_get",
-    "bevpool_plan_export", "bevpool_plan_destroy", "bevpool_last_error", "bevpool_version",
+    "bevpool_plan_export", "bevpool_plan_import", "bevpool_plan_destroy", "bevpool_last_error", "bevpool_version",
     "bevpool_geometry", "geometry_of", "BEVPOOL_F32", "BEVPOOL_BF16", "BEVPOOL_F16",
 ]
 
@@ -100,6 +101,21 @@ class Plan:
     @classmethod
     def from_rig(cls, rig, stream=None) -> "Plan":
         return cls(rig.intrinsics, rig.extrinsics, rig, stream)
+
+    @classmethod
+    def from_cells(cls, cell_of_point, geometry, stream=None) -> "Plan":
+        """A plan from a stored association (bevpool_plan_import):
+        cell_of_point as ``export`` returns it, geometry with the
+        bevpool_geometry fields."""
+        torch = _torch()
+        _binding.load()
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        self = cls.__new__(cls)
+        self.geometry = geometry_of(geometry)
+        self.handle = bevpool_plan_import(cell_of_point, self.geometry, stream.cuda_stream)
+        self.info = bevpool_plan_info_get(self.handle)
+        return self
 
     def close(self) -> None:
         if getattr(self, "handle", None):

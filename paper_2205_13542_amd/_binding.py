@@ -22,7 +22,7 @@ BEVPOOL_F32, BEVPOOL_BF16, BEVPOOL_F16 = 0, 1, 2
 BEVPOOL_SUM, BEVPOOL_MEAN, BEVPOOL_MAX = 0, 1, 2
 
 EXPORTED = ("bevpool_plan", "bevpool_forward", "bevpool_forward_ex", "bevpool_forward_timed",
-            "bevpool_backward", "bevpool_to_nchw",
+            "bevpool_backward", "bevpool_to_nchw", "bevpool_plan_import",
             "bevpool_plan_info_get",
             "bevpool_plan_export", "bevpool_plan_destroy", "bevpool_last_error",
             "bevpool_version")
@@ -81,6 +81,9 @@ def load(path: str = LIB_PATH):
     lib.bevpool_forward.restype = ctypes.c_int
     lib.bevpool_forward_ex.argtypes = [vp, vp, vp, vp, ctypes.c_int64, i32, i32, i32, i32, vp]
     lib.bevpool_forward_ex.restype = ctypes.c_int
+    lib.bevpool_plan_import.argtypes = [vp, ctypes.POINTER(bevpool_geometry), vp,
+                                        ctypes.POINTER(ctypes.c_void_p)]
+    lib.bevpool_plan_import.restype = ctypes.c_int
     lib.bevpool_to_nchw.argtypes = [vp, ctypes.c_int64, vp, i32, i32, i32, i32, vp]
     lib.bevpool_to_nchw.restype = ctypes.c_int
     lib.bevpool_forward_timed.argtypes = [vp, vp, vp, vp, i32, i32, i32, vp, vp, vp]
@@ -126,6 +129,16 @@ def bevpool_plan(intrinsics, extrinsics, geom: bevpool_geometry, hip_stream: int
     _check(load().bevpool_plan(intr.ctypes.data_as(dp), extr.ctypes.data_as(dp),
                                ctypes.byref(geom), ctypes.c_void_p(hip_stream),
                                ctypes.byref(out)))
+    return int(out.value)
+
+
+def bevpool_plan_import(cell_of_point, geom: bevpool_geometry, hip_stream: int = 0) -> int:
+    """cell_of_point: host int32 array [n_points] (as exported)."""
+    import numpy as np
+    cop = np.ascontiguousarray(cell_of_point, dtype=np.int32)
+    out = ctypes.c_void_p()
+    _check(load().bevpool_plan_import(cop.ctypes.data_as(ctypes.c_void_p), ctypes.byref(geom),
+                                      ctypes.c_void_p(hip_stream), ctypes.byref(out)))
     return int(out.value)
 
 

@@ -63,14 +63,9 @@ const char *bevpool_last_error(void) { return g_last_error; }
 
 int32_t bevpool_version(void) { return 200; }  // 0.2.0: bevpool_forward_ex
 
-int bevpool_plan(const double *intrinsics, const double *extrinsics, const bevpool_geometry *geom,
-                 void *hip_stream, bevpool_plan_t **out_plan) {
-    g_last_error[0] = '\0';
-    if (!out_plan) return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "out_plan is NULL");
-    *out_plan = nullptr;
-    if (!intrinsics || !extrinsics || !geom)
-        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "intrinsics, extrinsics and geom must be non-NULL");
-    const bevpool_geometry &g = *geom;
+namespace {
+// Sizes and parameters of a geometry (both plan constructors).
+int check_geometry(const bevpool_geometry &g) {
     if (g.n_cams < 1 || g.feat_h < 1 || g.feat_w < 1 || g.n_depth < 1 || g.nx < 1 || g.ny < 1)
         return bevpool_fail(BEVPOOL_ERR_INVALID_ARG,
                             "sizes must be >= 1 (n_cams=%d feat_h=%d feat_w=%d n_depth=%d nx=%d ny=%d)",
@@ -89,12 +84,11 @@ int bevpool_plan(const double *intrinsics, const double *extrinsics, const bevpo
     if (int64_t(g.nx) * g.ny + 1 > int64_t(INT32_MAX))
         return bevpool_fail(BEVPOOL_ERR_OVERFLOW, "nx*ny = %lld cells exceeds int32",
                             (long long)(int64_t(g.nx) * g.ny));
-    if (!finite_all(intrinsics, size_t(4) * g.n_cams) || !finite_all(extrinsics, size_t(12) * g.n_cams))
-        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "calibration values must be finite");
-    for (int n = 0; n < g.n_cams; ++n)
-        if (intrinsics[4 * n] == 0.0 || intrinsics[4 * n + 1] == 0.0)
-            return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "camera %d has a zero focal length", n);
+    return BEVPOOL_OK;
+}
 
+int make_plan(const double *intrinsics, const double *extrinsics, const int32_t *host_cells,
+              const bevpool_geometry &g, void *hip_stream, bevpool_plan_t **out_plan) {
     bevpool_plan_s *plan = new (std::nothrow) bevpool_plan_s();
     if (!plan) return bevpool_fail(BEVPOOL_ERR_OOM, "host allocation of the plan failed");
     memset(plan, 0, sizeof(*plan));
@@ -105,13 +99,53 @@ int bevpool_plan(const double *intrinsics, const double *extrinsics, const bevpo
         delete plan;
         return bevpool_hip_fail(e, "hipGetDevice");
     }
-    const int rc = bevpool_build_plan(intrinsics, extrinsics, g, hipStream_t(hip_stream), plan);
+    const int rc = bevpool_build_plan(intrinsics, extrinsics, host_cells, g,
+                                      hipStream_t(hip_stream), plan);
     if (rc != BEVPOOL_OK) {
         free_plan(plan);
         return rc;
     }
     *out_plan = plan;
     return BEVPOOL_OK;
+}
+}  // namespace
+
+int bevpool_plan(const double *intrinsics, const double *extrinsics, const bevpool_geometry *geom,
+                 void *hip_stream, bevpool_plan_t **out_plan) {
+    g_last_error[0] = '\0';
+    if (!out_plan) return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "out_plan is NULL");
+    *out_plan = nullptr;
+    if (!intrinsics || !extrinsics || !geom)
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "intrinsics, extrinsics and geom must be non-NULL");
+    const bevpool_geometry &g = *geom;
+    int rc = check_geometry(g);
+    if (rc != BEVPOOL_OK) return rc;
+    if (!finite_all(intrinsics, size_t(4) * g.n_cams) || !finite_all(extrinsics, size_t(12) * g.n_cams))
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "calibration values must be finite");
+    for (int n = 0; n < g.n_cams; ++n)
+        if (intrinsics[4 * n] == 0.0 || intrinsics[4 * n + 1] == 0.0)
+            return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "camera %d has a zero focal length", n);
+    return make_plan(intrinsics, extrinsics, nullptr, g, hip_stream, out_plan);
+}
+
+int bevpool_plan_import(const int32_t *cell_of_point, const bevpool_geometry *geom,
+                        void *hip_stream, bevpool_plan_t **out_plan) {
+    g_last_error[0] = '\0';
+    if (!out_plan) return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "out_plan is NULL");
+    *out_plan = nullptr;
+    if (!cell_of_point || !geom)
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "cell_of_point and geom must be non-NULL");
+    const bevpool_geometry &g = *geom;
+    int rc = check_geometry(g);
+    if (rc != BEVPOOL_OK) return rc;
+    const int64_t np = int64_t(g.n_cams) * g.n_depth * g.feat_h * g.feat_w;
+    const int32_t n_cells = g.nx * g.ny;
+    for (int64_t p = 0; p < np; ++p)
+        if (cell_of_point[p] < -1 || cell_of_point[p] >= n_cells)
+            return bevpool_fail(BEVPOOL_ERR_INVALID_ARG,
+                                "cell_of_point[%lld] = %d is neither -1 nor a cell below %d",
+                                (long long)p, cell_of_point[p], n_cells);
+    return make_plan(nullptr, nullptr, cell_of_point, g, hip_stream, out_plan);
 }
 
 namespace {

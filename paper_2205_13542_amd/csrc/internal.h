@@ -106,9 +106,11 @@ int bevpool_hip_fail(hipError_t err, const char *what);
     } while (0)
 
 // Plan building (plan.hip) and the forward pass (forward.hip).
+// Plan building (plan.hip): from the calibration, or, when host_cells is
+// not null, from a stored cell map (validated by the caller).
 int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
-                       const bevpool_geometry &g, hipStream_t stream,
-                       bevpool_plan_s *plan);
+                       const int32_t *host_cells, const bevpool_geometry &g,
+                       hipStream_t stream, bevpool_plan_s *plan);
 int bevpool_launch_backward(const float *G, const void *P, const void *F,
                             const bevpool_plan_s *plan, float *dP, float *dF, int32_t batch,
                             int32_t channels, int32_t dtype, hipStream_t stream);

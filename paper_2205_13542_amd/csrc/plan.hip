@@ -88,6 +88,18 @@ __global__ __launch_bounds__(kBlock) void k_project(ProjectArgs a) {
     a.vals[p] = p;
 }
 
+// A stored association (bevpool_plan_import): the sort keys and point ids
+// from a cell map validated on the host.
+__global__ __launch_bounds__(kBlock) void k_keys_from_cells(const int32_t *cell_of_point,
+                                                            int32_t n_points, int32_t n_cells,
+                                                            uint32_t *keys, int32_t *vals) {
+    const int32_t p = blockIdx.x * kBlock + threadIdx.x;
+    if (p >= n_points) return;
+    const int32_t cell = cell_of_point[p];
+    keys[p] = cell >= 0 ? uint32_t(cell) : uint32_t(n_cells);
+    vals[p] = p;
+}
+
 // ---------------------------------------------------------------- scan
 
 // Exclusive scan of one value per thread across the block; *total gets the
@@ -562,7 +574,8 @@ void device_scan(int32_t *data, int64_t n, int32_t *total, int32_t *sums, hipStr
 using namespace bevpool;
 
 int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
-                       const bevpool_geometry &g, hipStream_t stream, bevpool_plan_s *plan) {
+                       const int32_t *host_cells, const bevpool_geometry &g, hipStream_t stream,
+                       bevpool_plan_s *plan) {
     const int64_t np64 = int64_t(g.n_cams) * g.n_depth * g.feat_h * g.feat_w;
     const int32_t np = int32_t(np64);
     const int32_t n_cells = g.nx * g.ny;
@@ -640,7 +653,8 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
 
     auto run = [&]() -> int {
         int rc2;
-        if ((rc2 = dev_alloc(&d_calib, size_t(g.n_cams) * 16, "calibration"))) return rc2;
+        if (!host_cells && (rc2 = dev_alloc(&d_calib, size_t(g.n_cams) * 16, "calibration")))
+            return rc2;
         if ((rc2 = dev_alloc(&keys_a, size_t(sort_cap), "sort keys"))) return rc2;
         if ((rc2 = dev_alloc(&keys_b, size_t(sort_cap), "sort keys"))) return rc2;
         if ((rc2 = dev_alloc(&vals_a, size_t(sort_cap), "sort values"))) return rc2;
@@ -654,27 +668,35 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         if ((rc2 = dev_alloc(&flag_a, size_t(n_cells) + 1, "flags"))) return rc2;
         if ((rc2 = dev_alloc(&flag_b, size_t(n_cells) + 1, "flags"))) return rc2;
 
-        BEVPOOL_HIP(hipMemcpyAsync(d_calib, intrinsics, sizeof(double) * 4 * g.n_cams,
-                                   hipMemcpyHostToDevice, stream));
-        BEVPOOL_HIP(hipMemcpyAsync(d_calib + 4 * g.n_cams, extrinsics,
-                                   sizeof(double) * 12 * g.n_cams, hipMemcpyHostToDevice, stream));
         fill(small, 8, 0);
+        if (host_cells) {
+            // a stored association: the cell map as exported, checked by the caller
+            BEVPOOL_HIP(hipMemcpyAsync(plan->cell_of_point, host_cells, sizeof(int32_t) * size_t(np),
+                                       hipMemcpyHostToDevice, stream));
+            hipLaunchKernelGGL(k_keys_from_cells, dim3(blocks_for(np)), dim3(kBlock), 0, stream,
+                               plan->cell_of_point, np, n_cells, keys_a, plan->sorted_point);
+        } else {
+            BEVPOOL_HIP(hipMemcpyAsync(d_calib, intrinsics, sizeof(double) * 4 * g.n_cams,
+                                       hipMemcpyHostToDevice, stream));
+            BEVPOOL_HIP(hipMemcpyAsync(d_calib + 4 * g.n_cams, extrinsics,
+                                       sizeof(double) * 12 * g.n_cams, hipMemcpyHostToDevice, stream));
 
-        // Sec. III-B, precomputation: cell of every point, then the points
-        // sorted by (cell, id) and the interval table.
-        ProjectArgs pa;
-        pa.intr = d_calib;
-        pa.extr = d_calib + 4 * g.n_cams;
-        pa.g = g;
-        pa.div_w = make_fastdiv(uint32_t(W));
-        pa.div_h = make_fastdiv(uint32_t(H));
-        pa.div_d = make_fastdiv(uint32_t(D));
-        pa.n_points = np;
-        pa.n_cells = n_cells;
-        pa.cell_of_point = plan->cell_of_point;
-        pa.keys = keys_a;
-        pa.vals = plan->sorted_point;
-        hipLaunchKernelGGL(k_project, dim3(blocks_for(np)), dim3(kBlock), 0, stream, pa);
+            // Sec. III-B, precomputation: cell of every point, then the points
+            // sorted by (cell, id) and the interval table.
+            ProjectArgs pa;
+            pa.intr = d_calib;
+            pa.extr = d_calib + 4 * g.n_cams;
+            pa.g = g;
+            pa.div_w = make_fastdiv(uint32_t(W));
+            pa.div_h = make_fastdiv(uint32_t(H));
+            pa.div_d = make_fastdiv(uint32_t(D));
+            pa.n_points = np;
+            pa.n_cells = n_cells;
+            pa.cell_of_point = plan->cell_of_point;
+            pa.keys = keys_a;
+            pa.vals = plan->sorted_point;
+            hipLaunchKernelGGL(k_project, dim3(blocks_for(np)), dim3(kBlock), 0, stream, pa);
+        }
         BEVPOOL_HIP(hipGetLastError());
         if ((rc2 = radix_sort(keys_a, plan->sorted_point, np, bits_for(n_cells)))) return rc2;
         hipLaunchKernelGGL(k_cell_start, dim3(blocks_for(int64_t(np) + 1)), dim3(kBlock), 0,

@@ -30,7 +30,7 @@ def _declared_functions():
 def test_header_declares_the_boundary():
     names = _declared_functions()
     assert {"bevpool_plan", "bevpool_forward", "bevpool_forward_timed"} <= set(names)
-    assert len(names) == 11
+    assert len(names) == 12
 
 
 def test_library_exports_every_declared_symbol(binding):
@@ -111,6 +111,21 @@ def test_forward_rejects_bad_handles_before_device_work(binding):
     assert lib.bevpool_plan_export(None, None, None, None) == -1
     lib.bevpool_plan_destroy(None)            # NULL-safe
     lib.bevpool_plan_destroy(ctypes.cast(fake, vp))   # bad magic: ignored
+    # plan import: null arguments, and a cell map entry outside [-1, nx*ny)
+    out = ctypes.c_void_p(123)
+    g, _ = _geom()
+    assert lib.bevpool_plan_import(None, ctypes.byref(g), None, ctypes.byref(out)) == -1
+    assert out.value is None
+    import numpy as np
+    n_points = g.n_cams * g.n_depth * g.feat_h * g.feat_w
+    cop = np.full(n_points, -1, dtype=np.int32)
+    cop[5] = g.nx * g.ny
+    assert lib.bevpool_plan_import(cop.ctypes.data_as(vp), ctypes.byref(g), None,
+                                   ctypes.byref(out)) == -1
+    assert b"cell_of_point[5]" in lib.bevpool_last_error()
+    cop[5] = -2
+    assert lib.bevpool_plan_import(cop.ctypes.data_as(vp), ctypes.byref(g), None,
+                                   ctypes.byref(out)) == -1
     # forward_ex: bad handle
     assert lib.bevpool_forward_ex(vp(1), vp(1), None, vp(1), 8, 1, 8, 0, 0, None) == -1
     assert lib.bevpool_forward_ex(vp(1), vp(1), ctypes.cast(fake, vp), vp(1), 8, 1, 8, 0, 2,

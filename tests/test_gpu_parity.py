@@ -272,6 +272,28 @@ def test_deterministic(torch_cuda, pkg):
     assert np.array_equal(a, b)
 
 
+@pytest.mark.parametrize("name", ["tiny", "nuscenes", "nuscenes_tilted", "coarse", "empty"])
+def test_plan_import_round_trip(torch_cuda, pkg, name):
+    """A plan rebuilt from its exported cell map (bevpool_plan_import) has
+    the same association, the same partition and the same pooled map, bit
+    for bit, as the plan built from the calibration."""
+    torch = torch_cuda
+    print(f"[import] {name}", flush=True)
+    rig = RIGS[name]()
+    a = pkg.Plan.from_rig(rig)
+    cop, sp, cs = a.export()
+    b = pkg.Plan.from_cells(cop, rig)
+    cop2, sp2, cs2 = b.export()
+    assert np.array_equal(cop, cop2) and np.array_equal(sp, sp2) and np.array_equal(cs, cs2)
+    for f, _ in pkg._binding.bevpool_plan_info._fields_:
+        assert getattr(a.info, f) == getattr(b.info, f), f
+    P, F = wl.frames(rig, 16, 1, "peaked", seed=4)
+    Pd, Fd = _to_device(torch, P, "f32"), _to_device(torch, F, "f32")
+    assert torch.equal(a.forward(Pd, Fd), b.forward(Pd, Fd))
+    a.close()
+    b.close()
+
+
 def test_one_plan_on_two_streams(torch_cuda, pkg):
     """The plan is read-only during a forward: two streams pool different
     frames with it at once (each into its own map), several times over, and
