@@ -9,6 +9,10 @@
  *    apart equals the oracle's max rounded to float, and the other floats
  *    of the map keep their contents;
  *  - bevpool_to_nchw gives the planes of the summed map exactly;
+ *  - bevpool_plan_import rebuilds the plan from the exported cell map, and
+ *    its pooled map equals the first plan's bit for bit;
+ *  - bevpool_backward's gradients are within 1e-4 sqrt(C) (dP) and
+ *    1e-4 sqrt(kept bins) (dF) of the oracle's;
  *  - bad arguments return the documented error codes with a message.
  * Exit status 0 when every check passes; the first failure is printed.
  */
@@ -39,6 +43,9 @@ void oracle_pool(const float *P, const float *F, const int32_t *cell_of_point,
 void oracle_pool_reduce(const float *P, const float *F, const int32_t *cell_of_point,
                         const oracle_geometry *g, int32_t batch, int32_t channels,
                         int32_t mode, double *out64);
+void oracle_backward(const float *P, const float *F, const float *G,
+                     const int32_t *cell_of_point, const oracle_geometry *g,
+                     int32_t batch, int32_t channels, double *dP64, double *dF64);
 
 #define FAIL(...)                          \
     do {                                   \
@@ -200,6 +207,60 @@ int main(void) {
             for (int64_t c = 0; c < n_cells; ++c)
                 if (planes[(b * C + k) * n_cells + c] != got[(b * n_cells + c) * C + k])
                     FAIL("plane %d of frame %lld, cell %lld differs", k, (long long)b, (long long)c);
+
+    /* the plan rebuilt from its exported cell map pools the same map */
+    bevpool_plan_t *imported = NULL;
+    if (bevpool_plan_import(cop_lib, &g, stream, &imported) != BEVPOOL_OK)
+        FAIL("bevpool_plan_import: %s", bevpool_last_error());
+    if (bevpool_forward(dP, dF, imported, (float *)dN, B, C, BEVPOOL_F32, stream) != BEVPOOL_OK)
+        FAIL("bevpool_forward on the imported plan: %s", bevpool_last_error());
+    HIP_OK(hipStreamSynchronize(stream));
+    HIP_OK(hipMemcpy(planes, dN, sizeof(float) * B * n_cells * C, hipMemcpyDeviceToHost));
+    if (memcmp(planes, got, sizeof(float) * B * n_cells * C) != 0)
+        FAIL("the imported plan pools a different map");
+    bevpool_plan_destroy(imported);
+
+    /* gradients against the oracle's, for G = 1 + 0.01 * element index mod 7 */
+    {
+        float *G = malloc(sizeof(float) * B * n_cells * C);
+        float *gdP = malloc(sizeof(float) * B * n_points);
+        float *gdF = malloc(sizeof(float) * B * n_pix * C);
+        double *rdP = malloc(sizeof(double) * B * n_points);
+        double *rdF = malloc(sizeof(double) * B * n_pix * C);
+        if (!G || !gdP || !gdF || !rdP || !rdF) FAIL("host allocation");
+        for (int64_t i = 0; i < B * n_cells * C; ++i) G[i] = 1.0f + 0.01f * (float)(i % 7);
+        void *dG, *ddP, *ddF;
+        HIP_OK(hipMalloc(&dG, sizeof(float) * B * n_cells * C));
+        HIP_OK(hipMalloc(&ddP, sizeof(float) * B * n_points));
+        HIP_OK(hipMalloc(&ddF, sizeof(float) * B * n_pix * C));
+        HIP_OK(hipMemcpy(dG, G, sizeof(float) * B * n_cells * C, hipMemcpyHostToDevice));
+        if (bevpool_backward((const float *)dG, dP, dF, plan, (float *)ddP, (float *)ddF, B, C,
+                             BEVPOOL_F32, stream) != BEVPOOL_OK)
+            FAIL("bevpool_backward: %s", bevpool_last_error());
+        HIP_OK(hipStreamSynchronize(stream));
+        HIP_OK(hipMemcpy(gdP, ddP, sizeof(float) * B * n_points, hipMemcpyDeviceToHost));
+        HIP_OK(hipMemcpy(gdF, ddF, sizeof(float) * B * n_pix * C, hipMemcpyDeviceToHost));
+        oracle_backward(P, F, G, cop_ref, &og, B, C, rdP, rdF);
+        for (int64_t i = 0; i < B * n_points; ++i)
+            if (!(fabs((double)gdP[i] - rdP[i]) <= 1e-4 * sqrt((double)C)))
+                FAIL("dP[%lld] = %.9g, oracle %.9g", (long long)i, gdP[i], rdP[i]);
+        for (int64_t b = 0; b < B; ++b)
+            for (int64_t pix = 0; pix < n_pix; ++pix) {
+                const int64_t n = pix / (H * W), hw = pix % (H * W);
+                int kept_bins = 0;
+                for (int d = 0; d < D; ++d) kept_bins += cop_ref[(n * D + d) * H * W + hw] >= 0;
+                const double bound = 1e-4 * sqrt(kept_bins > 1 ? (double)kept_bins : 1.0);
+                for (int k = 0; k < C; ++k) {
+                    const int64_t i = (b * n_pix + pix) * C + k;
+                    if (!(fabs((double)gdF[i] - rdF[i]) <= bound))
+                        FAIL("dF[%lld] = %.9g, oracle %.9g", (long long)i, gdF[i], rdF[i]);
+                }
+            }
+        HIP_OK(hipFree(dG));
+        HIP_OK(hipFree(ddP));
+        HIP_OK(hipFree(ddF));
+        free(G); free(gdP); free(gdF); free(rdP); free(rdF);
+    }
 
     /* documented errors */
     if (bevpool_forward(dP, dF, plan, (float *)dO, 0, C, BEVPOOL_F32, stream) != BEVPOOL_ERR_INVALID_ARG ||
