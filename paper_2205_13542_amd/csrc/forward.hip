@@ -591,7 +591,10 @@ void launch_dtype(const FwdArgs &a, dim3 grid, int nch, bool vec, hipStream_t s,
         case 1: hipExtLaunchKernelGGL((k_forward<DT, 1, false, MAXR>), grid, block, 0, s, e0, e1, 0, a); break;
         case 2: hipExtLaunchKernelGGL((k_forward<DT, 2, false, MAXR>), grid, block, 0, s, e0, e1, 0, a); break;
         case 3: hipExtLaunchKernelGGL((k_forward<DT, 3, false, MAXR>), grid, block, 0, s, e0, e1, 0, a); break;
-        case 4: hipExtLaunchKernelGGL((k_forward<DT, 4, false, MAXR>), grid, block, 0, s, e0, e1, 0, a); break;
+        case 4:
+            if (vec) hipExtLaunchKernelGGL((k_forward<DT, 4, true, MAXR>), grid, block, 0, s, e0, e1, 0, a);
+            else hipExtLaunchKernelGGL((k_forward<DT, 4, false, MAXR>), grid, block, 0, s, e0, e1, 0, a);
+            break;
         default:
             if (vec) hipExtLaunchKernelGGL((k_forward<DT, 5, true, MAXR>), grid, block, 0, s, e0, e1, 0, a);
             else hipExtLaunchKernelGGL((k_forward<DT, 5, false, MAXR>), grid, block, 0, s, e0, e1, 0, a);
@@ -698,9 +701,11 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
     const dim3 grid(n_blocks, batch, n_slices);
     // 4-element lanes: every row slice of F (elements) and of the output
     // (fp32) starts on a 4-element boundary of an aligned buffer
-    const bool vec = nch == 5 && channels % 4 == 0 && slice_c % 4 == 0 && ldo % 4 == 0 &&
-                     reinterpret_cast<uintptr_t>(F) % (4 * esize) == 0 &&
-                     reinterpret_cast<uintptr_t>(out) % 16 == 0;
+    // (slices of 65..80 channels, or exactly 64)
+    const bool aligned = ldo % 4 == 0 && reinterpret_cast<uintptr_t>(F) % (4 * esize) == 0 &&
+                         reinterpret_cast<uintptr_t>(out) % 16 == 0;
+    const bool vec = aligned && ((nch == 5 && channels % 4 == 0 && slice_c % 4 == 0) ||
+                                 (nch == 4 && slice_c == 64 && channels % 64 == 0));
     const bool maxr = reduce == BEVPOOL_MAX;
     if (maxr) launch_forward<true>(a, dtype, grid, nch, vec, stream, start, combine ? nullptr : stop);
     else launch_forward<false>(a, dtype, grid, nch, vec, stream, start, combine ? nullptr : stop);

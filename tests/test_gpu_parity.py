@@ -211,7 +211,7 @@ def test_forward_edge_rigs(torch_cuda, pkg, oracle_lib, oracle_plans, name):
 
 
 @pytest.mark.parametrize("rig_name", ["nuscenes", "nuscenes_tilted"])
-@pytest.mark.parametrize("channels", [1, 3, 5, 12, 17, 33, 64, 72, 81, 160, 260])
+@pytest.mark.parametrize("channels", [1, 3, 5, 12, 17, 33, 64, 72, 81, 128, 160, 192, 260])
 def test_forward_channel_counts(torch_cuda, pkg, oracle_lib, oracle_plans, channels, rig_name):
     """Every lane-chunk count (1..5 channels per lane of a 16-lane group),
     ragged last chunks, rows split into channel slices (81, 160, 260), and

@@ -105,9 +105,10 @@ def test_reduce_matches_oracle(torch_cuda, pkg, oracle_lib, name, C, mode):
 
 
 @pytest.mark.parametrize("mode", ["mean", "max"])
-@pytest.mark.parametrize("C", [1, 5, 17, 81, 160])
+@pytest.mark.parametrize("C", [1, 5, 17, 64, 81, 128, 160])
 def test_reduce_channel_counts(torch_cuda, pkg, oracle_lib, C, mode):
-    """Every lane-chunk count, and channel slices (81, 160)."""
+    """Every lane-chunk count, channel slices (81, 128, 160), and 64-channel
+    slices moved as 16-byte lanes (64, 128)."""
     _say(f"[reduce] nuscenes_tilted C={C} {mode}")
     torch = torch_cuda
     rig = RIGS["nuscenes_tilted"]()
