@@ -60,6 +60,23 @@ def _anisotropic_rig():
                                extrinsics=base.extrinsics[[1, 4]].copy())
 
 
+def _odd_rig(tilt: bool):
+    """Three cameras of the ring with odd sizes everywhere (13 rows, 27
+    columns, 37 depth bins, a 151 x 149 grid): ragged row passes, column
+    blocks and depth blocks; tilted, it also has generic cells."""
+    base = wl.ring_rig()
+    intr = base.intrinsics[[0, 2, 4]].copy()
+    intr[:, 0] *= 27 / 88
+    intr[:, 1] *= 13 / 32
+    intr[:, 2] = 27 / 2
+    intr[:, 3] = 13 / 2
+    rig = dataclasses.replace(base, n_cams=3, feat_h=13, feat_w=27, n_depth=37, depth_min=1.0,
+                              depth_step=1.5, nx=151, ny=149, x_min=-45.3, y_min=-44.7,
+                              cell_x=0.6, cell_y=0.6, intrinsics=intr,
+                              extrinsics=base.extrinsics[[0, 2, 4]].copy())
+    return wl.tilt_rig(rig, 4.0, -3.0) if tilt else rig
+
+
 def _empty_rig():
     return dataclasses.replace(wl.tiny_rig(), x_min=100.0)      # grid far from the camera
 
@@ -74,6 +91,7 @@ RIGS = {
     "nuscenes_tilted": lambda: wl.tilt_rig(wl.ring_rig()), "highres": lambda: wl.ring_rig(2),
     "anisotropic": _anisotropic_rig, "coarse": _coarse_rig, "coarse_tilted": _coarse_tilted_rig,
     "empty": _empty_rig,
+    "odd": lambda: _odd_rig(False), "odd_tilted": lambda: _odd_rig(True),
     "one_cell": _one_cell_rig,
 }
 
@@ -187,7 +205,8 @@ def test_forward_highres(torch_cuda, pkg, oracle_lib, oracle_plans):
     _check_fp32(got, ref, np.diff(cs))
 
 
-@pytest.mark.parametrize("name", ["coarse", "coarse_tilted", "anisotropic", "empty", "one_cell"])
+@pytest.mark.parametrize("name", ["coarse", "coarse_tilted", "anisotropic", "empty", "one_cell",
+                                  "odd", "odd_tilted"])
 def test_forward_edge_rigs(torch_cuda, pkg, oracle_lib, oracle_plans, name):
     _say(f"[forward edge] {name}")
     rig = RIGS[name]()
@@ -208,6 +227,10 @@ def test_forward_edge_rigs(torch_cuda, pkg, oracle_lib, oracle_plans, name):
         assert plan.info.n_generic > 0 and plan.info.max_per_cell > 1536   # heavy generic cells
     if name == "empty":
         assert plan.info.n_kept == 0 and (got == 0).all()
+    if name.startswith("odd"):
+        assert plan.info.n_kept > 0 and plan.info.n_column > 0
+        if name == "odd_tilted":
+            assert plan.info.n_generic > 0
 
 
 @pytest.mark.parametrize("rig_name", ["nuscenes", "nuscenes_tilted"])
