@@ -300,7 +300,7 @@ int bevpool_launch_backward(const float *G, const void *P, const void *F,
     if (batch > 65535)
         return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "batch=%d exceeds 65535 frames per call", batch);
 
-    const int n_slices = (channels + kSliceChannels - 1) / kSliceChannels;
+    const int n_slices = (channels + kBwdSliceChannels - 1) / kBwdSliceChannels;
     const int slice_c = (channels + n_slices - 1) / n_slices;
     const int nch = (slice_c + 15) / 16;
     const bool vec = nch == 5 && channels % 4 == 0 && slice_c % 4 == 0 &&

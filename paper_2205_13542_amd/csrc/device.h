@@ -108,20 +108,23 @@ struct Row {
 // channel j + 16k. With VEC (rows starting on 16-byte boundaries), values
 // 0..3 are channels 4j..4j+3 instead, so that 64 of the channels move as one
 // 4-element access per lane: for slices of 65..80 channels value 4 is
-// channel 64 + j (NCH = 5), and slices of exactly 64 channels need nothing
-// else (NCH = 4). Lanes past the slice's last channel read bytes that are
-// never stored.
+// channel 64 + j (NCH = 5), slices of exactly 64 channels need nothing else
+// (NCH = 4), and in slices of exactly 128 values 4..7 are channels
+// 64 + 4j..64 + 4j + 3 (NCH = 8). Lanes past the slice's last channel read
+// bytes that are never stored.
 
 // Row slice at byte offset off of its first channel (or kOff plus less than
 // 2^31: every access is then out of range).
 template <int DT, int NCH, bool VEC>
 __device__ __forceinline__ void load_row(Row<NCH> &r, Rsrc src, uint32_t off) {
-    static_assert(!VEC || NCH == 5 || NCH == 4, "4-element lanes hold 64 or 65..80 channels");
+    static_assert(!VEC || NCH == 4 || NCH == 5 || NCH == 8,
+                  "4-element lanes hold 64, 65..80 or 128 channels");
     constexpr uint32_t ES = Elem<DT>::kBytes;
     const uint32_t j = threadIdx.x & 15;
     if constexpr (VEC) {
         Elem<DT>::load4(src, off + 4 * j * ES, r.v);
         if constexpr (NCH == 5) r.v[4] = Elem<DT>::load(src, off + (64 + j) * ES);
+        if constexpr (NCH == 8) Elem<DT>::load4(src, off + (64 + 4 * j) * ES, r.v + 4);
     } else {
 #pragma unroll
         for (int k = 0; k < NCH; ++k) r.v[k] = Elem<DT>::load(src, off + (j + 16 * k) * ES);
@@ -135,12 +138,17 @@ template <int NCH, bool VEC>
 __device__ __forceinline__ void store_row(Rsrc dst, uint32_t off, const float *v, bool tail_ok) {
     const uint32_t j = threadIdx.x & 15;
     if constexpr (VEC) {
-        // a 64-channel slice has no tail: all four values of every lane are in it
+        // slices of 64 or 128 channels have no tail: all their values are in
         __builtin_amdgcn_raw_buffer_store_b128(
             (__attribute__((ext_vector_type(4))) uint32_t){__float_as_uint(v[0]), __float_as_uint(v[1]),
                                                            __float_as_uint(v[2]), __float_as_uint(v[3])},
             dst, int(NCH == 5 || tail_ok ? off + 16 * j : kOff), 0, 0);
         if constexpr (NCH == 5) store_f32(dst, tail_ok ? off + (64 + j) * 4 : kOff, v[4]);
+        if constexpr (NCH == 8)
+            __builtin_amdgcn_raw_buffer_store_b128(
+                (__attribute__((ext_vector_type(4))) uint32_t){__float_as_uint(v[4]), __float_as_uint(v[5]),
+                                                               __float_as_uint(v[6]), __float_as_uint(v[7])},
+                dst, int(tail_ok ? off + 256 + 16 * j : kOff), 0, 0);
     } else {
 #pragma unroll
         for (int k = 0; k < NCH - 1; ++k) store_f32(dst, off + (j + 16 * k) * 4, v[k]);

@@ -33,8 +33,8 @@
 // without write traffic beside it.
 //
 // Channels go across the 16 lanes of a group (channel j + 16k in lane j, or
-// 4j..4j+3 and 64 + j for aligned slices of 65..80 channels), so every load
-// and store of a row is contiguous across the group. Rows wider than
+// 16-byte lanes for aligned slices of 64, 65..80 or 128 channels), so every
+// load and store of a row is contiguous across the group. Rows wider than
 // kSliceChannels are done in slices (grid z).
 //
 // All reads and writes of P, F and the BEV map go through buffer resources
@@ -595,9 +595,15 @@ void launch_dtype(const FwdArgs &a, dim3 grid, int nch, bool vec, hipStream_t s,
             if (vec) hipExtLaunchKernelGGL((k_forward<DT, 4, true, MAXR>), grid, block, 0, s, e0, e1, 0, a);
             else hipExtLaunchKernelGGL((k_forward<DT, 4, false, MAXR>), grid, block, 0, s, e0, e1, 0, a);
             break;
-        default:
+        case 5:
             if (vec) hipExtLaunchKernelGGL((k_forward<DT, 5, true, MAXR>), grid, block, 0, s, e0, e1, 0, a);
             else hipExtLaunchKernelGGL((k_forward<DT, 5, false, MAXR>), grid, block, 0, s, e0, e1, 0, a);
+            break;
+        case 6: hipExtLaunchKernelGGL((k_forward<DT, 6, false, MAXR>), grid, block, 0, s, e0, e1, 0, a); break;
+        case 7: hipExtLaunchKernelGGL((k_forward<DT, 7, false, MAXR>), grid, block, 0, s, e0, e1, 0, a); break;
+        default:
+            if (vec) hipExtLaunchKernelGGL((k_forward<DT, 8, true, MAXR>), grid, block, 0, s, e0, e1, 0, a);
+            else hipExtLaunchKernelGGL((k_forward<DT, 8, false, MAXR>), grid, block, 0, s, e0, e1, 0, a);
             break;
     }
 }
@@ -642,8 +648,15 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
     if (batch > 65535)
         return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "batch=%d exceeds 65535 frames per call", batch);
 
-    const int n_slices = (channels + kSliceChannels - 1) / kSliceChannels;
-    const int slice_c = (channels + n_slices - 1) / n_slices;
+    // Equal slices of at most kSliceChannels channels; slices of 128, 80 or
+    // 64 when they divide C, whose rows move as 16-byte lanes.
+    int slice_c;
+    if (channels % 128 == 0) slice_c = 128;
+    else if (channels % 80 == 0) slice_c = 80;
+    else if (channels % 64 == 0) slice_c = 64;
+    else slice_c = (channels + (channels + kSliceChannels - 1) / kSliceChannels - 1) /
+                   ((channels + kSliceChannels - 1) / kSliceChannels);
+    const int n_slices = (channels + slice_c - 1) / slice_c;
     const int nch = (slice_c + 15) / 16;
 
     FwdArgs a;
@@ -705,7 +718,8 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
     const bool aligned = ldo % 4 == 0 && reinterpret_cast<uintptr_t>(F) % (4 * esize) == 0 &&
                          reinterpret_cast<uintptr_t>(out) % 16 == 0;
     const bool vec = aligned && ((nch == 5 && channels % 4 == 0 && slice_c % 4 == 0) ||
-                                 (nch == 4 && slice_c == 64 && channels % 64 == 0));
+                                 (nch == 4 && slice_c == 64 && channels % 64 == 0) ||
+                                 (nch == 8 && slice_c == 128 && channels % 128 == 0));
     const bool maxr = reduce == BEVPOOL_MAX;
     if (maxr) launch_forward<true>(a, dtype, grid, nch, vec, stream, start, combine ? nullptr : stop);
     else launch_forward<false>(a, dtype, grid, nch, vec, stream, start, combine ? nullptr : stop);

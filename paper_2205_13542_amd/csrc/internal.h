@@ -40,7 +40,8 @@ constexpr int kGroupLanes = 16;                 // lanes per pixel column
 constexpr int kColDepth = 8;
 constexpr int kColWidth = kFwdBlock / kGroupLanes;  // 8 columns per item
 constexpr int kGenHeavy = 256;
-constexpr int kSliceChannels = 80;              // channels per pass
+constexpr int kSliceChannels = 128;             // channels per forward pass, at most
+constexpr int kBwdSliceChannels = 80;           // channels per backward pass
 constexpr int kCombineInline = 8;               // borrowed rows listed with each multi-combo cell
 
 // Column-table entry: {cell (single-combo cell) or borrowed row of its
