@@ -30,7 +30,10 @@
 // in slot order, zeroes the borrowed rows, and zeroes the other empty rows.
 // The zeroing is bandwidth-bound work that covers the latency of the slot
 // reads, and the first launch, whose column items are latency-bound, runs
-// without write traffic beside it.
+// without write traffic beside it. The column items also read the plan
+// arrays that the second launch starts from (the empty-cell list and the
+// multi-combo records) once, so that those first loads of the second launch
+// are served from the caches rather than from HBM.
 //
 // Channels go across the 16 lanes of a group (channel j + 16k in lane j, or
 // 16-byte lanes for aligned slices of 64, 65..80 or 128 channels), so every
@@ -95,7 +98,12 @@ struct FwdArgs {
     int32_t n_heavy, n_light;
     int32_t base_col, base_zero, base_light;
     ZeroArgs zero;
+    // plan arrays read first by the second launch; the column items of
+    // frame 0, slice 0 touch them (kWarmArrays arrays of warm_n[i] words)
+    const int32_t *warm[4];
+    int32_t warm_n[4];
 };
+constexpr int kWarmArrays = 4;
 
 // The buffers of frame b: depth probabilities, features, BEV map.
 struct Frame {
@@ -263,6 +271,18 @@ __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0,
         __builtin_amdgcn_sched_barrier(0);
     }
 
+    // Touch the second launch's plan arrays (after this item's own loads):
+    // item i reads words i * kFwdBlock + t, i * kFwdBlock + t + kFwdBlock *
+    // n_items, ... of each. The values are only kept live until the end.
+    int warm = 0;
+    if (blockIdx.y == 0 && blockIdx.z == 0) {
+        const int stride = a.n_items * kFwdBlock;
+#pragma unroll
+        for (int q = 0; q < kWarmArrays; ++q)
+            for (int i = item * kFwdBlock + int(threadIdx.x); i < a.warm_n[q]; i += stride)
+                warm ^= a.warm[q][i];
+    }
+
     const bool act = e.x >= 0;
     const uint32_t ey = uint32_t(e.y);
     const int hlo = act ? int(ey & 0xFFFFu) : 0x7FFFFFFF;
@@ -308,6 +328,7 @@ __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0,
 
     Emit<0, NCH, VEC>::run(acc, e.x, e.y, dm, fr.O, uint32_t(c0) * 4u, a.ldo, !MAXR && a.mean != 0,
                            tail_ok);
+    asm volatile("" ::"v"(warm));   // the touched words are not needed, only loaded
 }
 
 // A generic cell's runs in chunks of 64: lane i loads run i of the chunk and
@@ -463,9 +484,10 @@ __global__ __launch_bounds__(kFwdBlock) void k_forward(FwdArgs a) {
 // listed in multi_rows[k], so one round of loads finds the cell, its slot
 // count and those rows. The slots are added in slot order into the cell's
 // row, and the borrowed rows are zeroed. One group of 16 lanes per cell,
-// channels j, j + 16, ... The first n_zblocks workgroups zero empty rows
-// instead: dispatched first, their bandwidth-bound stores start at once and
-// cover the latency of the slot reads.
+// channels j, j + 16, ... The last n_zblocks workgroups zero empty rows
+// instead: the combine workgroups are dispatched first, so their two rounds
+// of loads (records, then slot rows; both cached, see the column items) are
+// issued before the bandwidth-bound zero stores, which then cover them.
 constexpr int kCombineChunks = 5;   // 16-channel chunks per pass (80 channels)
 constexpr int kCombineGroups = kBlock / 16;   // cells per workgroup
 static_assert(kCombineInline <= 16, "inline rows come from one lane each of a 16-lane group");
@@ -508,11 +530,12 @@ template <bool MAXR, bool VEC>
 __global__ __launch_bounds__(kBlock) void k_combine(CombineArgs a) {
     __shared__ int s_cell[kBlock];
     const int b = blockIdx.y;
-    if (int(blockIdx.x) < a.n_zblocks) {
-        zero_rows<kBlock>(a.zero, blockIdx.x, b, s_cell);
+    const int n_cblocks = int(gridDim.x) - a.n_zblocks;
+    if (int(blockIdx.x) >= n_cblocks) {
+        zero_rows<kBlock>(a.zero, int(blockIdx.x) - n_cblocks, b, s_cell);
         return;
     }
-    const int k = (int(blockIdx.x) - a.n_zblocks) * kCombineGroups + int(threadIdx.x >> 4);
+    const int k = int(blockIdx.x) * kCombineGroups + int(threadIdx.x >> 4);
     if (k >= a.n_multi) return;
     const int j = threadIdx.x & 15;
     const int ji = j % kCombineInline;
@@ -691,6 +714,14 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
     // partial slots (the combine kernel zeroes them); of the rest, the
     // combine kernel, when there is one, takes the last kZeroLate / 8.
     const bool combine = plan->n_multi > 0;
+    a.warm[0] = plan->empty_cells;
+    a.warm_n[0] = combine ? plan->n_empty : 0;
+    a.warm[1] = plan->multi_rows;
+    a.warm_n[1] = combine ? plan->n_multi * kCombineInline : 0;
+    a.warm[2] = plan->multi_begin;
+    a.warm_n[2] = combine ? plan->n_multi + 1 : 0;
+    a.warm[3] = plan->multi_cell;
+    a.warm_n[3] = combine ? plan->n_multi : 0;
     ZeroArgs z;
     z.out = out;
     z.empty_cells = plan->empty_cells;
