@@ -12,7 +12,10 @@
 // gradient row when the combo (camera, depth bin, column) is clean — all its
 // kept points in one cell, which the plan records — or one per kept row
 // otherwise. dF gets P x G; dP gets the dot product F . G, reduced across the
-// 16 lanes by a transpose-reduce (8 shuffles for the 8 rows' sums). The
+// 16 lanes by a transpose-reduce (8 shuffles for the 8 rows' sums). A
+// wave parks the dP values of a chunk of depth bins in LDS and writes them
+// after the chunk (vector loads and stores share one in-order counter, so a
+// store inside the loop would hold up the waits for the next loads). The
 // waves' dF sums are added in LDS in wave order and stored once; every dP
 // element is written by the one wave that owns its depth bin, so nothing is
 // accumulated with atomics and repeated calls give bitwise equal results.
@@ -135,6 +138,8 @@ constexpr int bwd_stride() { return kBRows * NCH * 16 + 16; }   // one lane grou
 template <int DT, int NCH, bool VEC>
 __global__ __launch_bounds__(kBBlock) void k_backward(BwdArgs a) {
     __shared__ float s_df[(kBWaves - 1) * kBCols * bwd_stride<NCH>()];
+    // dP of a chunk: [wave][depth bin of the chunk][row][column]
+    __shared__ float s_dp[kBWaves * kBChunk * kBRows * kBCols];
     constexpr uint32_t ES = Elem<DT>::kBytes;
     const int b = blockIdx.y;
     // the row blocks of one column block share its gradient rows: placed on
@@ -223,15 +228,26 @@ __global__ __launch_bounds__(kBBlock) void k_backward(BwdArgs a) {
                 }
                 if (a.want_dp) {
                     const float s = transpose_reduce(dot, j);
-                    if (j < kBRows && i < dn && row_ok) {
-                        const uint32_t off = (pt0 + uint32_t(dc + i) * uint32_t(a.HW)) * 4u;
-                        float v = kept ? s : 0.f;
-                        if (a.accumulate_dp) v += __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(dP, int(off), 0, 0));
-                        store_f32(dP, off, v);
-                    }
+                    if (j < kBRows && i < dn)
+                        s_dp[((wave * kBChunk + i) * kBRows + j) * kBCols + grp] = kept ? s : 0.f;
                 }
                 load_stage(st[u], i + kBStages);
             }
+        }
+        if (a.want_dp) {
+            // the chunk's dP, 4 columns (16 contiguous bytes) per 4 lanes:
+            // value q of the wave is column q % 4, row q / 4 % 8, bin q / 32
+            __builtin_amdgcn_wave_barrier();
+            for (int q = lane; q < dn * kBRows * kBCols; q += kWaveSize) {
+                const int qc = q % kBCols, qr = (q / kBCols) % kBRows, qi = q / (kBCols * kBRows);
+                const int wq = cb * kBCols + qc, hq = h0 + qr;
+                const uint32_t off = wq < a.W && hq < a.H
+                    ? uint32_t(((n * a.D + dc + qi) * a.H + hq) * a.W + wq) * 4u : kOff;
+                float v = s_dp[(wave * kBChunk + qi) * kBRows * kBCols + q % (kBRows * kBCols)];
+                if (a.accumulate_dp) v += __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(dP, int(off), 0, 0));
+                store_f32(dP, off, v);
+            }
+            __builtin_amdgcn_wave_barrier();
         }
     }
 
