@@ -304,6 +304,16 @@ __global__ __launch_bounds__(kBlock) void k_cell_stats(const int32_t *cell_start
     }
 }
 
+// Four single counts next to each other, so that one copy brings them to
+// the host.
+__global__ void k_gather4(int32_t *dst, const int32_t *a, const int32_t *b, const int32_t *c,
+                          const int32_t *d) {
+    dst[0] = *a;
+    dst[1] = *b;
+    dst[2] = *c;
+    dst[3] = *d;
+}
+
 // ---------------------------------------------------------------- work partition
 //
 // Combos, items and cell classes as described in internal.h. Every kernel
@@ -552,6 +562,29 @@ int dev_alloc(T **p, size_t count, const char *what) {
     return BEVPOOL_OK;
 }
 
+// One device allocation carved into the plan build's temporaries: each
+// piece is rounded to 256 bytes, and the total is reserved from upper bounds
+// that the geometry fixes, so a build makes one allocation for them instead
+// of one per array (each hipMalloc and hipFree costs about 10 us of host
+// time).
+struct Arena {
+    char *base = nullptr;
+    size_t cap = 0, used = 0;
+    static size_t piece(size_t bytes) { return ((bytes ? bytes : 1) + 255) & ~size_t(255); }
+    template <typename T>
+    int take(T **p, size_t count, const char *what) {
+        const size_t b = piece(count * sizeof(T));
+        if (used + b > cap) {
+            *p = nullptr;
+            return bevpool_fail(BEVPOOL_ERR_HIP, "plan temporaries: %s does not fit the reserved %zu bytes",
+                                what, cap);
+        }
+        *p = reinterpret_cast<T *>(base + used);
+        used += b;
+        return BEVPOOL_OK;
+    }
+};
+
 // Chunk sums a multi-block scan of n elements needs.
 int64_t scan_sums_needed(int64_t n) { return (n + kScanChunk - 1) / kScanChunk; }
 
@@ -591,9 +624,10 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
     if ((rc = dev_alloc(&plan->cell_start, size_t(n_cells) + 1, "cell_start"))) return rc;
     if ((rc = dev_alloc(&plan->column_table, size_t(n_combo), "column_table"))) return rc;
 
-    // temporaries, freed on every exit path below
+    // temporaries, carved from one arena that is freed on every exit path below
     const int64_t sort_cap = np64 > n_cells ? np64 : int64_t(n_cells);
     const int sort_tiles_cap = int((sort_cap + kSortTile - 1) / kSortTile);
+    Arena arena;
     double *d_calib = nullptr;
     uint32_t *keys_a = nullptr, *keys_b = nullptr;
     int32_t *vals_a = nullptr, *vals_b = nullptr, *hist = nullptr, *small = nullptr;
@@ -602,15 +636,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
     int32_t *combo_cell = nullptr, *combo_range = nullptr, *combo_flag = nullptr;
     int32_t *cell_generic = nullptr, *cell_ncombo = nullptr, *head_scan = nullptr;
     int32_t *run_scan = nullptr, *run_begin = nullptr, *pos_of_cell = nullptr;
-    auto cleanup = [&]() {
-        for (void *q : {(void *)d_calib, (void *)keys_a, (void *)keys_b, (void *)vals_a,
-                        (void *)vals_b, (void *)hist, (void *)small, (void *)scan_sums, (void *)flag_a,
-                        (void *)flag_b, (void *)combo_range,
-                        (void *)combo_flag, (void *)cell_generic, (void *)cell_ncombo,
-                        (void *)head_scan, (void *)run_scan, (void *)run_begin,
-                        (void *)pos_of_cell})
-            (void)hipFree(q);
-    };
+    auto cleanup = [&]() { (void)hipFree(arena.base); };
 
     // stable LSD radix sort of (keys, vals)[0, n) on the low `bits` bits; the
     // result ends in (keys, vals)
@@ -653,22 +679,41 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
 
     auto run = [&]() -> int {
         int rc2;
-        if (!host_cells && (rc2 = dev_alloc(&d_calib, size_t(g.n_cams) * 16, "calibration")))
+        {
+            // upper bounds of every temporary taken below: the partial slots
+            // (n_part) are at most the combos, the kept points at most the
+            // points, the generic cells at most the cells
+            const size_t i4 = sizeof(int32_t);
+            const size_t sort_b = Arena::piece(size_t(sort_cap) * i4);
+            const size_t cells1_b = Arena::piece((size_t(n_cells) + 1) * i4);
+            const size_t combo1_b = Arena::piece((size_t(n_combo) + 1) * i4);
+            arena.cap = Arena::piece(size_t(g.n_cams) * 16 * sizeof(double)) + 4 * sort_b +
+                        Arena::piece(size_t(sort_tiles_cap) * 256 * i4) + Arena::piece(12 * i4) +
+                        Arena::piece(size_t(scan_sums_needed(sort_cap + 1)) * i4) +
+                        5 * cells1_b +                 // flag_a, flag_b, cell_generic, cell_ncombo, run_begin
+                        Arena::piece(size_t(n_cells) * i4) +          // pos_of_cell
+                        2 * combo1_b +                 // combo_flag, head_scan
+                        Arena::piece(size_t(n_combo) * i4) +          // combo_range
+                        Arena::piece((size_t(np) + 1) * i4);          // run_scan
+            if ((rc2 = dev_alloc(&arena.base, arena.cap, "plan temporaries"))) return rc2;
+        }
+        if (!host_cells && (rc2 = arena.take(&d_calib, size_t(g.n_cams) * 16, "calibration")))
             return rc2;
-        if ((rc2 = dev_alloc(&keys_a, size_t(sort_cap), "sort keys"))) return rc2;
-        if ((rc2 = dev_alloc(&keys_b, size_t(sort_cap), "sort keys"))) return rc2;
-        if ((rc2 = dev_alloc(&vals_a, size_t(sort_cap), "sort values"))) return rc2;
-        if ((rc2 = dev_alloc(&vals_b, size_t(sort_cap), "sort values"))) return rc2;
-        if ((rc2 = dev_alloc(&hist, size_t(sort_tiles_cap) * 256, "radix histogram"))) return rc2;
-        if ((rc2 = dev_alloc(&small, 8, "plan counters"))) return rc2;
+        if ((rc2 = arena.take(&keys_a, size_t(sort_cap), "sort keys"))) return rc2;
+        if ((rc2 = arena.take(&keys_b, size_t(sort_cap), "sort keys"))) return rc2;
+        if ((rc2 = arena.take(&vals_a, size_t(sort_cap), "sort values"))) return rc2;
+        if ((rc2 = arena.take(&vals_b, size_t(sort_cap), "sort values"))) return rc2;
+        if ((rc2 = arena.take(&hist, size_t(sort_tiles_cap) * 256, "radix histogram"))) return rc2;
+        // [0..1] cell stats, [3] scan totals, [4..5] class counters, [8..11] gathered counts
+        if ((rc2 = arena.take(&small, 12, "plan counters"))) return rc2;
         // the longest scan is over sort_cap + 1 elements (radix histograms
         // are shorter)
-        if ((rc2 = dev_alloc(&scan_sums, size_t(scan_sums_needed(sort_cap + 1)), "scan chunk sums")))
+        if ((rc2 = arena.take(&scan_sums, size_t(scan_sums_needed(sort_cap + 1)), "scan chunk sums")))
             return rc2;
-        if ((rc2 = dev_alloc(&flag_a, size_t(n_cells) + 1, "flags"))) return rc2;
-        if ((rc2 = dev_alloc(&flag_b, size_t(n_cells) + 1, "flags"))) return rc2;
+        if ((rc2 = arena.take(&flag_a, size_t(n_cells) + 1, "flags"))) return rc2;
+        if ((rc2 = arena.take(&flag_b, size_t(n_cells) + 1, "flags"))) return rc2;
 
-        fill(small, 8, 0);
+        fill(small, 12, 0);
         if (host_cells) {
             // a stored association: the cell map as exported, checked by the caller
             BEVPOOL_HIP(hipMemcpyAsync(plan->cell_of_point, host_cells, sizeof(int32_t) * size_t(np),
@@ -709,10 +754,10 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         // the combo cells stay with the plan (the backward pass reads them)
         if ((rc2 = dev_alloc(&plan->combo_cells, size_t(n_combo), "combo cells"))) return rc2;
         combo_cell = plan->combo_cells;
-        if ((rc2 = dev_alloc(&combo_range, size_t(n_combo), "combo ranges"))) return rc2;
-        if ((rc2 = dev_alloc(&combo_flag, size_t(n_combo) + 1, "combo flags"))) return rc2;
-        if ((rc2 = dev_alloc(&cell_generic, size_t(n_cells), "cell classes"))) return rc2;
-        if ((rc2 = dev_alloc(&cell_ncombo, size_t(n_cells), "cell combos"))) return rc2;
+        if ((rc2 = arena.take(&combo_range, size_t(n_combo), "combo ranges"))) return rc2;
+        if ((rc2 = arena.take(&combo_flag, size_t(n_combo) + 1, "combo flags"))) return rc2;
+        if ((rc2 = arena.take(&cell_generic, size_t(n_cells), "cell classes"))) return rc2;
+        if ((rc2 = arena.take(&cell_ncombo, size_t(n_cells), "cell combos"))) return rc2;
         fill(cell_generic, n_cells, 0);
         fill(cell_ncombo, n_cells, 0);
         ComboArgs ca;
@@ -741,15 +786,20 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
             device_scan(flag_b, int64_t(n_cells) + 1, small + 3, scan_sums, stream);       // empty cells
             device_scan(combo_flag, n_combo + 1, small + 3, scan_sums, stream);   // combos of multi cells
             BEVPOOL_HIP(hipGetLastError());
-            BEVPOOL_HIP(hipMemcpyAsync(stats, small, sizeof(stats), hipMemcpyDeviceToHost, stream));
-            BEVPOOL_HIP(hipMemcpyAsync(counters, small + 4, sizeof(counters),
-                                       hipMemcpyDeviceToHost, stream));
-            int rc3;
-            if ((rc3 = to_host(&n_gen, flag_a + n_cells))) return rc3;
-            if ((rc3 = to_host(&n_empty, flag_b + n_cells))) return rc3;
-            if ((rc3 = to_host(&kept, plan->cell_start + n_cells))) return rc3;
-            if ((rc3 = to_host(&n_part, combo_flag + n_combo))) return rc3;
+            hipLaunchKernelGGL(k_gather4, dim3(1), dim3(1), 0, stream, small + 8, flag_a + n_cells,
+                               flag_b + n_cells, plan->cell_start + n_cells, combo_flag + n_combo);
+            BEVPOOL_HIP(hipGetLastError());
+            int32_t h[12];
+            BEVPOOL_HIP(hipMemcpyAsync(h, small, sizeof(h), hipMemcpyDeviceToHost, stream));
             BEVPOOL_HIP(hipStreamSynchronize(stream));
+            stats[0] = h[0];
+            stats[1] = h[1];
+            counters[0] = h[4];
+            counters[1] = h[5];
+            n_gen = h[8];          // generic cells
+            n_empty = h[9];        // empty cells
+            kept = h[10];          // kept points
+            n_part = h[11];        // combos of multi-combo cells (partial slots)
             return BEVPOOL_OK;
         };
         if ((rc2 = classify())) return rc2;
@@ -774,7 +824,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
 
         // partial-sum slots of the multi-combo cells, kept in the first
         // n_part empty rows
-        if ((rc2 = dev_alloc(&head_scan, size_t(n_part) + 1, "multi heads"))) return rc2;
+        if ((rc2 = arena.take(&head_scan, size_t(n_part) + 1, "multi heads"))) return rc2;
         fill(head_scan, int64_t(n_part) + 1, 0);
         if (n_part > 0) {
             hipLaunchKernelGGL(k_multi_compact, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream,
@@ -815,9 +865,9 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         if ((rc2 = radix_sort(gen_key, gen_cell, n_gen, bits_for(plan->max_per_cell)))) return rc2;
 
         // runs of the generic cells, in list order
-        if ((rc2 = dev_alloc(&run_scan, size_t(kept) + 1, "run flags"))) return rc2;
-        if ((rc2 = dev_alloc(&run_begin, size_t(n_gen) + 1, "run offsets"))) return rc2;
-        if ((rc2 = dev_alloc(&pos_of_cell, size_t(n_cells), "cell positions"))) return rc2;
+        if ((rc2 = arena.take(&run_scan, size_t(kept) + 1, "run flags"))) return rc2;
+        if ((rc2 = arena.take(&run_begin, size_t(n_gen) + 1, "run offsets"))) return rc2;
+        if ((rc2 = arena.take(&pos_of_cell, size_t(n_cells), "cell positions"))) return rc2;
         fill(run_scan, int64_t(kept) + 1, 0);
         fill(run_begin, int64_t(n_gen) + 1, 0);
         const FastDiv div_hw = make_fastdiv(uint32_t(HW)), div_d = make_fastdiv(uint32_t(D));
