@@ -50,6 +50,8 @@ WORKLOAD_TEXT = {
     "nuscenes_f16": "nuScenes-shaped frame, fp16 P and F, fp32 accumulate/output -> 360x360",
     "nuscenes_b8": "8 nuScenes-shaped frames sharing one plan, C=80 fp32 -> 8 x 360x360",
     "highres": "6 cams x 236 bins x 64x176, C=128 fp32, 90% one-hot depth -> 720x720 at 0.15 m",
+    "nuscenes_tilted": "nuScenes-shaped frame, every camera pitched 5 deg and rolled 2 deg (generic cells), C=80 fp32 -> 360x360",
+    "nuscenes_tilt1": "nuScenes-shaped frame, every camera pitched 1 deg and rolled 0.5 deg, C=80 fp32 -> 360x360",
 }
 
 

@@ -248,6 +248,8 @@ WORKLOADS = {
     # test-only rigs
     "tiny_identity": (identity_rig, 8, 1, "normal", "f32"),
     "nuscenes_tilted": (lambda: tilt_rig(ring_rig()), 80, 1, "peaked", "f32"),
+    # the same rig with a calibration-sized tilt: pitch 1 deg, roll 0.5 deg
+    "nuscenes_tilt1": (lambda: tilt_rig(ring_rig(), 1.0, 0.5), 80, 1, "peaked", "f32"),
 }
 
 
