@@ -95,6 +95,7 @@ struct FwdArgs {
     const int32_t *cell_start;          // interval table: point counts of the cells
     uint32_t p_bytes, f_bytes, o_bytes, run_bytes;   // per frame (runs: whole table)
     int32_t items_d, items_w, n_items;
+    int32_t n_planes, plane;            // column-table planes in use, entries per plane
     int32_t n_heavy, n_light;
     int32_t base_col, base_zero, base_light;
     ZeroArgs zero;
@@ -226,7 +227,7 @@ __device__ void zero_rows(const ZeroArgs &z, int zb, int b, int *s_cell) {
 template <int BS>
 int zero_blocks(const ZeroArgs &z) { return (z.zero_end - z.zero_begin + BS - 1) / BS; }
 
-template <int DT, int NCH, bool VEC, bool MAXR>
+template <int DT, int NCH, bool VEC, bool MAXR, bool SEG>
 __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0, int cn,
                             float *s_pb) {
     constexpr uint32_t ES = Elem<DT>::kBytes;
@@ -258,8 +259,11 @@ __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0,
         load_row<DT, NCH, VEC>(st.f0, fr.F, h < H ? f_col + uint32_t(h) * f_row : kOff);
         load_row<DT, NCH, VEC>(st.f1, fr.F, h + 1 < H ? f_col + uint32_t(h + 1) * f_row : kOff);
     };
+    // plane 0 of the column table holds each combo's first row segment (the
+    // whole combo on a level rig); plane s its segment s, done in pass s
+    const int64_t tab0 = (int64_t(n) * a.D + d) * a.W + w;
     int2 e = make_int2(-1, 0);
-    if (dw_ok) e = a.table[(int64_t(n) * a.D + d) * a.W + w];
+    if (dw_ok) e = a.table[tab0];
     Stage<NCH> st[kStages];
     // Issued stage by stage, in the order in which the loop consumes them:
     // the loop's waits count outstanding loads in issue order, and a
@@ -283,6 +287,7 @@ __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0,
                 warm ^= a.warm[q][i];
     }
 
+    for (int pass = 0;;) {
     const bool act = e.x >= 0;
     const uint32_t ey = uint32_t(e.y);
     const int hlo = act ? int(ey & 0xFFFFu) : 0x7FFFFFFF;
@@ -328,6 +333,26 @@ __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0,
 
     Emit<0, NCH, VEC>::run(acc, e.x, e.y, dm, fr.O, uint32_t(c0) * 4u, a.ldo, !MAXR && a.mean != 0,
                            tail_ok);
+    // the next plane with an entry in this wave, if any: its rows again
+    // (only in the SEG instantiation, launched for plans with several
+    // planes: the loop costs registers that the generic roles, which share
+    // the kernel, would lose in occupancy)
+    if constexpr (!SEG) break;
+    bool more = false;
+    while (++pass < a.n_planes) {
+        e = dw_ok ? a.table[int64_t(pass) * a.plane + tab0] : make_int2(-1, 0);
+        if (__ballot(e.x >= 0) != 0) {
+            more = true;
+            break;
+        }
+    }
+    if (!more) break;
+#pragma unroll
+    for (int u = 0; u < kStages; ++u) {
+        load_stage(st[u], 2 * u);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    }
     asm volatile("" ::"v"(warm));   // the touched words are not needed, only loaded
 }
 
@@ -453,7 +478,7 @@ __device__ void heavy_generic(const FwdArgs &a, const Frame &fr, int k, int c0, 
     }
 }
 
-template <int DT, int NCH, bool VEC, bool MAXR>
+template <int DT, int NCH, bool VEC, bool MAXR, bool SEG>
 __global__ __launch_bounds__(kFwdBlock) void k_forward(FwdArgs a) {
     __shared__ float s_part[kColWidth * slot_stride<NCH>()];   // heavy cells: group partials
     __shared__ int s_cell[kFwdBlock];                          // zero rows: cell ids
@@ -466,7 +491,7 @@ __global__ __launch_bounds__(kFwdBlock) void k_forward(FwdArgs a) {
     } else if (bx < a.base_col) {
         return;  // padding: column items start on a multiple of 8
     } else if (bx < a.base_col + a.n_items) {
-        column_item<DT, NCH, VEC, MAXR>(a, Frame(a, b), xcd_cu_remap<kCuRounds>(bx - a.base_col, a.n_items),
+        column_item<DT, NCH, VEC, MAXR, SEG>(a, Frame(a, b), xcd_cu_remap<kCuRounds>(bx - a.base_col, a.n_items),
                                         c0, cn, s_pb);
     } else if (bx < a.base_zero) {
         return;
@@ -606,38 +631,38 @@ __global__ __launch_bounds__(kBlock) void k_combine(CombineArgs a) {
 
 // Kernel-boundary events (either may be null): they take the timestamps of
 // the dispatch itself rather than of separate queue entries.
-template <int DT, bool MAXR>
+template <int DT, bool MAXR, bool SEG>
 void launch_dtype(const FwdArgs &a, dim3 grid, int nch, bool vec, hipStream_t s, hipEvent_t e0,
                   hipEvent_t e1) {
     const dim3 block(kFwdBlock);
     switch (nch) {
-        case 1: hipExtLaunchKernelGGL((k_forward<DT, 1, false, MAXR>), grid, block, 0, s, e0, e1, 0, a); break;
-        case 2: hipExtLaunchKernelGGL((k_forward<DT, 2, false, MAXR>), grid, block, 0, s, e0, e1, 0, a); break;
-        case 3: hipExtLaunchKernelGGL((k_forward<DT, 3, false, MAXR>), grid, block, 0, s, e0, e1, 0, a); break;
+        case 1: hipExtLaunchKernelGGL((k_forward<DT, 1, false, MAXR, SEG>), grid, block, 0, s, e0, e1, 0, a); break;
+        case 2: hipExtLaunchKernelGGL((k_forward<DT, 2, false, MAXR, SEG>), grid, block, 0, s, e0, e1, 0, a); break;
+        case 3: hipExtLaunchKernelGGL((k_forward<DT, 3, false, MAXR, SEG>), grid, block, 0, s, e0, e1, 0, a); break;
         case 4:
-            if (vec) hipExtLaunchKernelGGL((k_forward<DT, 4, true, MAXR>), grid, block, 0, s, e0, e1, 0, a);
-            else hipExtLaunchKernelGGL((k_forward<DT, 4, false, MAXR>), grid, block, 0, s, e0, e1, 0, a);
+            if (vec) hipExtLaunchKernelGGL((k_forward<DT, 4, true, MAXR, SEG>), grid, block, 0, s, e0, e1, 0, a);
+            else hipExtLaunchKernelGGL((k_forward<DT, 4, false, MAXR, SEG>), grid, block, 0, s, e0, e1, 0, a);
             break;
         case 5:
-            if (vec) hipExtLaunchKernelGGL((k_forward<DT, 5, true, MAXR>), grid, block, 0, s, e0, e1, 0, a);
-            else hipExtLaunchKernelGGL((k_forward<DT, 5, false, MAXR>), grid, block, 0, s, e0, e1, 0, a);
+            if (vec) hipExtLaunchKernelGGL((k_forward<DT, 5, true, MAXR, SEG>), grid, block, 0, s, e0, e1, 0, a);
+            else hipExtLaunchKernelGGL((k_forward<DT, 5, false, MAXR, SEG>), grid, block, 0, s, e0, e1, 0, a);
             break;
-        case 6: hipExtLaunchKernelGGL((k_forward<DT, 6, false, MAXR>), grid, block, 0, s, e0, e1, 0, a); break;
-        case 7: hipExtLaunchKernelGGL((k_forward<DT, 7, false, MAXR>), grid, block, 0, s, e0, e1, 0, a); break;
+        case 6: hipExtLaunchKernelGGL((k_forward<DT, 6, false, MAXR, SEG>), grid, block, 0, s, e0, e1, 0, a); break;
+        case 7: hipExtLaunchKernelGGL((k_forward<DT, 7, false, MAXR, SEG>), grid, block, 0, s, e0, e1, 0, a); break;
         default:
-            if (vec) hipExtLaunchKernelGGL((k_forward<DT, 8, true, MAXR>), grid, block, 0, s, e0, e1, 0, a);
-            else hipExtLaunchKernelGGL((k_forward<DT, 8, false, MAXR>), grid, block, 0, s, e0, e1, 0, a);
+            if (vec) hipExtLaunchKernelGGL((k_forward<DT, 8, true, MAXR, SEG>), grid, block, 0, s, e0, e1, 0, a);
+            else hipExtLaunchKernelGGL((k_forward<DT, 8, false, MAXR, SEG>), grid, block, 0, s, e0, e1, 0, a);
             break;
     }
 }
 
-template <bool MAXR>
+template <bool MAXR, bool SEG>
 void launch_forward(const FwdArgs &a, int dtype, dim3 grid, int nch, bool vec, hipStream_t s,
                     hipEvent_t e0, hipEvent_t e1) {
     switch (dtype) {
-        case BEVPOOL_F32: launch_dtype<BEVPOOL_F32, MAXR>(a, grid, nch, vec, s, e0, e1); break;
-        case BEVPOOL_BF16: launch_dtype<BEVPOOL_BF16, MAXR>(a, grid, nch, vec, s, e0, e1); break;
-        default: launch_dtype<BEVPOOL_F16, MAXR>(a, grid, nch, vec, s, e0, e1); break;
+        case BEVPOOL_F32: launch_dtype<BEVPOOL_F32, MAXR, SEG>(a, grid, nch, vec, s, e0, e1); break;
+        case BEVPOOL_BF16: launch_dtype<BEVPOOL_BF16, MAXR, SEG>(a, grid, nch, vec, s, e0, e1); break;
+        default: launch_dtype<BEVPOOL_F16, MAXR, SEG>(a, grid, nch, vec, s, e0, e1); break;
     }
 }
 
@@ -707,6 +732,8 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
     a.items_d = (g.n_depth + kColDepth - 1) / kColDepth;
     a.items_w = (g.feat_w + kColWidth - 1) / kColWidth;
     a.n_items = g.n_cams * a.items_d * a.items_w;
+    a.n_planes = plan->n_planes;
+    a.plane = g.n_cams * g.n_depth * g.feat_w;
     a.n_heavy = plan->n_generic_heavy;
     a.n_light = plan->n_generic - plan->n_generic_heavy;
 
@@ -752,8 +779,12 @@ int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *p
                                  (nch == 4 && slice_c == 64 && channels % 64 == 0) ||
                                  (nch == 8 && slice_c == 128 && channels % 128 == 0));
     const bool maxr = reduce == BEVPOOL_MAX;
-    if (maxr) launch_forward<true>(a, dtype, grid, nch, vec, stream, start, combine ? nullptr : stop);
-    else launch_forward<false>(a, dtype, grid, nch, vec, stream, start, combine ? nullptr : stop);
+    hipEvent_t fstop = combine ? nullptr : stop;
+    const bool seg = a.n_planes > 1;   // some combos split into row segments: several passes
+    if (maxr && seg) launch_forward<true, true>(a, dtype, grid, nch, vec, stream, start, fstop);
+    else if (maxr) launch_forward<true, false>(a, dtype, grid, nch, vec, stream, start, fstop);
+    else if (seg) launch_forward<false, true>(a, dtype, grid, nch, vec, stream, start, fstop);
+    else launch_forward<false, false>(a, dtype, grid, nch, vec, stream, start, fstop);
     BEVPOOL_HIP(hipGetLastError());
     if (combine) {
         CombineArgs ca;

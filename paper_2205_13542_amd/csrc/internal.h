@@ -48,6 +48,7 @@ constexpr int kCombineInline = 8;               // borrowed rows listed with eac
 // partial slot (multi), h_lo | h_hi << 16 | kComboMulti}.
 constexpr uint32_t kComboMulti = 1u << 31;
 constexpr int kMaxFeatH = 1 << 14;              // rows must fit the 15-bit fields
+constexpr int kMaxSeg = 4;                      // row segments of a combo served by column items
 
 // Unsigned division by a run-time constant through a multiply-high, after
 // Granlund and Montgomery, "Division by invariant integers using
@@ -89,6 +90,7 @@ struct bevpool_plan_s {
     int32_t *multi_begin;    // [n_multi + 1]: first partial slot of each multi-combo cell
     int32_t *multi_cell;     // [n_multi]
     int32_t *multi_rows;     // [n_multi][kCombineInline]: borrowed rows of the first slots, or -1
+    int32_t n_planes;        // segment planes of the column table in use (1 for a level rig)
     int4 *generic_hdr;       // [n_generic]: {cell, first run, runs, points}, most points first
     int4 *generic_runs;      // [n_runs]: {first point id, pixel, depth bins, 0}
     int32_t *empty_cells;    // [n_empty] cells without points, ascending

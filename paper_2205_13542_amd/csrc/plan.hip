@@ -332,10 +332,19 @@ struct ComboArgs {
     int32_t *combo_cell;        // [N*D*W]: cell of a clean combo, -1 none kept, -2 not clean
     int32_t *combo_range;       // [N*D*W]: h_lo | h_hi << 16
     int32_t *cell_generic;      // [n_cells]: 1 if a combo that is not clean touches the cell
-    int32_t *cell_ncombo;       // [n_cells]: clean combos of the cell
+    int32_t *cell_ncombo;       // [n_cells]: row segments of column-served combos in the cell
+    int32_t planes;             // segments a combo may have and stay column-served
+    int32_t *seg_cell;          // [planes][N*D*W]: cell of segment s of the combo, or -1
+    int32_t *seg_range;         // [planes][N*D*W]: its rows h_lo | h_hi << 16
+    int32_t *max_seg;           // most segments of a column-served combo
+    int32_t *served_pts;        // kept points of column-served combos
 };
 
-// One thread per combo walks its H rows.
+// One thread per combo walks its H rows and splits the kept ones into
+// segments: maximal runs of consecutive kept rows in one cell. A combo with
+// at most `planes` segments is served by the column items, one segment per
+// pass (a level camera gives every combo one segment: a clean combo);
+// otherwise its cells are generic.
 __global__ __launch_bounds__(kBlock) void k_combo_walk(ComboArgs a) {
     const int64_t x = int64_t(blockIdx.x) * kBlock + threadIdx.x;
     const int64_t n_combo = int64_t(a.N) * a.D * a.W;
@@ -343,34 +352,47 @@ __global__ __launch_bounds__(kBlock) void k_combo_walk(ComboArgs a) {
     const int32_t X = int32_t(x);
     const int32_t w = X % a.W, nd = X / a.W;
     const int64_t base = int64_t(nd) * a.H * a.W + w;
-    int32_t c0 = -1, hlo = -1, hlast = -1, kept = 0;
-    bool one_cell = true;
+    int32_t cell[kMaxSeg], lo[kMaxSeg], hi[kMaxSeg];
+    int32_t n_seg = 0, cur = -1, first = -1, last = -1, kept = 0;
     for (int32_t h = 0; h < a.H; ++h) {
         const int32_t c = a.cell_of_point[base + int64_t(h) * a.W];
-        if (c < 0) continue;
-        if (kept == 0) {
-            c0 = c;
-            hlo = h;
-        } else if (c != c0) {
-            one_cell = false;
+        if (c < 0) {
+            cur = -1;
+            continue;
         }
-        hlast = h;
         ++kept;
+        if (first < 0) first = h;
+        last = h;
+        if (c != cur) {
+            if (n_seg < a.planes) {
+                cell[n_seg] = c;
+                lo[n_seg] = h;
+            }
+            ++n_seg;
+            cur = c;
+        }
+        if (n_seg <= a.planes) hi[n_seg - 1] = h + 1;
     }
-    if (kept == 0) {
+    for (int s = 0; s < a.planes; ++s) a.seg_cell[int64_t(s) * n_combo + X] = -1;
+    if (n_seg == 0) {
         a.combo_cell[X] = -1;
         a.combo_range[X] = 0;
         return;
     }
-    const bool clean = a.allow_clean && one_cell && kept == hlast - hlo + 1;
-    if (clean) {
-        a.combo_cell[X] = c0;
-        a.combo_range[X] = hlo | ((hlast + 1) << 16);
-        atomicAdd(&a.cell_ncombo[c0], 1);
+    if (a.allow_clean && n_seg <= a.planes) {
+        for (int s = 0; s < n_seg; ++s) {
+            a.seg_cell[int64_t(s) * n_combo + X] = cell[s];
+            a.seg_range[int64_t(s) * n_combo + X] = lo[s] | (hi[s] << 16);
+            atomicAdd(&a.cell_ncombo[cell[s]], 1);
+        }
+        atomicMax(a.max_seg, n_seg);
+        atomicAdd(a.served_pts, kept);
+        a.combo_cell[X] = n_seg == 1 ? cell[0] : -2;
+        a.combo_range[X] = n_seg == 1 ? (lo[0] | (hi[0] << 16)) : 0;
     } else {
         a.combo_cell[X] = -2;
         a.combo_range[X] = 0;
-        for (int32_t h = hlo; h <= hlast; ++h) {
+        for (int32_t h = first; h <= last; ++h) {
             const int32_t c = a.cell_of_point[base + int64_t(h) * a.W];
             if (c >= 0) atomicOr(&a.cell_generic[c], 1);
         }
@@ -392,20 +414,20 @@ __global__ __launch_bounds__(kBlock) void k_cell_class(ComboArgs a, const int32_
     if (cnt > kGenHeavy && !served) atomicAdd(&counters[1], 1);
 }
 
-// Column table entries, and a flag on each combo of a multi-combo cell.
+// Column table entries, one plane per segment index, and a flag on each
+// segment of a cell fed by several segments.
 __global__ __launch_bounds__(kBlock) void k_combo_table(ComboArgs a, int2 *table, int32_t *multi_flag) {
-    const int64_t x = int64_t(blockIdx.x) * kBlock + threadIdx.x;
-    if (x >= int64_t(a.N) * a.D * a.W) return;
-    const int32_t X = int32_t(x);
-    const int32_t c = a.combo_cell[X];
+    const int64_t t = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    if (t >= int64_t(a.planes) * a.N * a.D * a.W) return;
+    const int32_t c = a.seg_cell[t];
     int2 e = make_int2(-1, 0);
     bool multi = false;
     if (c >= 0 && a.cell_generic[c] == 0) {
         multi = a.cell_ncombo[c] > 1;
-        e = make_int2(c, a.combo_range[X] | int32_t(multi ? kComboMulti : 0u));
+        e = make_int2(c, a.seg_range[t] | int32_t(multi ? kComboMulti : 0u));
     }
-    table[X] = e;
-    multi_flag[X] = multi ? 1 : 0;
+    table[t] = e;
+    multi_flag[t] = multi ? 1 : 0;
 }
 
 // Not enough empty rows to hold the partial sums: cells fed by several
@@ -421,13 +443,13 @@ __global__ __launch_bounds__(kBlock) void k_empty_list(const int32_t *empty_pos,
     if (c < n_cells && empty_pos[c + 1] != empty_pos[c]) empty_cells[empty_pos[c]] = c;
 }
 
-// Combos of multi-combo cells as (cell, combo) pairs in combo order.
-__global__ __launch_bounds__(kBlock) void k_multi_compact(const int32_t *combo_cell,
-                                                          const int32_t *multi_pos, int32_t n_combo,
+// Segments of multi-segment cells as (cell, segment) pairs in segment order.
+__global__ __launch_bounds__(kBlock) void k_multi_compact(const int32_t *seg_cell,
+                                                          const int32_t *multi_pos, int32_t n_seg,
                                                           uint32_t *key, int32_t *val) {
     const int32_t X = blockIdx.x * kBlock + threadIdx.x;
-    if (X >= n_combo || multi_pos[X + 1] == multi_pos[X]) return;
-    key[multi_pos[X]] = uint32_t(combo_cell[X]);
+    if (X >= n_seg || multi_pos[X + 1] == multi_pos[X]) return;
+    key[multi_pos[X]] = uint32_t(seg_cell[X]);
     val[multi_pos[X]] = X;
 }
 
@@ -615,6 +637,11 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
     const int32_t N = g.n_cams, D = g.n_depth, H = g.feat_h, W = g.feat_w;
     const int32_t HW = H * W;
     const int64_t n_combo = int64_t(N) * D * W;
+    // column-table planes: segment indices a combo may use (a segment has a
+    // row of its own, so never more than H)
+    const int32_t planes = H < kMaxSeg ? H : kMaxSeg;
+    const int64_t n_seg = int64_t(planes) * n_combo;   // table entries reserved
+    int64_t n_seg_act = n_seg;                          // entries of the planes in use
     plan->n_points = np64;
     plan->n_cells = n_cells;
 
@@ -622,7 +649,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
     if ((rc = dev_alloc(&plan->cell_of_point, size_t(np), "cell_of_point"))) return rc;
     if ((rc = dev_alloc(&plan->sorted_point, size_t(np), "sorted_point"))) return rc;
     if ((rc = dev_alloc(&plan->cell_start, size_t(n_cells) + 1, "cell_start"))) return rc;
-    if ((rc = dev_alloc(&plan->column_table, size_t(n_combo), "column_table"))) return rc;
+    if ((rc = dev_alloc(&plan->column_table, size_t(n_seg), "column_table"))) return rc;
 
     // temporaries, carved from one arena that is freed on every exit path below
     const int64_t sort_cap = np64 > n_cells ? np64 : int64_t(n_cells);
@@ -686,7 +713,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
             const size_t i4 = sizeof(int32_t);
             const size_t sort_b = Arena::piece(size_t(sort_cap) * i4);
             const size_t cells1_b = Arena::piece((size_t(n_cells) + 1) * i4);
-            const size_t combo1_b = Arena::piece((size_t(n_combo) + 1) * i4);
+            const size_t combo1_b = Arena::piece((size_t(n_seg) + 1) * i4);
             arena.cap = Arena::piece(size_t(g.n_cams) * 16 * sizeof(double)) + 4 * sort_b +
                         Arena::piece(size_t(sort_tiles_cap) * 256 * i4) + Arena::piece(12 * i4) +
                         Arena::piece(size_t(scan_sums_needed(sort_cap + 1)) * i4) +
@@ -694,6 +721,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
                         Arena::piece(size_t(n_cells) * i4) +          // pos_of_cell
                         2 * combo1_b +                 // combo_flag, head_scan
                         Arena::piece(size_t(n_combo) * i4) +          // combo_range
+                        2 * Arena::piece(size_t(n_seg) * i4) +        // seg_cell, seg_range
                         Arena::piece((size_t(np) + 1) * i4);          // run_scan
             if ((rc2 = dev_alloc(&arena.base, arena.cap, "plan temporaries"))) return rc2;
         }
@@ -704,7 +732,8 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         if ((rc2 = arena.take(&vals_a, size_t(sort_cap), "sort values"))) return rc2;
         if ((rc2 = arena.take(&vals_b, size_t(sort_cap), "sort values"))) return rc2;
         if ((rc2 = arena.take(&hist, size_t(sort_tiles_cap) * 256, "radix histogram"))) return rc2;
-        // [0..1] cell stats, [3] scan totals, [4..5] class counters, [8..11] gathered counts
+        // [0..1] cell stats, [3] scan totals, [4..5] class counters, [6] most
+        // segments of a combo, [7] their kept points, [8..11] gathered counts
         if ((rc2 = arena.take(&small, 12, "plan counters"))) return rc2;
         // the longest scan is over sort_cap + 1 elements (radix histograms
         // are shorter)
@@ -755,7 +784,10 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         if ((rc2 = dev_alloc(&plan->combo_cells, size_t(n_combo), "combo cells"))) return rc2;
         combo_cell = plan->combo_cells;
         if ((rc2 = arena.take(&combo_range, size_t(n_combo), "combo ranges"))) return rc2;
-        if ((rc2 = arena.take(&combo_flag, size_t(n_combo) + 1, "combo flags"))) return rc2;
+        if ((rc2 = arena.take(&combo_flag, size_t(n_seg) + 1, "segment flags"))) return rc2;
+        int32_t *seg_cell = nullptr, *seg_range = nullptr;
+        if ((rc2 = arena.take(&seg_cell, size_t(n_seg), "segment cells"))) return rc2;
+        if ((rc2 = arena.take(&seg_range, size_t(n_seg), "segment rows"))) return rc2;
         if ((rc2 = arena.take(&cell_generic, size_t(n_cells), "cell classes"))) return rc2;
         if ((rc2 = arena.take(&cell_ncombo, size_t(n_cells), "cell combos"))) return rc2;
         fill(cell_generic, n_cells, 0);
@@ -771,29 +803,36 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         ca.combo_range = combo_range;
         ca.cell_generic = cell_generic;
         ca.cell_ncombo = cell_ncombo;
+        ca.planes = planes;
+        ca.seg_cell = seg_cell;
+        ca.seg_range = seg_range;
+        ca.max_seg = small + 6;
+        ca.served_pts = small + 7;
         hipLaunchKernelGGL(k_combo_walk, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream, ca);
-        int32_t stats[2], counters[2], n_gen = 0, n_empty = 0, kept = 0, n_part = 0;
+        int32_t stats[4], counters[2], n_gen = 0, n_empty = 0, kept = 0, n_part = 0;
         auto classify = [&]() -> int {
             fill(flag_a, int64_t(n_cells) + 1, 0);
             fill(flag_b, int64_t(n_cells) + 1, 0);
-            fill(combo_flag, n_combo + 1, 0);
+            fill(combo_flag, n_seg_act + 1, 0);
             fill(small + 4, 2, 0);
             hipLaunchKernelGGL(k_cell_class, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream, ca,
                                plan->cell_start, n_cells, flag_a, flag_b, small + 4);
-            hipLaunchKernelGGL(k_combo_table, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream,
+            hipLaunchKernelGGL(k_combo_table, dim3(blocks_for(n_seg_act)), dim3(kBlock), 0, stream,
                                ca, plan->column_table, combo_flag);
             device_scan(flag_a, int64_t(n_cells) + 1, small + 3, scan_sums, stream);       // generic cells
             device_scan(flag_b, int64_t(n_cells) + 1, small + 3, scan_sums, stream);       // empty cells
-            device_scan(combo_flag, n_combo + 1, small + 3, scan_sums, stream);   // combos of multi cells
+            device_scan(combo_flag, n_seg_act + 1, small + 3, scan_sums, stream);   // segments of multi cells
             BEVPOOL_HIP(hipGetLastError());
             hipLaunchKernelGGL(k_gather4, dim3(1), dim3(1), 0, stream, small + 8, flag_a + n_cells,
-                               flag_b + n_cells, plan->cell_start + n_cells, combo_flag + n_combo);
+                               flag_b + n_cells, plan->cell_start + n_cells, combo_flag + n_seg_act);
             BEVPOOL_HIP(hipGetLastError());
             int32_t h[12];
             BEVPOOL_HIP(hipMemcpyAsync(h, small, sizeof(h), hipMemcpyDeviceToHost, stream));
             BEVPOOL_HIP(hipStreamSynchronize(stream));
             stats[0] = h[0];
             stats[1] = h[1];
+            stats[2] = h[6];       // most segments of a column-served combo
+            stats[3] = h[7];       // kept points of column-served combos
             counters[0] = h[4];
             counters[1] = h[5];
             n_gen = h[8];          // generic cells
@@ -803,6 +842,18 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
             return BEVPOOL_OK;
         };
         if ((rc2 = classify())) return rc2;
+        if (ca.planes > 1 && int64_t(stats[3]) * 2 < int64_t(kept)) {
+            // segments serve under half of the kept points (a strongly tilted
+            // rig): the extra passes would cost more than they save, so the
+            // partition is rebuilt with whole combos only
+            ca.planes = 1;
+            n_seg_act = n_combo;
+            fill(cell_generic, n_cells, 0);
+            fill(cell_ncombo, n_cells, 0);
+            fill(small + 6, 2, 0);
+            hipLaunchKernelGGL(k_combo_walk, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream, ca);
+            if ((rc2 = classify())) return rc2;
+        }
         if (n_part > n_empty) {
             hipLaunchKernelGGL(k_demote_multi, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream, ca,
                                n_cells);
@@ -816,6 +867,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         plan->n_generic = n_gen;
         plan->n_empty = n_empty;
         plan->n_partials = n_part;
+        plan->n_planes = stats[2] > 0 ? stats[2] : 1;
 
         // cells without points, ascending
         if ((rc2 = dev_alloc(&plan->empty_cells, size_t(n_empty), "empty_cells"))) return rc2;
@@ -827,8 +879,8 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         if ((rc2 = arena.take(&head_scan, size_t(n_part) + 1, "multi heads"))) return rc2;
         fill(head_scan, int64_t(n_part) + 1, 0);
         if (n_part > 0) {
-            hipLaunchKernelGGL(k_multi_compact, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream,
-                               combo_cell, combo_flag, int32_t(n_combo), keys_a, vals_a);
+            hipLaunchKernelGGL(k_multi_compact, dim3(blocks_for(n_seg_act)), dim3(kBlock), 0, stream,
+                               seg_cell, combo_flag, int32_t(n_seg_act), keys_a, vals_a);
             if ((rc2 = radix_sort(keys_a, vals_a, n_part, bits_for(n_cells)))) return rc2;
             hipLaunchKernelGGL(k_multi_slots, dim3(blocks_for(n_part)), dim3(kBlock), 0, stream,
                                keys_a, vals_a, n_part, plan->empty_cells, plan->column_table,

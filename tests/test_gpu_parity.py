@@ -89,6 +89,8 @@ def _one_cell_rig():
 RIGS = {
     "tiny": wl.tiny_rig, "tiny_identity": wl.identity_rig, "nuscenes": wl.ring_rig,
     "nuscenes_tilted": lambda: wl.tilt_rig(wl.ring_rig()), "highres": lambda: wl.ring_rig(2),
+    # a calibration-sized tilt: combos split into row segments, one pass each
+    "nuscenes_tilt1": lambda: wl.tilt_rig(wl.ring_rig(), 1.0, 0.5),
     "anisotropic": _anisotropic_rig, "coarse": _coarse_rig, "coarse_tilted": _coarse_tilted_rig,
     "empty": _empty_rig,
     "odd": lambda: _odd_rig(False), "odd_tilted": lambda: _odd_rig(True),
@@ -233,7 +235,7 @@ def test_forward_edge_rigs(torch_cuda, pkg, oracle_lib, oracle_plans, name):
             assert plan.info.n_generic > 0
 
 
-@pytest.mark.parametrize("rig_name", ["nuscenes", "nuscenes_tilted"])
+@pytest.mark.parametrize("rig_name", ["nuscenes", "nuscenes_tilted", "nuscenes_tilt1"])
 @pytest.mark.parametrize("channels", [1, 3, 5, 12, 17, 33, 64, 72, 81, 128, 160, 192, 260])
 def test_forward_channel_counts(torch_cuda, pkg, oracle_lib, oracle_plans, channels, rig_name):
     """Every lane-chunk count (1..5 channels per lane of a 16-lane group),
@@ -356,7 +358,8 @@ def test_plan_reuse_and_shape_checks(torch_cuda, pkg):
     assert (plan.forward(P, F) == 0).all()
 
 
-@pytest.mark.parametrize("name", ["nuscenes", "nuscenes_tilted", "coarse", "anisotropic", "tiny"])
+@pytest.mark.parametrize("name", ["nuscenes", "nuscenes_tilted", "nuscenes_tilt1", "coarse",
+                                  "anisotropic", "tiny"])
 def test_plan_partition_counts(pkg, oracle_plans, name):
     """Every cell is column-served, generic or empty; the level rig has no
     generic cell at all."""
@@ -368,6 +371,11 @@ def test_plan_partition_counts(pkg, oracle_plans, name):
     assert info.n_empty == int((counts == 0).sum())
     assert info.n_runs >= info.n_generic
     assert info.n_partials <= info.n_empty
+    if name == "nuscenes_tilt1":
+        # every combo's kept rows fall into at most four segments of one
+        # cell each, so the column items serve every cell (whole combos
+        # alone would leave most cells generic)
+        assert info.n_generic == 0 and info.n_column == int((counts > 0).sum())
     if name == "nuscenes":
         # a level rig: every combo is clean, so the partial slots are the
         # combos of cells whose kept points come from two or more (n, d, w)

@@ -52,6 +52,7 @@ RIGS = {
     "tiny": wl.tiny_rig,
     "nuscenes": wl.ring_rig,                                   # column items + combine
     "nuscenes_tilted": lambda: wl.tilt_rig(wl.ring_rig()),     # generic cells, light and heavy
+    "nuscenes_tilt1": lambda: wl.tilt_rig(wl.ring_rig(), 1.0, 0.5),   # row segments, several passes
     "coarse": lambda: _coarse(wl.ring_rig()),                  # many slots per cell
     "coarse_tilted": lambda: _coarse(wl.tilt_rig(wl.ring_rig())),
     "empty": lambda: dataclasses.replace(wl.tiny_rig(), x_min=100.0),
@@ -88,7 +89,8 @@ def _check_reduce(got, ref, n, mode):
 
 @pytest.mark.parametrize("mode", ["mean", "max"])
 @pytest.mark.parametrize("name,C", [("tiny", 8), ("nuscenes", 80), ("nuscenes_tilted", 80),
-                                    ("coarse", 16), ("coarse_tilted", 16), ("empty", 8)])
+                                    ("nuscenes_tilt1", 80), ("coarse", 16), ("coarse_tilted", 16),
+                                    ("empty", 8)])
 def test_reduce_matches_oracle(torch_cuda, pkg, oracle_lib, name, C, mode):
     _say(f"[reduce] {name} C={C} {mode}")
     torch = torch_cuda
