@@ -245,16 +245,12 @@ typedef struct {
     int32_t n_nonempty;   /* cells with at least one point */
     int32_t max_per_cell; /* largest interval */
     int32_t n_cams, n_depth, feat_h, feat_w, nx, ny;
-    int32_t n_column;     /* swept cells: fed by consecutive pixel columns of one
-                             camera at one depth bin (the forward's matrix-core sweep) */
-    int32_t n_generic;    /* other cells with points (gathered point by point) */
+    int32_t n_column;     /* cells fed by one (camera, depth bin, pixel column) */
+    int32_t n_generic;    /* other cells with points */
     int32_t n_empty;      /* cells without points */
     int32_t n_runs;       /* gather runs of the generic cells */
-    int32_t n_multi;      /* swept cells fed by more than one pixel column */
-    int32_t sweep_ok;     /* 1 when the camera width fits a sweep workgroup (feat_w up
-                             to 183 columns), else 0 and every cell with points is generic */
-    int32_t n_combo_cells; /* generic cells whose points all lie in clean combos (e.g.
-                             cells that two cameras see), gathered combo by combo */
+    int32_t n_partials;   /* partial-sum slots of cells fed by several combos */
+    int32_t n_multi;      /* cells with partial-sum slots */
 } bevpool_plan_info;
 
 /* Fill *info. Host only, no device work. Errors: INVALID_ARG. */

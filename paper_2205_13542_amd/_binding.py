@@ -57,8 +57,7 @@ class bevpool_plan_info(ctypes.Structure):
         ("nx", ctypes.c_int32), ("ny", ctypes.c_int32),
         ("n_column", ctypes.c_int32), ("n_generic", ctypes.c_int32),
         ("n_empty", ctypes.c_int32), ("n_runs", ctypes.c_int32),
-        ("n_multi", ctypes.c_int32), ("sweep_ok", ctypes.c_int32),
-        ("n_combo_cells", ctypes.c_int32),
+        ("n_partials", ctypes.c_int32), ("n_multi", ctypes.c_int32),
     ]
 
 

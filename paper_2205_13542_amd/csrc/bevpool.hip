@@ -33,9 +33,10 @@ void free_plan(bevpool_plan_s *plan) {
     (void)hipFree(plan->column_table);
     (void)hipFree(plan->generic_hdr);
     (void)hipFree(plan->generic_runs);
-    (void)hipFree(plan->cc_hdr);
-    (void)hipFree(plan->cc_list);
     (void)hipFree(plan->empty_cells);
+    (void)hipFree(plan->multi_begin);
+    (void)hipFree(plan->multi_cell);
+    (void)hipFree(plan->multi_rows);
     (void)hipFree(plan->combo_cells);
     if (prev >= 0 && prev != plan->device) (void)hipSetDevice(prev);
     plan->magic = 0;
@@ -238,9 +239,8 @@ int bevpool_plan_info_get(const bevpool_plan_t *plan, bevpool_plan_info *info) {
     info->n_generic = plan->n_generic;
     info->n_empty = plan->n_empty;
     info->n_runs = plan->n_runs;
+    info->n_partials = plan->n_partials;
     info->n_multi = plan->n_multi;
-    info->n_combo_cells = plan->n_combo_cells;
-    info->sweep_ok = plan->sweep_ok;
     info->n_cams = plan->geom.n_cams;
     info->n_depth = plan->geom.n_depth;
     info->feat_h = plan->geom.feat_h;

@@ -10,53 +10,45 @@ namespace bevpool {
 
 // Work partition of the forward pass.
 //
-// A frustum point is (camera n, depth bin d, pixel row h, pixel column w). A
-// "combo" is one (n, d, w): a column of H points on one depth plane. A combo
-// is clean when its kept points lie in one cell and their rows form one
-// range h_lo..h_hi-1. A level camera makes every combo clean, since its rows
-// then differ only in height.
+// A frustum point is (camera n, depth bin d, pixel row h, pixel column w).
+// A "combo" is one (n, d, w): a column of H points on one depth plane. A
+// combo is clean when all its kept points lie in one cell and their rows
+// form one range h_lo..h_hi-1. A level camera makes almost every combo
+// clean, since its rows then differ only in height.
 //
-// A cell is "swept" when all its points come from clean combos of one camera
-// and one depth bin, in consecutive pixel columns. On a level camera the
-// points of one depth bin lie on a straight line of the ground plane, so a
-// cell meets that line in one stretch of columns: every cell that only one
-// camera sees is swept. The sum of a swept cell is the sum over its columns
-// of the column sums S[d][w][:] = sum_h P[d][h][w] F[h][w][:], a small dense
-// product per pixel column (depth bins x rows by rows x channels). The
-// forward pass computes these products on the matrix cores, 16 depth bins
-// by 16 channels at a time, walks each depth bin's columns in order and
-// writes a cell when its last column has been added (the column table flags
-// a cell's first and last column). One workgroup covers a camera's full
-// width for 16 depth bins and 16 channels, so every swept cell is finished
-// inside one workgroup; cells that straddle two waves' column ranges are
-// completed through LDS.
-//
-// Every other cell with points (cells seen by two cameras, cells of tilted
-// cameras) is "generic": its points are gathered in runs of consecutive
+// A cell whose points all come from clean combos is "column-served". The
+// forward pass reads each feature row (n, h, w) once per block of
+// kColDepth depth bins and applies it to all of them, with the sums of the
+// block's combos held in registers (column items of kColDepth x
+// kColWidth combos of one camera). A cell fed by one combo is stored from
+// registers. A cell fed by several combos (near the rig a cell spans
+// several pixel columns) gets one partial-sum slot per combo; slot s is the
+// output row of the s-th empty cell, which is free until zeroed. A second
+// kernel adds the slots of each such cell in slot order and then zeroes the
+// borrowed rows. (A grid with fewer empty cells than slots serves these
+// cells generically instead.) Every other cell
+// with points is "generic": its points are gathered in runs of consecutive
 // depth bins of one pixel, by one wave, or by a whole workgroup when it has
-// more than kGenHeavy points. Cells without points are zeroed. All of it runs
-// in one launch, and every output row is written once.
+// more than kGenHeavy points. Cells without points are zeroed by
+// workgroups of their own.
 constexpr int kWaveSize = 64;
 constexpr int kWaves = 4;
-constexpr int kBlock = kWaves * kWaveSize;      // plan kernels
+constexpr int kBlock = kWaves * kWaveSize;      // plan kernels, combine kernel
+constexpr int kFwdWaves = 2;
+constexpr int kFwdBlock = kFwdWaves * kWaveSize;  // forward kernel
+constexpr int kGroupLanes = 16;                 // lanes per pixel column
+constexpr int kColDepth = 8;
+constexpr int kColWidth = kFwdBlock / kGroupLanes;  // 8 columns per item
 constexpr int kGenHeavy = 256;
-constexpr int kSliceChannels = 128;             // channels per generic-cell pass, at most
+constexpr int kSliceChannels = 128;             // channels per forward pass, at most
 constexpr int kBwdSliceChannels = 80;           // channels per backward pass
+constexpr int kCombineInline = 8;               // borrowed rows listed with each multi-combo cell
 
-// Forward workgroups: kSweepWaves waves; a sweep workgroup takes
-// kSweepDepths depth bins x kSweepChannels channels of one camera.
-constexpr int kSweepWaves = 16;
-constexpr int kSweepBlock = kSweepWaves * kWaveSize;
-constexpr int kSweepDepths = 16;                // matrix-core tile: N (depth bins)
-constexpr int kSweepChannels = 16;              // matrix-core tile: M (channels)
-constexpr int kSweepMaxCols = 12;               // pixel columns per wave, at most
-constexpr int kSweepPBuf = 12288;               // floats per LDS buffer of staged probabilities
-
-// Column-table entry of a combo of a swept cell: {cell, h_lo | h_hi << 15 |
-// kColFirst | kColLast}; {-1, 0} for any other combo.
-constexpr uint32_t kColFirst = 1u << 30;        // first column of its cell
-constexpr uint32_t kColLast = 1u << 31;         // last column of its cell
+// Column-table entry: {cell (single-combo cell) or borrowed row of its
+// partial slot (multi), h_lo | h_hi << 16 | kComboMulti}.
+constexpr uint32_t kComboMulti = 1u << 31;
 constexpr int kMaxFeatH = 1 << 14;              // rows must fit the 15-bit fields
+constexpr int kMaxSeg = 4;                      // row segments of a combo served by column items
 
 // Unsigned division by a run-time constant through a multiply-high, after
 // Granlund and Montgomery, "Division by invariant integers using
@@ -87,22 +79,19 @@ struct bevpool_plan_s {
     int64_t n_points, n_kept;
     int32_t n_cells, n_nonempty, max_per_cell;
     int32_t n_column, n_generic, n_generic_heavy, n_runs, n_empty;
-    int32_t n_multi;         // swept cells fed by several combos
-    int32_t n_run_cells;     // generic cells gathered in runs (the first of generic_hdr)
-    int32_t n_combo_cells;   // generic cells gathered combo by combo
-    int32_t n_cc_combos;     // their combos
-    int32_t sweep_ok;        // the camera width fits one sweep workgroup
-    int32_t n_cus;           // compute units of the plan's device
+    int32_t n_partials, n_multi;
     // canonical association (exported)
     int32_t *cell_of_point;  // [n_points]
     int32_t *sorted_point;   // [n_points]: kept ids by (cell, id), then dropped ids
     int32_t *cell_start;     // [n_cells + 1]
     // forward work partition
-    int2 *column_table;      // [N][W][D]: {cell, h_lo | h_hi << 15 | flags} or {-1, 0}
+    int2 *column_table;      // [N][D][W]: {cell or borrowed row or -1, h_lo | h_hi << 16 | flags}
     int32_t *combo_cells;    // [N][D][W]: cell of a clean combo, -1 none kept, -2 not clean
-    int4 *generic_hdr;       // [n_run_cells]: {cell, first run, runs, points}, most points first
-    int4 *cc_hdr;            // [n_combo_cells]: {cell, first combo entry, entries, points}
-    int2 *cc_list;           // [n_cc_combos]: {combo (n * D + d) * W + w, h_lo | h_hi << 15}
+    int32_t *multi_begin;    // [n_multi + 1]: first partial slot of each multi-combo cell
+    int32_t *multi_cell;     // [n_multi]
+    int32_t *multi_rows;     // [n_multi][kCombineInline]: borrowed rows of the first slots, or -1
+    int32_t n_planes;        // segment planes of the column table in use (1 for a level rig)
+    int4 *generic_hdr;       // [n_generic]: {cell, first run, runs, points}, most points first
     int4 *generic_runs;      // [n_runs]: {first point id, pixel, depth bins, 0}
     int32_t *empty_cells;    // [n_empty] cells without points, ascending
 };
@@ -122,10 +111,6 @@ int bevpool_hip_fail(hipError_t err, const char *what);
 // Plan building (plan.hip) and the forward pass (forward.hip).
 // Plan building (plan.hip): from the calibration, or, when host_cells is
 // not null, from a stored cell map (validated by the caller).
-// Rows of staged depth probabilities per pass of a sweep workgroup for a
-// camera W columns wide and H rows high (a multiple of 4), or 0 when a row of
-// that width does not fit (plan.hip).
-int bevpool_sweep_rows(int32_t W, int32_t H);
 int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
                        const int32_t *host_cells, const bevpool_geometry &g,
                        hipStream_t stream, bevpool_plan_s *plan);

@@ -12,8 +12,9 @@
 //   k_cell_start   interval table from the sorted keys
 //   k_cell_stats   non-empty cells and the largest interval
 //   k_combo_walk ... k_generic_runs   work partition of the forward pass:
-//                  clean combos, swept cells and the column table, empty
-//                  cells, generic cells and their runs
+//                  clean combos, the column table, empty cells, the
+//                  partial-sum slots of multi-combo cells, generic cells and
+//                  their runs
 //
 // The geometry is evaluated in IEEE double with the file built without
 // floating-point contraction, in one fixed expression order, so the cell ids
@@ -328,20 +329,22 @@ struct ComboArgs {
     const int32_t *cell_of_point;
     int32_t N, D, H, W;
     int32_t allow_clean;        // 0 when rows do not fit the packed row range
-    int32_t sweep_ok;           // 0 when the camera width does not fit a sweep workgroup
     int32_t *combo_cell;        // [N*D*W]: cell of a clean combo, -1 none kept, -2 not clean
-    int32_t *combo_range;       // [N*D*W]: h_lo | h_hi << 15
+    int32_t *combo_range;       // [N*D*W]: h_lo | h_hi << 16
     int32_t *cell_generic;      // [n_cells]: 1 if a combo that is not clean touches the cell
-    int32_t *cell_ncombo;       // [n_cells]: clean combos in the cell
-    int32_t *cell_key_min;      // [n_cells]: smallest and largest n * D + d of its clean combos
-    int32_t *cell_key_max;
-    int32_t *cell_w_min;        // [n_cells]: first and last pixel column of its clean combos
-    int32_t *cell_w_max;
+    int32_t *cell_ncombo;       // [n_cells]: row segments of column-served combos in the cell
+    int32_t planes;             // segments a combo may have and stay column-served
+    int32_t *seg_cell;          // [planes][N*D*W]: cell of segment s of the combo, or -1
+    int32_t *seg_range;         // [planes][N*D*W]: its rows h_lo | h_hi << 16
+    int32_t *max_seg;           // most segments of a column-served combo
+    int32_t *served_pts;        // kept points of column-served combos
 };
 
-// One thread per combo walks its H rows. A combo whose kept rows are
-// consecutive and lie in one cell is clean; otherwise every cell it touches
-// is generic.
+// One thread per combo walks its H rows and splits the kept ones into
+// segments: maximal runs of consecutive kept rows in one cell. A combo with
+// at most `planes` segments is served by the column items, one segment per
+// pass (a level camera gives every combo one segment: a clean combo);
+// otherwise its cells are generic.
 __global__ __launch_bounds__(kBlock) void k_combo_walk(ComboArgs a) {
     const int64_t x = int64_t(blockIdx.x) * kBlock + threadIdx.x;
     const int64_t n_combo = int64_t(a.N) * a.D * a.W;
@@ -349,39 +352,43 @@ __global__ __launch_bounds__(kBlock) void k_combo_walk(ComboArgs a) {
     const int32_t X = int32_t(x);
     const int32_t w = X % a.W, nd = X / a.W;
     const int64_t base = int64_t(nd) * a.H * a.W + w;
-    int32_t cell = -1, lo = 0, hi = 0, n_seg = 0, cur = -1, first = -1, last = -1;
+    int32_t cell[kMaxSeg], lo[kMaxSeg], hi[kMaxSeg];
+    int32_t n_seg = 0, cur = -1, first = -1, last = -1, kept = 0;
     for (int32_t h = 0; h < a.H; ++h) {
         const int32_t c = a.cell_of_point[base + int64_t(h) * a.W];
         if (c < 0) {
             cur = -1;
             continue;
         }
+        ++kept;
         if (first < 0) first = h;
         last = h;
         if (c != cur) {
-            if (n_seg == 0) {
-                cell = c;
-                lo = h;
+            if (n_seg < a.planes) {
+                cell[n_seg] = c;
+                lo[n_seg] = h;
             }
             ++n_seg;
             cur = c;
         }
-        if (n_seg == 1) hi = h + 1;
+        if (n_seg <= a.planes) hi[n_seg - 1] = h + 1;
     }
+    for (int s = 0; s < a.planes; ++s) a.seg_cell[int64_t(s) * n_combo + X] = -1;
     if (n_seg == 0) {
         a.combo_cell[X] = -1;
         a.combo_range[X] = 0;
         return;
     }
-    if (a.allow_clean && n_seg == 1) {
-        a.combo_cell[X] = cell;
-        a.combo_range[X] = lo | (hi << 15);
-        const int32_t key = nd;   // n * D + d
-        atomicAdd(&a.cell_ncombo[cell], 1);
-        atomicMin(&a.cell_key_min[cell], key);
-        atomicMax(&a.cell_key_max[cell], key);
-        atomicMin(&a.cell_w_min[cell], w);
-        atomicMax(&a.cell_w_max[cell], w);
+    if (a.allow_clean && n_seg <= a.planes) {
+        for (int s = 0; s < n_seg; ++s) {
+            a.seg_cell[int64_t(s) * n_combo + X] = cell[s];
+            a.seg_range[int64_t(s) * n_combo + X] = lo[s] | (hi[s] << 16);
+            atomicAdd(&a.cell_ncombo[cell[s]], 1);
+        }
+        atomicMax(a.max_seg, n_seg);
+        atomicAdd(a.served_pts, kept);
+        a.combo_cell[X] = n_seg == 1 ? cell[0] : -2;
+        a.combo_range[X] = n_seg == 1 ? (lo[0] | (hi[0] << 16)) : 0;
     } else {
         a.combo_cell[X] = -2;
         a.combo_range[X] = 0;
@@ -392,101 +399,101 @@ __global__ __launch_bounds__(kBlock) void k_combo_walk(ComboArgs a) {
     }
 }
 
-// A cell with points is swept when no combo that is not clean touches it and
-// its clean combos share one camera and depth bin and fill consecutive
-// columns (the counts then match the column span).
-__device__ __forceinline__ bool cell_swept(const ComboArgs &a, int32_t c) {
-    return a.sweep_ok && a.cell_generic[c] == 0 && a.cell_ncombo[c] > 0 &&
-           a.cell_key_min[c] == a.cell_key_max[c] &&
-           a.cell_w_max[c] - a.cell_w_min[c] + 1 == a.cell_ncombo[c];
-}
-
-// Per cell: run-cell flag (a generic cell touched by a combo that is not
-// clean: its points are gathered in runs), combo-cell flag (any other
-// generic cell: all its points lie in clean combos, gathered combo by
-// combo), empty flag; counters[0] += swept cells, counters[1] += heavy run
-// cells, counters[2] += swept cells fed by several combos.
+// Per cell: generic flag, empty flag; counters[0] += column-served cells,
+// counters[1] += heavy generic cells.
 __global__ __launch_bounds__(kBlock) void k_cell_class(ComboArgs a, const int32_t *cell_start,
                                                        int32_t n_cells, int32_t *generic_flag,
-                                                       int32_t *empty_flag, int32_t *combo_flag,
-                                                       int32_t *counters) {
+                                                       int32_t *empty_flag, int32_t *counters) {
     const int32_t c = blockIdx.x * kBlock + threadIdx.x;
     if (c >= n_cells) return;
     const int32_t cnt = cell_start[c + 1] - cell_start[c];
-    const bool swept = cnt > 0 && cell_swept(a, c);
-    const bool by_combo = cnt > 0 && !swept && a.cell_generic[c] == 0;
-    const bool by_run = cnt > 0 && !swept && !by_combo;
-    generic_flag[c] = by_run ? 1 : 0;
-    combo_flag[c] = by_combo ? 1 : 0;
+    const bool served = cnt > 0 && a.cell_generic[c] == 0;
+    generic_flag[c] = (cnt > 0 && !served) ? 1 : 0;
     empty_flag[c] = cnt == 0 ? 1 : 0;
-    if (swept) atomicAdd(&counters[0], 1);
-    if (cnt > kGenHeavy && by_run) atomicAdd(&counters[1], 1);
-    if (swept && a.cell_ncombo[c] > 1) atomicAdd(&counters[2], 1);
+    if (served) atomicAdd(&counters[0], 1);
+    if (cnt > kGenHeavy && !served) atomicAdd(&counters[1], 1);
 }
 
-// The combos of combo cells, as (cell, combo) pairs in combo order: flag_x
-// marks them, its scan places them.
-__global__ __launch_bounds__(kBlock) void k_cc_flags(const int32_t *combo_cell, int64_t n_combo,
-                                                     const int32_t *combo_flag, int32_t *flag_x) {
-    const int64_t x = int64_t(blockIdx.x) * kBlock + threadIdx.x;
-    if (x > n_combo) return;
-    const int32_t c = x < n_combo ? combo_cell[x] : -1;
-    flag_x[x] = (c >= 0 && combo_flag[c + 1] != combo_flag[c]) ? 1 : 0;
-}
-
-__global__ __launch_bounds__(kBlock) void k_cc_compact(const int32_t *combo_cell, int64_t n_combo,
-                                                       const int32_t *pos_x, uint32_t *key,
-                                                       int32_t *val) {
-    const int64_t x = int64_t(blockIdx.x) * kBlock + threadIdx.x;
-    if (x >= n_combo || pos_x[x + 1] == pos_x[x]) return;
-    key[pos_x[x]] = uint32_t(combo_cell[x]);
-    val[pos_x[x]] = int32_t(x);
-}
-
-// After the stable sort by cell: entry i is combo val[i] of cell key[i]; the
-// combo list gets {combo, its rows h_lo | h_hi << 15} and each combo cell
-// its header {cell, first entry, entries, points}. Combo cells are listed in
-// cell order, which is the order of their first entries.
-__global__ __launch_bounds__(kBlock) void k_cc_list(const uint32_t *key, const int32_t *val, int32_t n,
-                                                    const int32_t *combo_range, const int32_t *combo_pos,
-                                                    const int32_t *cell_start, int2 *list, int4 *hdr) {
-    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
-    if (i >= n) return;
-    list[i] = make_int2(val[i], combo_range[val[i]]);
-    const uint32_t c = key[i];
-    if (i == 0 || key[i - 1] != c) {
-        int32_t e = i + 1;
-        while (e < n && key[e] == c) ++e;
-        hdr[combo_pos[c]] = make_int4(int32_t(c), i, e - i, cell_start[c + 1] - cell_start[c]);
-    }
-}
-
-// Column-table entries: the combos of swept cells, with their row range and
-// whether they are the first or last column of their cell. The table is
-// kept as [N][W][D], so that the 16 depth bins that a sweep step reads at
-// one column are adjacent.
-__global__ __launch_bounds__(kBlock) void k_combo_table(ComboArgs a, int2 *table) {
+// Column table entries, one plane per segment index, and a flag on each
+// segment of a cell fed by several segments.
+__global__ __launch_bounds__(kBlock) void k_combo_table(ComboArgs a, int2 *table, int32_t *multi_flag) {
     const int64_t t = int64_t(blockIdx.x) * kBlock + threadIdx.x;
-    if (t >= int64_t(a.N) * a.D * a.W) return;
-    const int32_t w_ = int32_t(t % a.W), nd = int32_t(t / a.W);
-    const int32_t n_ = nd / a.D, d_ = nd - n_ * a.D;
-    const int64_t slot = (int64_t(n_) * a.W + w_) * a.D + d_;
-    const int32_t c = a.combo_cell[t];
+    if (t >= int64_t(a.planes) * a.N * a.D * a.W) return;
+    const int32_t c = a.seg_cell[t];
     int2 e = make_int2(-1, 0);
-    if (c >= 0 && cell_swept(a, c)) {
-        const int32_t w = int32_t(t % a.W);
-        uint32_t y = uint32_t(a.combo_range[t]);
-        if (w == a.cell_w_min[c]) y |= kColFirst;
-        if (w == a.cell_w_max[c]) y |= kColLast;
-        e = make_int2(c, int32_t(y));
+    bool multi = false;
+    if (c >= 0 && a.cell_generic[c] == 0) {
+        multi = a.cell_ncombo[c] > 1;
+        e = make_int2(c, a.seg_range[t] | int32_t(multi ? kComboMulti : 0u));
     }
-    table[slot] = e;
+    table[t] = e;
+    multi_flag[t] = multi ? 1 : 0;
+}
+
+// Not enough empty rows to hold the partial sums: cells fed by several
+// combos become generic.
+__global__ __launch_bounds__(kBlock) void k_demote_multi(ComboArgs a, int32_t n_cells) {
+    const int32_t c = blockIdx.x * kBlock + threadIdx.x;
+    if (c < n_cells && a.cell_generic[c] == 0 && a.cell_ncombo[c] > 1) a.cell_generic[c] = 1;
 }
 
 __global__ __launch_bounds__(kBlock) void k_empty_list(const int32_t *empty_pos, int32_t n_cells,
                                                        int32_t *empty_cells) {
     const int32_t c = blockIdx.x * kBlock + threadIdx.x;
     if (c < n_cells && empty_pos[c + 1] != empty_pos[c]) empty_cells[empty_pos[c]] = c;
+}
+
+// Segments of multi-segment cells as (cell, segment) pairs in segment order.
+__global__ __launch_bounds__(kBlock) void k_multi_compact(const int32_t *seg_cell,
+                                                          const int32_t *multi_pos, int32_t n_seg,
+                                                          uint32_t *key, int32_t *val) {
+    const int32_t X = blockIdx.x * kBlock + threadIdx.x;
+    if (X >= n_seg || multi_pos[X + 1] == multi_pos[X]) return;
+    key[multi_pos[X]] = uint32_t(seg_cell[X]);
+    val[multi_pos[X]] = X;
+}
+
+// After the stable sort by cell, position i is the partial-sum slot of combo
+// val[i]: a cell's slots are contiguous and in combo order. Slot i is kept in
+// the BEV row of empty cell i (the output has a row for every cell, and the
+// rows of empty cells are free until they are zeroed), so the table entry of
+// the combo names that row; cell heads are flagged.
+__global__ __launch_bounds__(kBlock) void k_multi_slots(const uint32_t *key, const int32_t *val,
+                                                        int32_t n, const int32_t *empty_cells,
+                                                        int2 *table, int32_t *head_flag) {
+    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+    if (i >= n) return;
+    table[val[i]].x = empty_cells[i];
+    head_flag[i] = (i == 0 || key[i] != key[i - 1]) ? 1 : 0;
+}
+
+__global__ __launch_bounds__(kBlock) void k_multi_cells(const uint32_t *key, const int32_t *head_scan,
+                                                        int32_t n, int32_t *multi_begin,
+                                                        int32_t *multi_cell) {
+    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+    if (i > n) return;
+    if (i == n) {
+        multi_begin[head_scan[n]] = n;
+        return;
+    }
+    if (head_scan[i + 1] != head_scan[i]) {
+        multi_begin[head_scan[i]] = i;
+        multi_cell[head_scan[i]] = int32_t(key[i]);
+    }
+}
+
+// The borrowed rows of the first kCombineInline slots of each multi-combo
+// cell, next to each other, so that the combine kernel finds them with one
+// access (slot i belongs to cell head_scan[i + 1] - 1).
+__global__ __launch_bounds__(kBlock) void k_multi_rows(const int32_t *head_scan,
+                                                       const int32_t *multi_begin, int32_t n,
+                                                       const int32_t *empty_cells,
+                                                       int32_t *multi_rows) {
+    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+    if (i >= n) return;
+    const int32_t k = head_scan[i + 1] - 1;
+    const int32_t u = i - multi_begin[k];
+    if (u < kCombineInline) multi_rows[int64_t(k) * kCombineInline + u] = empty_cells[i];
 }
 
 // Generic cells keyed for a descending sort by point count.
@@ -621,21 +628,6 @@ void device_scan(int32_t *data, int64_t n, int32_t *total, int32_t *sums, hipStr
 
 using namespace bevpool;
 
-// Rows of staged depth probabilities per pass of a sweep workgroup (a
-// multiple of 4, one matrix-core step each), or 0 when a camera row of the
-// given width does not fit the LDS buffer.
-int bevpool_sweep_rows(int32_t W, int32_t H) {
-    // the buffer holds kSweepDepths depth bins of r rows of W values, each
-    // depth bin (r W) | 1 values long; 8 rows when a wave has at most 6
-    // columns (the kernel's two instantiations: 6 columns and 2 steps of 4
-    // rows, or kSweepMaxCols columns and 1 step)
-    (void)H;
-    const auto fits = [&](int r) { return int64_t(kSweepDepths) * ((int64_t(r) * W) | 1) <= kSweepPBuf; };
-    if (W <= kSweepWaves * 6 && fits(8)) return 8;
-    if (W <= kSweepWaves * kSweepMaxCols && fits(4)) return 4;
-    return 0;
-}
-
 int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
                        const int32_t *host_cells, const bevpool_geometry &g, hipStream_t stream,
                        bevpool_plan_s *plan) {
@@ -645,23 +637,19 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
     const int32_t N = g.n_cams, D = g.n_depth, H = g.feat_h, W = g.feat_w;
     const int32_t HW = H * W;
     const int64_t n_combo = int64_t(N) * D * W;
+    // column-table planes: segment indices a combo may use (a segment has a
+    // row of its own, so never more than H)
+    const int32_t planes = H < kMaxSeg ? H : kMaxSeg;
+    const int64_t n_seg = int64_t(planes) * n_combo;   // table entries reserved
+    int64_t n_seg_act = n_seg;                          // entries of the planes in use
     plan->n_points = np64;
     plan->n_cells = n_cells;
-    plan->sweep_ok = (W <= kSweepWaves * kSweepMaxCols && bevpool_sweep_rows(W, H) > 0) ? 1 : 0;
-    {
-        int cus = 0;
-        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, plan->device) !=
-                hipSuccess || cus < 1)
-            cus = 256;
-        plan->n_cus = cus;
-    }
 
     int rc;
     if ((rc = dev_alloc(&plan->cell_of_point, size_t(np), "cell_of_point"))) return rc;
     if ((rc = dev_alloc(&plan->sorted_point, size_t(np), "sorted_point"))) return rc;
     if ((rc = dev_alloc(&plan->cell_start, size_t(n_cells) + 1, "cell_start"))) return rc;
-    if ((rc = dev_alloc(&plan->column_table, size_t(n_combo), "column_table"))) return rc;
-    if ((rc = dev_alloc(&plan->combo_cells, size_t(n_combo), "combo cells"))) return rc;
+    if ((rc = dev_alloc(&plan->column_table, size_t(n_seg), "column_table"))) return rc;
 
     // temporaries, carved from one arena that is freed on every exit path below
     const int64_t sort_cap = np64 > n_cells ? np64 : int64_t(n_cells);
@@ -671,11 +659,9 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
     uint32_t *keys_a = nullptr, *keys_b = nullptr;
     int32_t *vals_a = nullptr, *vals_b = nullptr, *hist = nullptr, *small = nullptr;
     int32_t *scan_sums = nullptr;
-    int32_t *flag_a = nullptr, *flag_b = nullptr, *flag_c = nullptr, *flag_x = nullptr;
-    int32_t *combo_range = nullptr;
-    int32_t *cell_generic = nullptr, *cell_ncombo = nullptr;
-    int32_t *cell_key_min = nullptr, *cell_key_max = nullptr, *cell_w_min = nullptr,
-            *cell_w_max = nullptr;
+    int32_t *flag_a = nullptr, *flag_b = nullptr;
+    int32_t *combo_cell = nullptr, *combo_range = nullptr, *combo_flag = nullptr;
+    int32_t *cell_generic = nullptr, *cell_ncombo = nullptr, *head_scan = nullptr;
     int32_t *run_scan = nullptr, *run_begin = nullptr, *pos_of_cell = nullptr;
     auto cleanup = [&]() { (void)hipFree(arena.base); };
 
@@ -721,18 +707,21 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
     auto run = [&]() -> int {
         int rc2;
         {
-            // upper bounds of every temporary taken below: the kept points at
-            // most the points, the generic cells at most the cells
+            // upper bounds of every temporary taken below: the partial slots
+            // (n_part) are at most the combos, the kept points at most the
+            // points, the generic cells at most the cells
             const size_t i4 = sizeof(int32_t);
             const size_t sort_b = Arena::piece(size_t(sort_cap) * i4);
             const size_t cells1_b = Arena::piece((size_t(n_cells) + 1) * i4);
+            const size_t combo1_b = Arena::piece((size_t(n_seg) + 1) * i4);
             arena.cap = Arena::piece(size_t(g.n_cams) * 16 * sizeof(double)) + 4 * sort_b +
-                        Arena::piece(size_t(sort_tiles_cap) * 256 * i4) + Arena::piece(16 * i4) +
+                        Arena::piece(size_t(sort_tiles_cap) * 256 * i4) + Arena::piece(12 * i4) +
                         Arena::piece(size_t(scan_sums_needed(sort_cap + 1)) * i4) +
-                        10 * cells1_b +  // flags a/b/c, generic, ncombo, key min/max, w min/max, run_begin
-                        Arena::piece((size_t(n_combo) + 1) * i4) +    // flag_x
+                        5 * cells1_b +                 // flag_a, flag_b, cell_generic, cell_ncombo, run_begin
                         Arena::piece(size_t(n_cells) * i4) +          // pos_of_cell
+                        2 * combo1_b +                 // combo_flag, head_scan
                         Arena::piece(size_t(n_combo) * i4) +          // combo_range
+                        2 * Arena::piece(size_t(n_seg) * i4) +        // seg_cell, seg_range
                         Arena::piece((size_t(np) + 1) * i4);          // run_scan
             if ((rc2 = dev_alloc(&arena.base, arena.cap, "plan temporaries"))) return rc2;
         }
@@ -743,9 +732,9 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         if ((rc2 = arena.take(&vals_a, size_t(sort_cap), "sort values"))) return rc2;
         if ((rc2 = arena.take(&vals_b, size_t(sort_cap), "sort values"))) return rc2;
         if ((rc2 = arena.take(&hist, size_t(sort_tiles_cap) * 256, "radix histogram"))) return rc2;
-        // [0..1] cell stats, [3] scan totals, [4..6] class counters, [8..13]
-        // gathered counts
-        if ((rc2 = arena.take(&small, 16, "plan counters"))) return rc2;
+        // [0..1] cell stats, [3] scan totals, [4..5] class counters, [6] most
+        // segments of a combo, [7] their kept points, [8..11] gathered counts
+        if ((rc2 = arena.take(&small, 12, "plan counters"))) return rc2;
         // the longest scan is over sort_cap + 1 elements (radix histograms
         // are shorter)
         if ((rc2 = arena.take(&scan_sums, size_t(scan_sums_needed(sort_cap + 1)), "scan chunk sums")))
@@ -753,7 +742,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         if ((rc2 = arena.take(&flag_a, size_t(n_cells) + 1, "flags"))) return rc2;
         if ((rc2 = arena.take(&flag_b, size_t(n_cells) + 1, "flags"))) return rc2;
 
-        fill(small, 16, 0);
+        fill(small, 12, 0);
         if (host_cells) {
             // a stored association: the cell map as exported, checked by the caller
             BEVPOOL_HIP(hipMemcpyAsync(plan->cell_of_point, host_cells, sizeof(int32_t) * size_t(np),
@@ -790,21 +779,19 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
                            plan->cell_start, n_cells, small);
         BEVPOOL_HIP(hipGetLastError());
 
-        // combos, cell classes and the column table (the combo cells stay
-        // with the plan: the backward pass reads them)
+        // combos, cell classes and the column table
+        // the combo cells stay with the plan (the backward pass reads them)
+        if ((rc2 = dev_alloc(&plan->combo_cells, size_t(n_combo), "combo cells"))) return rc2;
+        combo_cell = plan->combo_cells;
         if ((rc2 = arena.take(&combo_range, size_t(n_combo), "combo ranges"))) return rc2;
+        if ((rc2 = arena.take(&combo_flag, size_t(n_seg) + 1, "segment flags"))) return rc2;
+        int32_t *seg_cell = nullptr, *seg_range = nullptr;
+        if ((rc2 = arena.take(&seg_cell, size_t(n_seg), "segment cells"))) return rc2;
+        if ((rc2 = arena.take(&seg_range, size_t(n_seg), "segment rows"))) return rc2;
         if ((rc2 = arena.take(&cell_generic, size_t(n_cells), "cell classes"))) return rc2;
         if ((rc2 = arena.take(&cell_ncombo, size_t(n_cells), "cell combos"))) return rc2;
-        if ((rc2 = arena.take(&cell_key_min, size_t(n_cells), "cell keys"))) return rc2;
-        if ((rc2 = arena.take(&cell_key_max, size_t(n_cells), "cell keys"))) return rc2;
-        if ((rc2 = arena.take(&cell_w_min, size_t(n_cells), "cell columns"))) return rc2;
-        if ((rc2 = arena.take(&cell_w_max, size_t(n_cells), "cell columns"))) return rc2;
         fill(cell_generic, n_cells, 0);
         fill(cell_ncombo, n_cells, 0);
-        fill(cell_key_min, n_cells, INT32_MAX);
-        fill(cell_key_max, n_cells, -1);
-        fill(cell_w_min, n_cells, INT32_MAX);
-        fill(cell_w_max, n_cells, -1);
         ComboArgs ca;
         ca.cell_of_point = plan->cell_of_point;
         ca.N = N;
@@ -812,76 +799,117 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         ca.H = H;
         ca.W = W;
         ca.allow_clean = H < kMaxFeatH ? 1 : 0;
-        ca.sweep_ok = plan->sweep_ok;
-        ca.combo_cell = plan->combo_cells;
+        ca.combo_cell = combo_cell;
         ca.combo_range = combo_range;
         ca.cell_generic = cell_generic;
         ca.cell_ncombo = cell_ncombo;
-        ca.cell_key_min = cell_key_min;
-        ca.cell_key_max = cell_key_max;
-        ca.cell_w_min = cell_w_min;
-        ca.cell_w_max = cell_w_max;
+        ca.planes = planes;
+        ca.seg_cell = seg_cell;
+        ca.seg_range = seg_range;
+        ca.max_seg = small + 6;
+        ca.served_pts = small + 7;
         hipLaunchKernelGGL(k_combo_walk, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream, ca);
-        if ((rc2 = arena.take(&flag_c, size_t(n_cells) + 1, "flags"))) return rc2;
-        if ((rc2 = arena.take(&flag_x, size_t(n_combo) + 1, "combo flags"))) return rc2;
-        fill(flag_a, int64_t(n_cells) + 1, 0);
-        fill(flag_b, int64_t(n_cells) + 1, 0);
-        fill(flag_c, int64_t(n_cells) + 1, 0);
-        hipLaunchKernelGGL(k_cell_class, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream, ca,
-                           plan->cell_start, n_cells, flag_a, flag_b, flag_c, small + 4);
-        hipLaunchKernelGGL(k_combo_table, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream, ca,
-                           plan->column_table);
-        device_scan(flag_a, int64_t(n_cells) + 1, small + 3, scan_sums, stream);   // run cells
-        device_scan(flag_b, int64_t(n_cells) + 1, small + 3, scan_sums, stream);   // empty cells
-        device_scan(flag_c, int64_t(n_cells) + 1, small + 3, scan_sums, stream);   // combo cells
-        hipLaunchKernelGGL(k_cc_flags, dim3(blocks_for(n_combo + 1)), dim3(kBlock), 0, stream,
-                           plan->combo_cells, n_combo, flag_c, flag_x);
-        device_scan(flag_x, n_combo + 1, small + 3, scan_sums, stream);            // their combos
-        BEVPOOL_HIP(hipGetLastError());
-        hipLaunchKernelGGL(k_gather4, dim3(1), dim3(1), 0, stream, small + 8, flag_a + n_cells,
-                           flag_b + n_cells, plan->cell_start + n_cells, small + 6);
-        hipLaunchKernelGGL(k_gather4, dim3(1), dim3(1), 0, stream, small + 12, flag_c + n_cells,
-                           flag_x + n_combo, small + 12, small + 12);
-        BEVPOOL_HIP(hipGetLastError());
-        int32_t h[16];
-        BEVPOOL_HIP(hipMemcpyAsync(h, small, sizeof(h), hipMemcpyDeviceToHost, stream));
-        BEVPOOL_HIP(hipStreamSynchronize(stream));
-        const int32_t n_gen = h[8], n_empty = h[9], kept = h[10];
-        const int32_t n_cc = h[12], n_cc_combos = h[13];
-        plan->n_nonempty = h[0];
-        plan->max_per_cell = h[1];
-        plan->n_kept = kept;
-        plan->n_column = h[4];
-        plan->n_generic_heavy = h[5];
-        plan->n_multi = h[11];
-        plan->n_generic = n_gen + n_cc;
-        plan->n_run_cells = n_gen;
-        plan->n_combo_cells = n_cc;
-        plan->n_cc_combos = n_cc_combos;
-        plan->n_empty = n_empty;
-
-        // combo cells: their combos grouped by cell (stable: combo order)
-        if ((rc2 = dev_alloc(&plan->cc_hdr, size_t(n_cc), "combo-cell headers"))) return rc2;
-        if ((rc2 = dev_alloc(&plan->cc_list, size_t(n_cc_combos), "combo-cell combos"))) return rc2;
-        if (n_cc_combos > 0) {
-            hipLaunchKernelGGL(k_cc_compact, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream,
-                               plan->combo_cells, n_combo, flag_x, keys_a, vals_a);
+        int32_t stats[4], counters[2], n_gen = 0, n_empty = 0, kept = 0, n_part = 0;
+        auto classify = [&]() -> int {
+            fill(flag_a, int64_t(n_cells) + 1, 0);
+            fill(flag_b, int64_t(n_cells) + 1, 0);
+            fill(combo_flag, n_seg_act + 1, 0);
+            fill(small + 4, 2, 0);
+            hipLaunchKernelGGL(k_cell_class, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream, ca,
+                               plan->cell_start, n_cells, flag_a, flag_b, small + 4);
+            hipLaunchKernelGGL(k_combo_table, dim3(blocks_for(n_seg_act)), dim3(kBlock), 0, stream,
+                               ca, plan->column_table, combo_flag);
+            device_scan(flag_a, int64_t(n_cells) + 1, small + 3, scan_sums, stream);       // generic cells
+            device_scan(flag_b, int64_t(n_cells) + 1, small + 3, scan_sums, stream);       // empty cells
+            device_scan(combo_flag, n_seg_act + 1, small + 3, scan_sums, stream);   // segments of multi cells
             BEVPOOL_HIP(hipGetLastError());
-            if ((rc2 = radix_sort(keys_a, vals_a, n_cc_combos, bits_for(n_cells)))) return rc2;
-            hipLaunchKernelGGL(k_cc_list, dim3(blocks_for(n_cc_combos)), dim3(kBlock), 0, stream,
-                               keys_a, vals_a, n_cc_combos, combo_range, flag_c, plan->cell_start,
-                               plan->cc_list, plan->cc_hdr);
+            hipLaunchKernelGGL(k_gather4, dim3(1), dim3(1), 0, stream, small + 8, flag_a + n_cells,
+                               flag_b + n_cells, plan->cell_start + n_cells, combo_flag + n_seg_act);
             BEVPOOL_HIP(hipGetLastError());
+            int32_t h[12];
+            BEVPOOL_HIP(hipMemcpyAsync(h, small, sizeof(h), hipMemcpyDeviceToHost, stream));
+            BEVPOOL_HIP(hipStreamSynchronize(stream));
+            stats[0] = h[0];
+            stats[1] = h[1];
+            stats[2] = h[6];       // most segments of a column-served combo
+            stats[3] = h[7];       // kept points of column-served combos
+            counters[0] = h[4];
+            counters[1] = h[5];
+            n_gen = h[8];          // generic cells
+            n_empty = h[9];        // empty cells
+            kept = h[10];          // kept points
+            n_part = h[11];        // combos of multi-combo cells (partial slots)
+            return BEVPOOL_OK;
+        };
+        if ((rc2 = classify())) return rc2;
+        if (ca.planes > 1 && int64_t(stats[3]) * 2 < int64_t(kept)) {
+            // segments serve under half of the kept points (a strongly tilted
+            // rig): the extra passes would cost more than they save, so the
+            // partition is rebuilt with whole combos only
+            ca.planes = 1;
+            n_seg_act = n_combo;
+            fill(cell_generic, n_cells, 0);
+            fill(cell_ncombo, n_cells, 0);
+            fill(small + 6, 2, 0);
+            hipLaunchKernelGGL(k_combo_walk, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream, ca);
+            if ((rc2 = classify())) return rc2;
         }
+        if (n_part > n_empty) {
+            hipLaunchKernelGGL(k_demote_multi, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream, ca,
+                               n_cells);
+            if ((rc2 = classify())) return rc2;
+        }
+        plan->n_nonempty = stats[0];
+        plan->max_per_cell = stats[1];
+        plan->n_kept = kept;
+        plan->n_column = counters[0];
+        plan->n_generic_heavy = counters[1];
+        plan->n_generic = n_gen;
+        plan->n_empty = n_empty;
+        plan->n_partials = n_part;
+        plan->n_planes = stats[2] > 0 ? stats[2] : 1;
 
         // cells without points, ascending
         if ((rc2 = dev_alloc(&plan->empty_cells, size_t(n_empty), "empty_cells"))) return rc2;
         hipLaunchKernelGGL(k_empty_list, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream, flag_b,
                            n_cells, plan->empty_cells);
 
+        // partial-sum slots of the multi-combo cells, kept in the first
+        // n_part empty rows
+        if ((rc2 = arena.take(&head_scan, size_t(n_part) + 1, "multi heads"))) return rc2;
+        fill(head_scan, int64_t(n_part) + 1, 0);
+        if (n_part > 0) {
+            hipLaunchKernelGGL(k_multi_compact, dim3(blocks_for(n_seg_act)), dim3(kBlock), 0, stream,
+                               seg_cell, combo_flag, int32_t(n_seg_act), keys_a, vals_a);
+            if ((rc2 = radix_sort(keys_a, vals_a, n_part, bits_for(n_cells)))) return rc2;
+            hipLaunchKernelGGL(k_multi_slots, dim3(blocks_for(n_part)), dim3(kBlock), 0, stream,
+                               keys_a, vals_a, n_part, plan->empty_cells, plan->column_table,
+                               head_scan);
+        }
+        device_scan(head_scan, int64_t(n_part) + 1, small + 3, scan_sums, stream);
+        BEVPOOL_HIP(hipGetLastError());
+        int32_t n_multi;
+        if ((rc2 = to_host(&n_multi, head_scan + n_part))) return rc2;
+        BEVPOOL_HIP(hipStreamSynchronize(stream));
+        plan->n_multi = n_multi;
+        if ((rc2 = dev_alloc(&plan->multi_begin, size_t(n_multi) + 1, "multi_begin"))) return rc2;
+        if ((rc2 = dev_alloc(&plan->multi_cell, size_t(n_multi), "multi_cell"))) return rc2;
+        hipLaunchKernelGGL(k_multi_cells, dim3(blocks_for(int64_t(n_part) + 1)), dim3(kBlock), 0,
+                           stream, keys_a, head_scan, n_part, plan->multi_begin, plan->multi_cell);
+        BEVPOOL_HIP(hipGetLastError());
+        if ((rc2 = dev_alloc(&plan->multi_rows, size_t(n_multi) * kCombineInline, "multi_rows")))
+            return rc2;
+        fill(plan->multi_rows, int64_t(n_multi) * kCombineInline, -1);
+        if (n_part > 0) {
+            hipLaunchKernelGGL(k_multi_rows, dim3(blocks_for(n_part)), dim3(kBlock), 0, stream,
+                               head_scan, plan->multi_begin, n_part, plan->empty_cells,
+                               plan->multi_rows);
+            BEVPOOL_HIP(hipGetLastError());
+        }
+
         // generic cells by descending point count
         if ((rc2 = dev_alloc(&plan->generic_hdr, size_t(n_gen), "generic_hdr"))) return rc2;
-        uint32_t *gen_key = keys_a;   // free again after the interval table
+        uint32_t *gen_key = keys_a;   // free again after k_multi_cells
         int32_t *gen_cell = vals_a;
         hipLaunchKernelGGL(k_compact_generic, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream,
                            plan->cell_start, n_cells, flag_a, plan->max_per_cell, gen_key, gen_cell);
