@@ -145,7 +145,8 @@ BEVPOOL_API int bevpool_plan(const double *intrinsics, const double *extrinsics,
  * A plan is not modified by the forward pass and may be used from several
  * streams at once (with distinct output buffers).
  * Errors: INVALID_ARG (null pointer or a bad plan handle, batch outside
- * 1..65535, channels < 1), UNSUPPORTED_DTYPE, OVERFLOW (one frame's
+ * 1..65535, channels < 1, the current device not the one the plan was
+ * built on), UNSUPPORTED_DTYPE, OVERFLOW (one frame's
  * depth_prob, cam_feat or bev_out reaches 2 GiB), HIP (launch failure).
  */
 BEVPOOL_API int bevpool_forward(const void *depth_prob, const void *cam_feat,
@@ -180,7 +181,8 @@ BEVPOOL_API int bevpool_forward_ex(const void *depth_prob, const void *cam_feat,
                        void *hip_stream);
 
 /*
- * bevpool_forward with kernel-boundary timing, for measurement: start_event
+ * bevpool_forward (the per-frame pooling of Sec. III-B, first paragraph and
+ * "Interval Reduction") with kernel-boundary timing, for measurement: start_event
  * and stop_event (hipEvent_t handles created by the caller; either may be
  * NULL) are recorded by the first and the last kernel dispatch of the
  * forward pass itself, so hipEventElapsedTime(start, stop) is the GPU time
@@ -194,8 +196,8 @@ BEVPOOL_API int bevpool_forward_timed(const void *depth_prob, const void *cam_fe
                           void *hip_stream, void *start_event, void *stop_event);
 
 /*
- * Gradients of bevpool_forward, for training (the paper trains the model
- * end to end; the pooling is bilinear in P and F). For each frame b, with
+ * Gradients of bevpool_forward, for training (the pooling of Sec. III-B is a
+ * layer of a model trained end to end; it is bilinear in P and F). For each frame b, with
  * grad_out = d loss / d bev_out:
  *   grad_depth[b][p] = sum_c cam_feat[b][pixel(p)][c] * grad_out[b][cell(p)][c]
  *                      for a kept point p, 0 for a dropped one;
@@ -212,7 +214,8 @@ BEVPOOL_API int bevpool_forward_timed(const void *depth_prob, const void *cam_fe
  * Asynchronous on hip_stream. Buffers must not overlap. A plan may be used
  * by several backward and forward calls at once on different streams.
  * Errors: INVALID_ARG (null pointer, a bad plan handle, both outputs NULL,
- * batch outside 1..65535, channels < 1), UNSUPPORTED_DTYPE, OVERFLOW (one
+ * batch outside 1..65535, channels < 1, the current device not the plan's),
+ * UNSUPPORTED_DTYPE, OVERFLOW (one
  * frame's tensor reaches 2 GiB), HIP (launch failure).
  */
 BEVPOOL_API int bevpool_backward(const float *grad_out, const void *depth_prob,
@@ -253,13 +256,21 @@ typedef struct {
     int32_t n_multi;      /* cells with partial-sum slots */
 } bevpool_plan_info;
 
-/* Fill *info. Host only, no device work. Errors: INVALID_ARG. */
+/* Fill *info: the sizes of the association ("Precomputation" paragraph of
+ * Sec. III-B) and of the forward's work partition. Host only, no device
+ * work. Errors: INVALID_ARG (null pointer or a bad plan handle). */
 BEVPOOL_API int bevpool_plan_info_get(const bevpool_plan_t *plan, bevpool_plan_info *info);
 
 /*
- * Copy the plan's association to host arrays: cell_of_point [n_points],
- * sorted_point [n_kept] and cell_start [n_cells + 1]. Any of them may be
- * NULL to skip it. Synchronous. Errors: INVALID_ARG, HIP.
+ * Copy the plan's association to host arrays (the "Precomputation"
+ * paragraph of Sec. III-B: every point's grid index, and the points sorted
+ * by that index with their ranks, which "Interval Reduction" turns into
+ * per-cell intervals): cell_of_point [n_points] (-1 for a dropped point),
+ * sorted_point [n_kept] (kept point ids by cell, then id) and cell_start
+ * [n_cells + 1] (cell c's points are sorted_point[cell_start[c] ..
+ * cell_start[c+1]-1]). Any of them may be NULL to skip it; the caller owns
+ * the host arrays. Synchronous (copies from the plan's device).
+ * Errors: INVALID_ARG (bad plan handle), HIP (copy failure).
  */
 BEVPOOL_API int bevpool_plan_export(const bevpool_plan_t *plan, int32_t *cell_of_point,
                         int32_t *sorted_point, int32_t *cell_start);

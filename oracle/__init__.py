@@ -75,7 +75,7 @@ class _Geom(ctypes.Structure):
 def build() -> str:
     """Compile the oracle with gcc (always, so a stale build never survives)."""
     tmp = LIB_PATH + ".tmp"
-    cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math",
+    cmd = ["gcc", "-O3", "-std=c11", "-ffp-contract=off", "-fno-fast-math",
            "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"]
     subprocess.run(cmd, check=True)
     os.replace(tmp, LIB_PATH)
@@ -105,6 +105,8 @@ def _load():
     lib.oracle_pool_reduce.restype = None
     lib.oracle_max_threads.argtypes = []
     lib.oracle_max_threads.restype = ctypes.c_int
+    lib.oracle_set_threads.argtypes = [ctypes.c_int]
+    lib.oracle_set_threads.restype = None
     _lib = lib
     return lib
 
@@ -244,3 +246,9 @@ def backward(rig, cell_of_point: np.ndarray, P: np.ndarray, F: np.ndarray, G: np
 
 def max_threads() -> int:
     return int(_load().oracle_max_threads())
+
+
+def set_threads(n: int) -> None:
+    """Thread count of later oracle calls from this thread (results are
+    bitwise the same for any count)."""
+    _load().oracle_set_threads(int(n))

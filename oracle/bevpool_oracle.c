@@ -325,3 +325,13 @@ int oracle_max_threads(void) {
     return 1;
 #endif
 }
+
+/* Threads of later parallel regions started from the calling thread (n >= 1);
+ * every function above gives bitwise the same result for any count. */
+void oracle_set_threads(int n) {
+#ifdef _OPENMP
+    omp_set_num_threads(n > 0 ? n : 1);
+#else
+    (void)n;
+#endif
+}

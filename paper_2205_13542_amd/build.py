@@ -14,6 +14,9 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(HERE, "libbevpool.so")
+# measurement probe for bench.py --floor (not part of the pooling library)
+FLOOR_SOURCE = "floor.hip"
+FLOOR_LIB_PATH = os.path.join(HERE, "libbevpool_floor.so")
 SOURCES = ["bevpool.hip", "plan.hip", "forward.hip", "backward.hip", "layout.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -29,12 +32,28 @@ FLAGS = [
 
 
 def build(verbose: bool = False) -> str:
-    tmp = LIB_PATH + ".tmp"
-    cmd = [HIPCC, *FLAGS, "-I", INCLUDE, "-I", CSRC,
-           *[os.path.join(CSRC, s) for s in SOURCES], "-o", tmp]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
+    """Compile every source to an object in parallel, then link the library."""
+    import concurrent.futures
+    import tempfile
+    compile_flags = [f for f in FLAGS if f != "-shared"]
+    with tempfile.TemporaryDirectory(prefix="bevpool_build_") as tmpdir:
+        objs = [os.path.join(tmpdir, os.path.splitext(s)[0] + ".o") for s in SOURCES]
+        cmds = [[HIPCC, *compile_flags, "-I", INCLUDE, "-I", CSRC, "-c",
+                 os.path.join(CSRC, s), "-o", o] for s, o in zip(SOURCES, objs)]
+        floor_tmp = FLOOR_LIB_PATH + ".tmp"
+        cmds.append([HIPCC, *FLAGS, os.path.join(CSRC, FLOOR_SOURCE), "-o", floor_tmp])
+        if verbose:
+            for c in cmds:
+                print(" ".join(c), flush=True)
+        workers = max(1, min(len(cmds), os.cpu_count() or 1))
+        with concurrent.futures.ThreadPoolExecutor(workers) as ex:
+            for r in ex.map(lambda c: subprocess.run(c, capture_output=True, text=True), cmds):
+                if r.returncode != 0:
+                    raise subprocess.CalledProcessError(r.returncode, r.args, r.stdout, r.stderr)
+        tmp = LIB_PATH + ".tmp"
+        subprocess.run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp],
+                       check=True)
+        os.replace(floor_tmp, FLOOR_LIB_PATH)
     os.replace(tmp, LIB_PATH)
     return LIB_PATH
 

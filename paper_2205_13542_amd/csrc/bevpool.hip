@@ -149,6 +149,18 @@ int bevpool_plan_import(const int32_t *cell_of_point, const bevpool_geometry *ge
 }
 
 namespace {
+// The plan's arrays live on the device it was built on; a call on another
+// device would read that memory through another device's stream.
+int check_device(const bevpool_plan_t *plan) {
+    int cur = -1;
+    BEVPOOL_HIP(hipGetDevice(&cur));
+    if (cur != plan->device)
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG,
+                            "the plan was built on device %d but the current device is %d",
+                            plan->device, cur);
+    return BEVPOOL_OK;
+}
+
 int forward_checked(const void *depth_prob, const void *cam_feat, const bevpool_plan_t *plan,
                     float *bev_out, int64_t out_row_stride, int32_t batch, int32_t channels,
                     int32_t dtype, int32_t reduce, void *hip_stream, void *start_event,
@@ -167,6 +179,8 @@ int forward_checked(const void *depth_prob, const void *cam_feat, const bevpool_
     if (out_row_stride < channels)
         return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "out_row_stride=%lld is below channels=%d",
                             (long long)out_row_stride, channels);
+    const int rc = check_device(plan);
+    if (rc != BEVPOOL_OK) return rc;
     return bevpool_launch_forward(depth_prob, cam_feat, plan, bev_out, out_row_stride, batch,
                                   channels, dtype, reduce, hipStream_t(hip_stream),
                                   hipEvent_t(start_event), hipEvent_t(stop_event));
@@ -208,6 +222,8 @@ int bevpool_backward(const float *grad_out, const void *depth_prob, const void *
                             channels);
     if (dtype != BEVPOOL_F32 && dtype != BEVPOOL_BF16 && dtype != BEVPOOL_F16)
         return bevpool_fail(BEVPOOL_ERR_UNSUPPORTED_DTYPE, "dtype %d is not F32, BF16 or F16", dtype);
+    const int rc = check_device(plan);
+    if (rc != BEVPOOL_OK) return rc;
     return bevpool_launch_backward(grad_out, depth_prob, cam_feat, plan, grad_depth, grad_feat,
                                    batch, channels, dtype, hipStream_t(hip_stream));
 }

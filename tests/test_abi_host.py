@@ -145,3 +145,28 @@ def test_package_fails_loudly_without_library(tmp_path):
             _binding.load(str(tmp_path / "missing.so"))
     finally:
         _binding._lib = saved
+
+
+def _declaration_comments():
+    """(name, comment) for every declared function: the block comment right
+    before its declaration."""
+    text = open(HEADER).read()
+    out = []
+    for m in re.finditer(r"/\*((?:(?!\*/).)*)\*/\s*(?:typedef[^;]*;\s*)?BEVPOOL_API\s+[\w\s\*]+?\b(bevpool_\w+)\s*\(",
+                         text, flags=re.S):
+        out.append((m.group(2), m.group(1)))
+    return out
+
+
+def test_every_operation_cites_its_passage():
+    """Each entry point that computes or stores part of the method names the
+    passage of the paper that defines it; utilities (error text, version,
+    destroy) are exempt."""
+    utilities = {"bevpool_last_error", "bevpool_version", "bevpool_plan_destroy"}
+    found = dict(_declaration_comments())
+    missing = set(_declared_functions()) - set(found)
+    assert not missing, missing
+    for name, comment in found.items():
+        if name in utilities:
+            continue
+        assert re.search(r"Sec\. III|Precomputation|Interval Reduction", comment), name

@@ -53,3 +53,23 @@ def test_committed_traffic_record_is_well_formed():
     entry = rec["workloads"]["nuscenes"]
     assert entry["hbm_bytes_per_launch"] == entry["read_bytes"] + entry["write_bytes"]
     assert os.path.exists(os.path.join(ROOT, entry["summary"]))
+
+
+def test_traffic_hash_covers_every_forward_source(tmp_path):
+    """An edit to any file that shapes the forward's traffic (kernels, device
+    helpers, constants, plan layout, build flags) changes the hash, so a
+    stale counter record is not reported as current."""
+    names = {os.path.basename(p) for p in bench.FORWARD_SOURCES}
+    assert {"forward.hip", "device.h", "internal.h", "plan.hip", "build.py"} <= names
+    copies = []
+    for p in bench.FORWARD_SOURCES:
+        q = tmp_path / os.path.basename(p)
+        q.write_bytes(open(p, "rb").read())
+        copies.append(str(q))
+    base = bench.kernel_hash(copies)
+    for q in copies:
+        orig = open(q, "rb").read()
+        open(q, "wb").write(orig + b" ")
+        assert bench.kernel_hash(copies) != base, q
+        open(q, "wb").write(orig)
+    assert bench.kernel_hash(copies) == base

@@ -358,6 +358,32 @@ def test_plan_reuse_and_shape_checks(torch_cuda, pkg):
     assert (plan.forward(P, F) == 0).all()
 
 
+def test_plan_used_on_another_device_is_rejected(torch_cuda, pkg):
+    """A plan's arrays live on the device it was built on: the forward and the
+    backward refuse to run when the current device differs. One GPU cannot
+    make another device current, so the test marks the plan as built on
+    device 7 (the int after the handle's 32-bit magic), checks the refusal
+    before any launch, and restores the field."""
+    import ctypes
+    torch = torch_cuda
+    plan = pkg.Plan.from_rig(wl.tiny_rig())
+    P = torch.zeros((1, 1, 8, 4, 8), device="cuda")
+    F = torch.zeros((1, 1, 4, 8, 8), device="cuda")
+    G = torch.zeros((1, 16, 16, 8), device="cuda")
+    dev = ctypes.c_int.from_address(plan.handle + 4)
+    assert dev.value == torch.cuda.current_device()
+    dev.value = 7
+    try:
+        with pytest.raises(pkg.BevpoolError, match="device 7"):
+            plan.forward(P, F)
+        with pytest.raises(pkg.BevpoolError, match="device 7"):
+            plan.backward(G, P, F)
+    finally:
+        dev.value = torch.cuda.current_device()
+    assert (plan.forward(P, F) == 0).all()
+    plan.close()
+
+
 @pytest.mark.parametrize("name", ["nuscenes", "nuscenes_tilted", "nuscenes_tilt1", "coarse",
                                   "anisotropic", "tiny"])
 def test_plan_partition_counts(pkg, oracle_plans, name):
