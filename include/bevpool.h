@@ -290,6 +290,35 @@ BEVPOOL_API int bevpool_plan_export(const bevpool_plan_t *plan, int32_t *cell_of
 BEVPOOL_API int bevpool_plan_import(const int32_t *cell_of_point, const bevpool_geometry *geom,
                         void *hip_stream, bevpool_plan_t **out_plan);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * association that bevpool_plan computes and bevpool_plan_export returns,
+ * written into the caller's device buffers with no allocation. Use it where a
+ * calibration changes per frame and a plan cannot be rebuilt.
+ *  intrinsics, extrinsics, geom: as for bevpool_plan (host; read before the
+ *              call returns, so they may be freed at once).
+ *  cell_of_point: device int32 [n_points], overwritten: each point's cell, -1
+ *              for a dropped one.
+ *  sorted_point:  device int32 [n_points], overwritten: the kept point ids by
+ *              (cell, id), then the dropped ids in ascending order.
+ *  cell_start:    device int32 [nx*ny + 1], overwritten: cell c owns
+ *              sorted_point[cell_start[c] .. cell_start[c+1]); cell_start[nx*ny]
+ *              is the kept count.
+ * The results equal bevpool_plan's bit for bit. Limits: at most 2^22
+ * points and 16 cameras. The temporaries live in one fixed device array of
+ * 50 MiB per device, held while the library is loaded and shared by every
+ * call on that device: calls that overlap on one device (two streams, or two
+ * host threads) race and must be serialised by the caller. Asynchronous and
+ * stream-ordered on hip_stream: no host synchronisation, no allocation, no
+ * host-to-device copy. Buffers must not overlap.
+ * Errors: INVALID_ARG (null pointer, a size < 1, a non-finite value, a zero
+ * focal length, more points or cameras than the limits), OVERFLOW, HIP.
+ */
+BEVPOOL_API int bevpool_associate_noalloc(const double *intrinsics, const double *extrinsics,
+                              const bevpool_geometry *geom, int32_t *cell_of_point,
+                              int32_t *sorted_point, int32_t *cell_start, void *hip_stream);
+
 /* Free a plan and its device memory. NULL-safe. The plan must not be in use
  * by work still queued on a stream. */
 BEVPOOL_API void bevpool_plan_destroy(bevpool_plan_t *plan);

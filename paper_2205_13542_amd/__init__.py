@@ -20,7 +20,7 @@ from ._binding import (BEVPOOL_BF16, BEVPOOL_F16, BEVPOOL_F32, BEVPOOL_MAX, BEVP
                        bevpool_forward_timed, bevpool_geometry, bevpool_to_nchw,
                        bevpool_last_error,
                        bevpool_plan, bevpool_plan_destroy, bevpool_plan_export,
-                       bevpool_plan_import,
+                       bevpool_plan_import, bevpool_associate_noalloc,
                        bevpool_plan_info_get, bevpool_version)
 
 __all__ = [
@@ -30,6 +30,7 @@ __all__ = [
     "bevpool_plan_info_get",
     "bevpool_plan_export", "bevpool_plan_import", "bevpool_plan_destroy", "bevpool_last_error", "bevpool_version",
     "bevpool_geometry", "geometry_of", "BEVPOOL_F32", "BEVPOOL_BF16", "BEVPOOL_F16",
+    "bevpool_associate_noalloc", "associate_noalloc",
 ]
 
 _GEOM_FIELDS = [f for f, _ in bevpool_geometry._fields_]
@@ -55,6 +56,25 @@ def _dtype_code(t) -> int:
     if t.dtype not in codes:
         raise BevpoolError(_binding.BEVPOOL_ERR_UNSUPPORTED_DTYPE, f"dtype {t.dtype}")
     return codes[t.dtype]
+
+
+def associate_noalloc(rig, cell_of_point, sorted_point, cell_start, stream=None):
+    """bevpool_associate_noalloc into caller tensors: int32 device tensors of
+    n_points, n_points and nx*ny + 1 elements (contiguous). rig has the
+    bevpool_geometry fields plus intrinsics and extrinsics. Allocates nothing
+    on the device."""
+    torch = _torch()
+    geom = geometry_of(rig)
+    n_points = geom.n_cams * geom.n_depth * geom.feat_h * geom.feat_w
+    for t, n, name in ((cell_of_point, n_points, "cell_of_point"), (sorted_point, n_points, "sorted_point"),
+                       (cell_start, geom.nx * geom.ny + 1, "cell_start")):
+        if t.dtype != torch.int32 or not t.is_cuda or not t.is_contiguous() or t.numel() != n:
+            raise BevpoolError(_binding.BEVPOOL_ERR_SHAPE_MISMATCH,
+                               f"{name} must be a contiguous int32 device tensor of {n} elements")
+    if stream is None:
+        stream = torch.cuda.current_stream(cell_of_point.device)
+    bevpool_associate_noalloc(rig.intrinsics, rig.extrinsics, geom, cell_of_point.data_ptr(),
+                              sorted_point.data_ptr(), cell_start.data_ptr(), stream.cuda_stream)
 
 
 def to_nchw(bev, out=None, stream=None):

@@ -25,7 +25,7 @@ EXPORTED = ("bevpool_plan", "bevpool_forward", "bevpool_forward_ex", "bevpool_fo
             "bevpool_backward", "bevpool_to_nchw", "bevpool_plan_import",
             "bevpool_plan_info_get",
             "bevpool_plan_export", "bevpool_plan_destroy", "bevpool_last_error",
-            "bevpool_version")
+            "bevpool_version", "bevpool_associate_noalloc")
 
 
 class BevpoolError(RuntimeError):
@@ -98,6 +98,8 @@ def load(path: str = LIB_PATH):
     lib.bevpool_plan_destroy.restype = None
     lib.bevpool_last_error.argtypes = []
     lib.bevpool_last_error.restype = ctypes.c_char_p
+    lib.bevpool_associate_noalloc.argtypes = [dp, dp, ctypes.POINTER(bevpool_geometry), vp, vp, vp, vp]
+    lib.bevpool_associate_noalloc.restype = ctypes.c_int
     lib.bevpool_version.argtypes = []
     lib.bevpool_version.restype = ctypes.c_int32
     _lib = lib
@@ -130,6 +132,20 @@ def bevpool_plan(intrinsics, extrinsics, geom: bevpool_geometry, hip_stream: int
                                ctypes.byref(geom), ctypes.c_void_p(hip_stream),
                                ctypes.byref(out)))
     return int(out.value)
+
+
+def bevpool_associate_noalloc(intrinsics, extrinsics, geom: bevpool_geometry, cell_of_point: int,
+                              sorted_point: int, cell_start: int, hip_stream: int = 0) -> None:
+    """intrinsics / extrinsics: host float64 arrays; the three outputs are
+    device pointers (int32 [n_points], [n_points], [nx*ny + 1])."""
+    import numpy as np
+    intr = np.ascontiguousarray(intrinsics, dtype=np.float64).reshape(-1)
+    extr = np.ascontiguousarray(extrinsics, dtype=np.float64).reshape(-1)
+    dp = ctypes.POINTER(ctypes.c_double)
+    _check(load().bevpool_associate_noalloc(intr.ctypes.data_as(dp), extr.ctypes.data_as(dp),
+                                            ctypes.byref(geom), ctypes.c_void_p(cell_of_point),
+                                            ctypes.c_void_p(sorted_point), ctypes.c_void_p(cell_start),
+                                            ctypes.c_void_p(hip_stream)))
 
 
 def bevpool_plan_import(cell_of_point, geom: bevpool_geometry, hip_stream: int = 0) -> int:

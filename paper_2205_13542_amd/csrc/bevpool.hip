@@ -128,6 +128,25 @@ int bevpool_plan(const double *intrinsics, const double *extrinsics, const bevpo
     return make_plan(intrinsics, extrinsics, nullptr, g, hip_stream, out_plan);
 }
 
+int bevpool_associate_noalloc(const double *intrinsics, const double *extrinsics,
+                              const bevpool_geometry *geom, int32_t *cell_of_point,
+                              int32_t *sorted_point, int32_t *cell_start, void *hip_stream) {
+    g_last_error[0] = '\0';
+    if (!intrinsics || !extrinsics || !geom || !cell_of_point || !sorted_point || !cell_start)
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG,
+                            "intrinsics, extrinsics, geom and the three outputs must be non-NULL");
+    const bevpool_geometry &g = *geom;
+    int rc = check_geometry(g);
+    if (rc != BEVPOOL_OK) return rc;
+    if (!finite_all(intrinsics, size_t(4) * g.n_cams) || !finite_all(extrinsics, size_t(12) * g.n_cams))
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "calibration values must be finite");
+    for (int n = 0; n < g.n_cams; ++n)
+        if (intrinsics[4 * n] == 0.0 || intrinsics[4 * n + 1] == 0.0)
+            return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "camera %d has a zero focal length", n);
+    return bevpool_associate_into(intrinsics, extrinsics, g, cell_of_point, sorted_point, cell_start,
+                                  hipStream_t(hip_stream));
+}
+
 int bevpool_plan_import(const int32_t *cell_of_point, const bevpool_geometry *geom,
                         void *hip_stream, bevpool_plan_t **out_plan) {
     g_last_error[0] = '\0';

@@ -119,6 +119,14 @@ int bevpool_launch_backward(const float *G, const void *P, const void *F,
                             int32_t channels, int32_t dtype, hipStream_t stream);
 int bevpool_launch_to_nchw(const float *in, int64_t in_row_stride, float *out, int32_t batch,
                            int32_t ny, int32_t nx, int32_t channels, hipStream_t stream);
+// The association alone into caller buffers, with no allocation (plan.hip):
+// temporaries in a fixed device array of kAssocScratchTotal bytes per device.
+constexpr int64_t kAssocMaxPoints = int64_t(1) << 22;
+constexpr int kAssocMaxCams = 16;
+constexpr size_t kAssocScratchTotal = 52431616;   // 50 MiB
+int bevpool_associate_into(const double *intrinsics, const double *extrinsics,
+                           const bevpool_geometry &g, int32_t *cell_of_point,
+                           int32_t *sorted_point, int32_t *cell_start, hipStream_t stream);
 int bevpool_launch_forward(const void *P, const void *F, const bevpool_plan_s *plan,
                            float *out, int64_t ldo, int32_t batch, int32_t channels,
                            int32_t dtype, int32_t reduce, hipStream_t stream,

@@ -23,6 +23,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <utility>
 
 #include "internal.h"
@@ -954,4 +955,136 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
     if (rc != BEVPOOL_OK) (void)hipStreamSynchronize(stream);
     cleanup();
     return rc;
+}
+
+// ---------------------------------------------------------------- association without allocation
+//
+// bevpool_associate_noalloc: the association of the "Precomputation"
+// paragraph (every point's cell, the points sorted by cell, the interval
+// table) into caller buffers, for callers that cannot allocate. Its
+// temporaries (the calibration, the radix sort's second key and value
+// arrays, histograms, counters, scan sums) live in one file-scope device
+// array of fixed size, which each device holds while the library is loaded.
+// Host code never uses the array's name as an address: the device address
+// comes from hipGetSymbolAddress, once per device, with that device current.
+namespace bevpool {
+namespace {
+
+constexpr size_t scratch_piece(size_t b) { return (b + 255) & ~size_t(255); }
+constexpr int64_t kAssocTiles = (kAssocMaxPoints + kSortTile - 1) / kSortTile;
+constexpr int64_t kAssocSums = (kAssocTiles * 256 + kScanChunk - 1) / kScanChunk;
+constexpr size_t kOffCalib = 0;
+constexpr size_t kOffKeysA = kOffCalib + scratch_piece(size_t(kAssocMaxCams) * 16 * sizeof(double));
+constexpr size_t kOffKeysB = kOffKeysA + scratch_piece(size_t(kAssocMaxPoints) * 4);
+constexpr size_t kOffValsB = kOffKeysB + scratch_piece(size_t(kAssocMaxPoints) * 4);
+constexpr size_t kOffHist = kOffValsB + scratch_piece(size_t(kAssocMaxPoints) * 4);
+constexpr size_t kOffSmall = kOffHist + scratch_piece(size_t(kAssocTiles) * 256 * 4);
+constexpr size_t kOffSums = kOffSmall + scratch_piece(16 * 4);
+constexpr size_t kAssocScratchBytes = kOffSums + scratch_piece(size_t(kAssocSums) * 4);
+static_assert(kAssocScratchBytes == kAssocScratchTotal, "scratch size stated in internal.h");
+
+static __device__ __align__(256) char noalloc_scratch[kAssocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+char *g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch (looked up on first use).
+int scratch_of_device(int dev, char **out) {
+    if (dev < 0 || dev >= kMaxDevices)
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "device %d is beyond the %d supported", dev,
+                            kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        BEVPOOL_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(noalloc_scratch)));
+        if (!p) return bevpool_fail(BEVPOOL_ERR_HIP, "no device address for the scratch array");
+        g_scratch_ptr[dev] = static_cast<char *>(p);
+    }
+    *out = g_scratch_ptr[dev];
+    return BEVPOOL_OK;
+}
+
+// The calibration travels in the kernel arguments, so the call reads the
+// caller's host arrays before it returns and copies nothing from host memory.
+struct CalibArgs {
+    double v[kAssocMaxCams * 16];   // [N][4] intrinsics, then [N][12] extrinsics
+    int32_t n;                      // values used
+};
+__global__ void k_store_calib(CalibArgs a, double *dst) {
+    for (int i = threadIdx.x; i < a.n; i += blockDim.x) dst[i] = a.v[i];
+}
+
+}  // namespace
+}  // namespace bevpool
+
+int bevpool_associate_into(const double *intrinsics, const double *extrinsics,
+                           const bevpool_geometry &g, int32_t *cell_of_point,
+                           int32_t *sorted_point, int32_t *cell_start, hipStream_t stream) {
+    using namespace bevpool;
+    const int64_t np64 = int64_t(g.n_cams) * g.n_depth * g.feat_h * g.feat_w;
+    if (np64 > kAssocMaxPoints || g.n_cams > kAssocMaxCams)
+        return bevpool_fail(BEVPOOL_ERR_INVALID_ARG,
+                            "%lld points on %d cameras exceed the no-allocation maximum of %lld points "
+                            "on %d cameras", (long long)np64, g.n_cams, (long long)kAssocMaxPoints,
+                            kAssocMaxCams);
+    int dev = -1;
+    BEVPOOL_HIP(hipGetDevice(&dev));
+    char *base = nullptr;
+    int rc = scratch_of_device(dev, &base);
+    if (rc != BEVPOOL_OK) return rc;
+    double *calib = reinterpret_cast<double *>(base + kOffCalib);
+    uint32_t *keys_a = reinterpret_cast<uint32_t *>(base + kOffKeysA);
+    uint32_t *keys_b = reinterpret_cast<uint32_t *>(base + kOffKeysB);
+    int32_t *vals_b = reinterpret_cast<int32_t *>(base + kOffValsB);
+    int32_t *hist = reinterpret_cast<int32_t *>(base + kOffHist);
+    int32_t *small = reinterpret_cast<int32_t *>(base + kOffSmall);
+    int32_t *sums = reinterpret_cast<int32_t *>(base + kOffSums);
+    const int32_t np = int32_t(np64), n_cells = g.nx * g.ny;
+
+    CalibArgs ca;
+    ca.n = 16 * g.n_cams;
+    for (int i = 0; i < 4 * g.n_cams; ++i) ca.v[i] = intrinsics[i];
+    for (int i = 0; i < 12 * g.n_cams; ++i) ca.v[4 * g.n_cams + i] = extrinsics[i];
+    hipLaunchKernelGGL(k_store_calib, dim3(1), dim3(kBlock), 0, stream, ca, calib);
+    // counters start at zero on every call (the array keeps the last call's contents)
+    hipLaunchKernelGGL(k_fill, dim3(1), dim3(kBlock), 0, stream, small, int64_t(16), 0);
+
+    ProjectArgs pa;
+    pa.intr = calib;
+    pa.extr = calib + 4 * g.n_cams;
+    pa.g = g;
+    pa.div_w = make_fastdiv(uint32_t(g.feat_w));
+    pa.div_h = make_fastdiv(uint32_t(g.feat_h));
+    pa.div_d = make_fastdiv(uint32_t(g.n_depth));
+    pa.n_points = np;
+    pa.n_cells = n_cells;
+    pa.cell_of_point = cell_of_point;
+    pa.keys = keys_a;
+    pa.vals = sorted_point;
+    hipLaunchKernelGGL(k_project, dim3(blocks_for(np)), dim3(kBlock), 0, stream, pa);
+    BEVPOOL_HIP(hipGetLastError());
+
+    // stable LSD radix sort of (cell, point id) on the cell's bits, 8 per pass
+    int bits = 1;
+    while ((int64_t(1) << bits) <= int64_t(n_cells)) ++bits;
+    const int tiles = int((int64_t(np) + kSortTile - 1) / kSortTile);
+    uint32_t *kin = keys_a, *kout = keys_b;
+    int32_t *vin = sorted_point, *vout = vals_b;
+    for (int shift = 0; shift < bits; shift += 8) {
+        hipLaunchKernelGGL(k_radix_hist, dim3(tiles), dim3(kBlock), 0, stream, kin, np, shift, hist);
+        device_scan(hist, int64_t(tiles) * 256, small + 3, sums, stream);
+        hipLaunchKernelGGL(k_radix_scatter, dim3(tiles), dim3(kBlock), 0, stream, kin, vin, np, shift,
+                           hist, kout, vout);
+        BEVPOOL_HIP(hipGetLastError());
+        std::swap(kin, kout);
+        std::swap(vin, vout);
+    }
+    if (vin != sorted_point)
+        BEVPOOL_HIP(hipMemcpyAsync(sorted_point, vin, sizeof(int32_t) * size_t(np),
+                                   hipMemcpyDeviceToDevice, stream));
+    hipLaunchKernelGGL(k_cell_start, dim3(blocks_for(int64_t(np) + 1)), dim3(kBlock), 0, stream, kin,
+                       np, n_cells, cell_start);
+    BEVPOOL_HIP(hipGetLastError());
+    return BEVPOOL_OK;
 }

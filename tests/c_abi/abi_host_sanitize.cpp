@@ -49,6 +49,11 @@ int bevpool_launch_to_nchw(const float *, int64_t, float *, int32_t, int32_t, in
     ++g_launches;
     return BEVPOOL_OK;
 }
+int bevpool_associate_into(const double *, const double *, const bevpool_geometry &, int32_t *,
+                           int32_t *, int32_t *, hipStream_t) {
+    ++g_launches;
+    return BEVPOOL_OK;
+}
 
 // ---------------------------------------------------------------- checks
 #define EXPECT(call, code)                                                                   \
@@ -162,6 +167,21 @@ int main() {
     EXPECT(bevpool_to_nchw(dummy, 4, dummy, 1, 16, 16, 8, nullptr), BEVPOOL_ERR_INVALID_ARG);
     EXPECT(bevpool_to_nchw(nullptr, 8, dummy, 1, 16, 16, 8, nullptr), BEVPOOL_ERR_INVALID_ARG);
     EXPECT(bevpool_to_nchw(dummy, 8, dummy, 1, 0, 16, 8, nullptr), BEVPOOL_ERR_INVALID_ARG);
+
+    // the association without allocation: argument checks before any launch
+    {
+        int32_t *d = reinterpret_cast<int32_t *>(dummy);
+        const int before = g_launches;
+        EXPECT(bevpool_associate_noalloc(intr, extr, &g, d, d, d, nullptr), BEVPOOL_OK);
+        EXPECT(bevpool_associate_noalloc(nullptr, extr, &g, d, d, d, nullptr), BEVPOOL_ERR_INVALID_ARG);
+        EXPECT(bevpool_associate_noalloc(intr, extr, &g, d, nullptr, d, nullptr), BEVPOOL_ERR_INVALID_ARG);
+        bevpool_geometry b = g;
+        b.cell_y = -1.0;
+        EXPECT(bevpool_associate_noalloc(intr, extr, &b, d, d, d, nullptr), BEVPOOL_ERR_INVALID_ARG);
+        const double z[4] = {4.0, 0.0, 4.0, 2.0};
+        EXPECT(bevpool_associate_noalloc(z, extr, &g, d, d, d, nullptr), BEVPOOL_ERR_INVALID_ARG);
+        if (g_launches != before + 1) { printf("FAIL: association launches\n"); return 1; }
+    }
 
     // a message longer than the buffer is cut, not overrun
     {
