@@ -420,16 +420,15 @@ def reduce_bench(args):
     }
     if not args.no_cpu_baseline:
         frames, spent = 0, 0.0
-        cops = [oracle.cell_map(oracle.slab_rig(rig, iz)) for iz in range(nz)]
+        cop = oracle.cell_map(rig, nz)
+        grid = oracle.slab_grid(rig, nz)
         while frames == 0 or (spent < args.cpu_seconds / 2 and frames < 16):
             b = frames % w.batch
             t0 = time.perf_counter()
-            for iz in range(nz):
-                r = oracle.slab_rig(rig, iz)
-                if args.reduce == "sum":
-                    oracle.pool(r, cops[iz], w.P[b:b + 1], w.F[b:b + 1])
-                else:
-                    oracle.pool_reduce(r, cops[iz], w.P[b:b + 1], w.F[b:b + 1], args.reduce)
+            if args.reduce == "sum":
+                oracle.pool(grid, cop, w.P[b:b + 1], w.F[b:b + 1])
+            else:
+                oracle.pool_reduce(grid, cop, w.P[b:b + 1], w.F[b:b + 1], args.reduce)
             spent += time.perf_counter() - t0
             frames += 1
         rec["cpu_baseline"] = {

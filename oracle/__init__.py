@@ -92,6 +92,8 @@ def _load():
     P = ctypes.c_void_p
     lib.oracle_cell_map.argtypes = [P, P, ctypes.POINTER(_Geom), P]
     lib.oracle_cell_map.restype = ctypes.c_int64
+    lib.oracle_cell_map_slabs.argtypes = [P, P, ctypes.POINTER(_Geom), ctypes.c_int32, P]
+    lib.oracle_cell_map_slabs.restype = ctypes.c_int64
     lib.oracle_sort_by_cell.argtypes = [P, ctypes.c_int64, ctypes.c_int32, P, P]
     lib.oracle_sort_by_cell.restype = None
     lib.oracle_pool.argtypes = [P, P, P, ctypes.POINTER(_Geom), ctypes.c_int32,
@@ -122,15 +124,20 @@ def _ptr(a: np.ndarray):
     return a.ctypes.data_as(ctypes.c_void_p)
 
 
-def cell_map(rig) -> np.ndarray:
-    """int32 [N*D*H*W]: cell id of each point in point-id order, -1 if dropped."""
+def cell_map(rig, nz: int = 1) -> np.ndarray:
+    """int32 [N*D*H*W]: cell id of each point in point-id order, -1 if dropped.
+    With nz > 1 the grid has nz stacked z slabs of z_cell each from z_min and
+    the cell id is (iy * nx + ix) * nz + iz (z quantised like x and y)."""
     lib = _load()
     intr = np.ascontiguousarray(rig.intrinsics, dtype=np.float64).reshape(-1)
     extr = np.ascontiguousarray(rig.extrinsics, dtype=np.float64).reshape(-1)
-    assert intr.size == 4 * rig.n_cams and extr.size == 12 * rig.n_cams
+    assert intr.size == 4 * rig.n_cams and extr.size == 12 * rig.n_cams and nz >= 1
     out = np.empty(rig.n_points, dtype=np.int32)
     g = _geom(rig)
-    lib.oracle_cell_map(_ptr(intr), _ptr(extr), ctypes.byref(g), _ptr(out))
+    if nz == 1:
+        lib.oracle_cell_map(_ptr(intr), _ptr(extr), ctypes.byref(g), _ptr(out))
+    else:
+        lib.oracle_cell_map_slabs(_ptr(intr), _ptr(extr), ctypes.byref(g), int(nz), _ptr(out))
     return out
 
 
@@ -202,25 +209,35 @@ def pool_reduce(rig, cell_of_point: np.ndarray, P: np.ndarray, F: np.ndarray, mo
     return out
 
 
-def slab_rig(rig, iz: int):
-    """The rig restricted to z slab iz: [z_min + iz z_cell, z_min + (iz+1) z_cell)."""
-    return dataclasses.replace(rig, z_min=rig.z_min + iz * rig.z_cell)
+def slab_grid(rig, nz: int):
+    """The rig with each BEV row widened to nx * nz cells, so that the cell id
+    (iy * nx + ix) * nz + iz of an nz-slab cell map indexes its pooled rows,
+    and [B][ny][nx * nz][C] reshapes to [B][ny][nx][nz * C]."""
+    return dataclasses.replace(rig, nx=rig.nx * nz)
+
+
+def plan_slabs(rig, nz: int):
+    """(cell_of_point, sorted_point, cell_start) over nz stacked z slabs."""
+    cop = cell_map(rig, nz)
+    sp, cs = sort_by_cell(cop, rig.n_cells * nz)
+    return cop, sp, cs
 
 
 def pool_slabs(rig, nz: int, P: np.ndarray, F: np.ndarray, mode: str = "sum"):
     """Pooling over nz stacked z slabs, flattened along z by concatenating
-    the slabs' channels (Sec. III-B: the features are flattened along the
-    z-axis): out[b][iy][ix][iz * C + c] is the pooled value of slab iz.
+    the slabs' channels (Sec. III-B: the point cloud is quantised on the grid
+    and the features are flattened along the z-axis): z is quantised like x
+    and y, iz = floor((z - z_min) / z_cell) in [0, nz), and
+    out[b][iy][ix][iz * C + c] is the pooled value of slab iz.
     Returns float64 [B][ny][nx][nz * C]."""
-    parts = []
-    for iz in range(nz):
-        r = slab_rig(rig, iz)
-        cop = cell_map(r)
-        if mode == "sum":
-            parts.append(pool(r, cop, P, F, want_f64=True)[1])
-        else:
-            parts.append(pool_reduce(r, cop, P, F, mode))
-    return np.concatenate(parts, axis=-1)
+    cop = cell_map(rig, nz)
+    grid = slab_grid(rig, nz)
+    if mode == "sum":
+        out = pool(grid, cop, P, F, want_f64=True)[1]
+    else:
+        out = pool_reduce(grid, cop, P, F, mode)
+    B, C = out.shape[0], out.shape[-1]
+    return out.reshape(B, rig.ny, rig.nx, nz * C)
 
 
 def backward(rig, cell_of_point: np.ndarray, P: np.ndarray, F: np.ndarray, G: np.ndarray):

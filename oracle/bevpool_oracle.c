@@ -31,8 +31,11 @@
  *   - extrinsics map camera to ego: p_ego = R p_cam + t;
  *   - quantisation uses floor, and the range test is done on the floored
  *     index, so each cell is half-open [min + i*r, min + (i+1)*r);
- *   - one z slab: a point is kept only if floor((z - z_min) / z_cell) == 0;
- *   - cell id = iy * nx + ix; output layout [B][ny][nx][C];
+ *   - z is quantised like x and y: iz = floor((z - z_min) / z_cell); with one
+ *     z slab a point is kept only if iz == 0, with nz slabs if 0 <= iz < nz;
+ *   - cell id = iy * nx + ix; output layout [B][ny][nx][C]; with nz slabs the
+ *     cell id is (iy * nx + ix) * nz + iz, so a [B][ny][nx][nz][C] map is the
+ *     slabs' features concatenated along channels (flattening along z);
  *   - ties in the sort are broken by point id (a stable sort);
  *   - all geometry is IEEE double, evaluated in the fixed order below, with
  *     no fused multiply-add (this file is built with -ffp-contract=off);
@@ -68,8 +71,13 @@ static int64_t n_points_of(const oracle_geometry *g) {
  * extrinsics: [N][12] = row-major [R | t], camera to ego.
  * Returns the number of kept points.
  */
-int64_t oracle_cell_map(const double *intrinsics, const double *extrinsics,
-                        const oracle_geometry *g, int32_t *cell_of_point) {
+/*
+ * Grid index of every frustum point over nz stacked z slabs (nz >= 1):
+ * iz = floor((z - z_min) / z_cell) in [0, nz), cell (iy * nx + ix) * nz + iz.
+ * Returns the number of kept points.
+ */
+int64_t oracle_cell_map_slabs(const double *intrinsics, const double *extrinsics,
+                              const oracle_geometry *g, int32_t nz, int32_t *cell_of_point) {
     int64_t kept = 0;
     int64_t p = 0;
     for (int n = 0; n < g->n_cams; ++n) {
@@ -92,14 +100,14 @@ int64_t oracle_cell_map(const double *intrinsics, const double *extrinsics,
                     const double X = ((E[0] * xc + E[1] * yc) + E[2] * zc) + E[3];
                     const double Y = ((E[4] * xc + E[5] * yc) + E[6] * zc) + E[7];
                     const double Z = ((E[8] * xc + E[9] * yc) + E[10] * zc) + E[11];
-                    /* quantise; keep only points inside the grid and z slab */
+                    /* quantise; keep only points inside the grid and the slabs */
                     const double qx = floor((X - g->x_min) / g->cell_x);
                     const double qy = floor((Y - g->y_min) / g->cell_y);
                     const double qz = floor((Z - g->z_min) / g->z_cell);
                     int32_t cell = -1;
                     if (qx >= 0.0 && qx < (double)g->nx &&
-                        qy >= 0.0 && qy < (double)g->ny && qz == 0.0) {
-                        cell = (int32_t)qy * g->nx + (int32_t)qx;
+                        qy >= 0.0 && qy < (double)g->ny && qz >= 0.0 && qz < (double)nz) {
+                        cell = ((int32_t)qy * g->nx + (int32_t)qx) * nz + (int32_t)qz;
                         ++kept;
                     }
                     cell_of_point[p] = cell;
@@ -108,6 +116,12 @@ int64_t oracle_cell_map(const double *intrinsics, const double *extrinsics,
         }
     }
     return kept;
+}
+
+/* One z slab: a point is kept only if iz == 0; cell id iy * nx + ix. */
+int64_t oracle_cell_map(const double *intrinsics, const double *extrinsics,
+                        const oracle_geometry *g, int32_t *cell_of_point) {
+    return oracle_cell_map_slabs(intrinsics, extrinsics, g, 1, cell_of_point);
 }
 
 /*

@@ -92,11 +92,12 @@ def test_identity_rig_closed_form(oracle_lib):
     assert (counts > 0).sum() == 86 and counts.max() == 18
 
 
-def _linalg_cells(rig):
+def _linalg_cells(rig, nz=1):
     """Cells through a different route: 3x3 intrinsic matrix inverted by
     numpy.linalg, 4x4 homogeneous extrinsic, matrix products. Returns the
     cell ids and a mask of points whose quantised coordinates sit within
-    1e-9 (relative) of a cell edge, where rounding may legitimately differ."""
+    1e-9 (relative) of a cell edge, where rounding may legitimately differ.
+    With nz slabs the cell id is (iy * nx + ix) * nz + iz."""
     N, D, H, W = rig.n_cams, rig.n_depth, rig.feat_h, rig.feat_w
     cells = np.empty(rig.n_points, dtype=np.int64)
     near = np.zeros(rig.n_points, dtype=bool)
@@ -119,8 +120,9 @@ def _linalg_cells(rig):
         fl = np.floor(q)
         frac = np.minimum(q - fl, fl + 1 - q)
         close = (frac < 1e-9 * np.maximum(1.0, np.abs(q))).any(axis=0)
-        keep = (fl[0] >= 0) & (fl[0] < rig.nx) & (fl[1] >= 0) & (fl[1] < rig.ny) & (fl[2] == 0)
-        c = np.where(keep, fl[1] * rig.nx + fl[0], -1).astype(np.int64)
+        keep = ((fl[0] >= 0) & (fl[0] < rig.nx) & (fl[1] >= 0) & (fl[1] < rig.ny) & (fl[2] >= 0)
+                & (fl[2] < nz))
+        c = np.where(keep, (fl[1] * rig.nx + fl[0]) * nz + fl[2], -1).astype(np.int64)
         sl = slice(n * D * H * W, (n + 1) * D * H * W)
         cells[sl] = c.reshape(-1)
         near[sl] = close.reshape(-1)
@@ -479,23 +481,22 @@ def test_min_mean_max_order(oracle_lib):
 
 # ------------------------------------------------------------------ z slab pins
 
-def test_slabs_identity_rig_union():
-    """Identity rig (z = d exactly): slabs of 2 m from z = 0 partition the
-    points of the single 8 m slab [0, 8); every kept point keeps its (x, y)
-    cell, and the slabs' sums add up to the sum over the 8 m slab."""
+def test_slabs_identity_rig_closed_form():
+    """Identity rig (z = d exactly): four 2 m slabs from z = 0. Each kept
+    point keeps the (x, y) cell of the single 8 m slab [0, 8), its slab is
+    floor(d / 2), exactly the points of that 8 m slab are kept, and the
+    slabs' sums add up to the sum over the 8 m slab."""
     import oracle
     w = wl.make("tiny_identity", seed=7)
     base = dataclasses.replace(w.rig, z_min=0.0, z_cell=2.0)
     union = dataclasses.replace(w.rig, z_min=0.0, z_cell=8.0)
     cu = oracle.cell_map(union)
-    hits = np.zeros(base.n_points, dtype=np.int64)
-    for iz in range(4):
-        c = oracle.cell_map(oracle.slab_rig(base, iz))
-        hits += c >= 0
-        assert (c[c >= 0] == cu[c >= 0]).all()
-    assert ((hits == 1) == (cu >= 0)).all() and hits.max() <= 1
+    c4 = oracle.cell_map(base, 4)
     _, k, _, _ = _decode(base, np.arange(base.n_points))
-    assert ((cu >= 0) == (k + 1 < 8)).all()
+    assert ((c4 >= 0) == (cu >= 0)).all() and ((cu >= 0) == (k + 1 < 8)).all()
+    kept = c4 >= 0
+    assert (c4[kept] // 4 == cu[kept]).all()
+    assert (c4[kept] % 4 == (k[kept] + 1) // 2).all()
     cat = oracle.pool_slabs(base, 4, w.P, w.F)
     C = w.channels
     total = sum(cat[..., iz * C:(iz + 1) * C] for iz in range(4))
@@ -506,17 +507,29 @@ def test_slabs_identity_rig_union():
 
 def test_slabs_ring_rig_union():
     """nuScenes-shaped rig, four 4 m slabs from z = -8 m against the 16 m slab
-    [-8, 8): the same partition of the kept points at full size."""
+    [-8, 8): the slab index divides z by 4 m, the union by 16 m (a power-of-
+    two scaling), so the kept points agree exactly, and each keeps its cell."""
     import oracle
     rig = dataclasses.replace(wl.ring_rig(), z_min=-8.0, z_cell=4.0)
     cu = oracle.cell_map(dataclasses.replace(rig, z_cell=16.0))
-    hits = np.zeros(rig.n_points, dtype=np.int64)
-    for iz in range(4):
-        c = oracle.cell_map(oracle.slab_rig(rig, iz))
-        hits += c >= 0
-        assert (c[c >= 0] == cu[c >= 0]).all()
-    assert ((hits == 1) == (cu >= 0)).all()
+    c4 = oracle.cell_map(rig, 4)
+    assert ((c4 >= 0) == (cu >= 0)).all()
+    assert (c4[c4 >= 0] // 4 == cu[cu >= 0]).all()
+    assert len(np.unique(c4[c4 >= 0] % 4)) == 4
     assert 0.2 < (cu >= 0).mean() < 1.0
+
+
+@pytest.mark.parametrize("rigname,nz", [("nuscenes", 4), ("nuscenes_tilted", 3), ("anisotropic", 5)])
+def test_slab_cells_match_homogeneous_matrix_route(oracle_lib, rigname, nz):
+    """The slab index and cell id through the numpy matrix route."""
+    rig = _anisotropic_rig() if rigname == "anisotropic" else wl.WORKLOADS[rigname][0]()
+    rig = dataclasses.replace(rig, z_min=rig.z_min, z_cell=rig.z_cell / nz)
+    cop = oracle_lib.cell_map(rig, nz)
+    ref, near = _linalg_cells(rig, nz)
+    assert near.mean() < 0.15
+    assert (cop[~near] == ref[~near]).all()
+    kept = cop >= 0
+    assert len(np.unique(cop[kept] % nz)) == nz
 
 
 def test_one_slab_is_pool(oracle_lib):
