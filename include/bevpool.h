@@ -118,12 +118,31 @@ BEVPOOL_API int bevpool_plan(const double *intrinsics, const double *extrinsics,
                  bevpool_plan_t **out_plan);
 
 /*
+ * A plan over nz >= 1 stacked z slabs (Sec. III-B, first paragraph: the
+ * lifted points are quantised on the grid and the features flattened along
+ * z). z is quantised like x and y: iz = floor((z - z_min) / z_cell), and a
+ * point is kept when 0 <= iz < nz (geom's z_cell is one slab's height). The
+ * cell id is (iy * nx + ix) * nz + iz, so the plan has nx * ny * nz cells
+ * and a forward map [batch][ny][nx][nz][channels] is the slabs' features
+ * concatenated along channels, [batch][ny][nx][nz * channels], from one
+ * forward call that reads the inputs once. nz = 1 is bevpool_plan.
+ * Arguments, ownership and errors are those of bevpool_plan, plus
+ * INVALID_ARG for nz < 1 and OVERFLOW when nx * ny * nz + 1 does not fit in
+ * int32. bevpool_plan_import rebuilds single-slab plans only.
+ */
+BEVPOOL_API int bevpool_plan_slabs(const double *intrinsics, const double *extrinsics,
+                       const bevpool_geometry *geom, int32_t nz, void *hip_stream,
+                       bevpool_plan_t **out_plan);
+
+/*
  * Pool one batch of frames with a plan (Sec. III-B: lift P x F, sum each
  * cell's points; "Interval Reduction": each cell's sum is written once).
  *
  *  depth_prob: device [batch][N][D][H][W] of dtype.
  *  cam_feat:   device [batch][N][H][W][channels] of dtype.
- *  bev_out:    device float [batch][ny][nx][channels]. Every element is
+ *  bev_out:    device float [batch][n_cells][channels]: [batch][ny][nx][channels]
+ *              for a plan of one z slab, [batch][ny][nx][nz * channels] for
+ *              a plan of nz slabs (bevpool_plan_slabs). Every element is
  *              overwritten, and cells with no kept point are set to 0.
  *  batch in 1..65535, channels >= 1. N, D, H, W, nx and ny come from the
  *  plan; the caller's buffers must have those sizes (the library cannot see
@@ -204,7 +223,7 @@ BEVPOOL_API int bevpool_forward_timed(const void *depth_prob, const void *cam_fe
  *   grad_feat[b][pixel][c] = sum over the pixel's kept points p of
  *                      depth_prob[b][p] * grad_out[b][cell(p)][c]  (0 if none).
  *
- *  grad_out:   device float [batch][ny][nx][channels].
+ *  grad_out:   device float [batch][n_cells][channels] (the forward's map).
  *  depth_prob, cam_feat: the forward's inputs, device, of dtype.
  *  grad_depth: device float [batch][N][D][H][W], overwritten; NULL to skip.
  *  grad_feat:  device float [batch][N][H][W][channels], overwritten; NULL to
@@ -244,7 +263,7 @@ BEVPOOL_API int bevpool_to_nchw(const float *bev_nhwc, int64_t in_row_stride, fl
 typedef struct {
     int64_t n_points;     /* N*D*H*W */
     int64_t n_kept;       /* points inside the grid and the z slab */
-    int32_t n_cells;      /* nx*ny */
+    int32_t n_cells;      /* nx*ny*nz */
     int32_t n_nonempty;   /* cells with at least one point */
     int32_t max_per_cell; /* largest interval */
     int32_t n_cams, n_depth, feat_h, feat_w, nx, ny;
@@ -254,6 +273,7 @@ typedef struct {
     int32_t n_runs;       /* gather runs of the generic cells */
     int32_t n_partials;   /* partial-sum slots of cells fed by several combos */
     int32_t n_multi;      /* cells with partial-sum slots */
+    int32_t nz;           /* stacked z slabs (n_cells = nx * ny * nz) */
 } bevpool_plan_info;
 
 /* Fill *info: the sizes of the association ("Precomputation" paragraph of

@@ -20,7 +20,7 @@ from ._binding import (BEVPOOL_BF16, BEVPOOL_F16, BEVPOOL_F32, BEVPOOL_MAX, BEVP
                        bevpool_forward_timed, bevpool_geometry, bevpool_to_nchw,
                        bevpool_last_error,
                        bevpool_plan, bevpool_plan_destroy, bevpool_plan_export,
-                       bevpool_plan_import, bevpool_associate_noalloc,
+                       bevpool_plan_import, bevpool_associate_noalloc, bevpool_plan_slabs,
                        bevpool_plan_info_get, bevpool_version)
 
 __all__ = [
@@ -30,7 +30,7 @@ __all__ = [
     "bevpool_plan_info_get",
     "bevpool_plan_export", "bevpool_plan_import", "bevpool_plan_destroy", "bevpool_last_error", "bevpool_version",
     "bevpool_geometry", "geometry_of", "BEVPOOL_F32", "BEVPOOL_BF16", "BEVPOOL_F16",
-    "bevpool_associate_noalloc", "associate_noalloc",
+    "bevpool_associate_noalloc", "associate_noalloc", "bevpool_plan_slabs",
 ]
 
 _GEOM_FIELDS = [f for f, _ in bevpool_geometry._fields_]
@@ -107,20 +107,37 @@ class Plan:
     bevpool_geometry fields (e.g. a rig object or a dict).
     """
 
-    def __init__(self, intrinsics, extrinsics, geometry, stream=None):
+    def __init__(self, intrinsics, extrinsics, geometry, stream=None, nz: int = 1):
         torch = _torch()
         _binding.load()
         if stream is None:
             stream = torch.cuda.current_stream()
         self.geometry = geometry_of(geometry)
-        self.handle = bevpool_plan(np.asarray(intrinsics, dtype=np.float64),
-                                   np.asarray(extrinsics, dtype=np.float64),
-                                   self.geometry, stream.cuda_stream)
+        intr = np.asarray(intrinsics, dtype=np.float64)
+        extr = np.asarray(extrinsics, dtype=np.float64)
+        if nz == 1:
+            self.handle = bevpool_plan(intr, extr, self.geometry, stream.cuda_stream)
+        else:
+            self.handle = bevpool_plan_slabs(intr, extr, self.geometry, nz, stream.cuda_stream)
         self.info = bevpool_plan_info_get(self.handle)
 
     @classmethod
-    def from_rig(cls, rig, stream=None) -> "Plan":
-        return cls(rig.intrinsics, rig.extrinsics, rig, stream)
+    def from_rig(cls, rig, stream=None, nz: int = 1) -> "Plan":
+        return cls(rig.intrinsics, rig.extrinsics, rig, stream, nz=nz)
+
+    @property
+    def nz(self) -> int:
+        return int(self.info.nz)
+
+    def _rows(self, t, B, C, what):
+        """A [B][ny][nx][nz * C] map of a plan with nz slabs as the library's
+        rows of C floats, [B][ny][nx * nz][C] (a view; the map is contiguous)."""
+        i = self.info
+        if tuple(t.shape) != (B, i.ny, i.nx, i.nz * C) or not t.is_contiguous():
+            raise BevpoolError(_binding.BEVPOOL_ERR_SHAPE_MISMATCH,
+                               f"{what} must be a contiguous tensor [B][ny][nx][nz * C] for a plan "
+                               f"with {i.nz} z slabs")
+        return t.view(B, i.ny, i.nx * i.nz, C)
 
     @classmethod
     def from_cells(cls, cell_of_point, geometry, stream=None) -> "Plan":
@@ -188,12 +205,16 @@ class Plan:
             raise BevpoolError(_binding.BEVPOOL_ERR_INVALID_ARG, "inputs must be contiguous")
         if reduce not in _REDUCE:
             raise BevpoolError(_binding.BEVPOOL_ERR_INVALID_ARG, f"reduce {reduce!r}")
+        nx = i.nx * i.nz
         if out is None:
-            out = torch.empty((B, i.ny, i.nx, C), dtype=torch.float32, device=cam_feat.device)
+            out = torch.empty((B, i.ny, i.nx, i.nz * C), dtype=torch.float32, device=cam_feat.device)
+        result = out
+        if i.nz > 1:
+            out = self._rows(out, B, C, "out")
         ldo = out.stride(2) if out.dim() == 4 else -1
-        if (tuple(out.shape) != (B, i.ny, i.nx, C) or out.dtype != torch.float32
+        if (tuple(out.shape) != (B, i.ny, nx, C) or out.dtype != torch.float32
                 or not out.is_cuda or out.stride(3) != 1 or ldo < C
-                or out.stride(1) != i.nx * ldo or out.stride(0) != i.ny * i.nx * ldo):
+                or out.stride(1) != nx * ldo or out.stride(0) != i.ny * nx * ldo):
             raise BevpoolError(_binding.BEVPOOL_ERR_SHAPE_MISMATCH,
                                "out must be an fp32 device tensor [B][ny][nx][C] whose rows are "
                                "evenly spaced (contiguous, or a channel slice of a wider map)")
@@ -217,7 +238,7 @@ class Plan:
             bevpool_forward_timed(depth_prob.data_ptr(), cam_feat.data_ptr(), self.handle,
                                   out.data_ptr(), B, C, _dtype_code(cam_feat), stream.cuda_stream,
                                   start.cuda_event, stop.cuda_event)
-        return out
+        return result
 
     def backward(self, grad_out, depth_prob, cam_feat, want_depth=True, want_feat=True,
                  stream=None):
@@ -229,7 +250,7 @@ class Plan:
         B, C = depth_prob.shape[0], cam_feat.shape[-1]
         if (tuple(depth_prob.shape) != (B, i.n_cams, i.n_depth, i.feat_h, i.feat_w)
                 or tuple(cam_feat.shape) != (B, i.n_cams, i.feat_h, i.feat_w, C)
-                or tuple(grad_out.shape) != (B, i.ny, i.nx, C)):
+                or tuple(grad_out.shape) != (B, i.ny, i.nx, i.nz * C)):
             raise BevpoolError(_binding.BEVPOOL_ERR_SHAPE_MISMATCH,
                                "grad_out, depth_prob or cam_feat does not match the plan")
         if cam_feat.dtype != depth_prob.dtype or grad_out.dtype != torch.float32:
@@ -251,49 +272,23 @@ class Plan:
         return gd, gf
 
 
-class SlabPlan:
-    """Several z slabs flattened along z by concatenating their channels
-    (Sec. III-B, first paragraph: the pooled features are flattened along
-    the z-axis). Slab iz is [z_min + iz z_cell, z_min + (iz+1) z_cell) and
-    has a plan of its own; forward writes slab iz's C channels at channel
-    offset iz * C of one [B][ny][nx][nz * C] map (bevpool_forward_ex with
-    out_row_stride = nz * C), one call per slab."""
+class SlabPlan(Plan):
+    """A plan over nz stacked z slabs, flattened along z by concatenating
+    their channels (Sec. III-B, first paragraph: the lifted points are
+    quantised on the grid, z like x and y, and the features flattened along
+    the z-axis). Slab iz is [z_min + iz z_cell, z_min + (iz+1) z_cell);
+    forward returns one [B][ny][nx][nz * C] map, channel iz * C + c being
+    channel c of slab iz, from a single library call that reads P and F
+    once (bevpool_plan_slabs: one association over nx * ny * nz cells)."""
 
     def __init__(self, intrinsics, extrinsics, geometry, nz: int, stream=None):
         if nz < 1:
             raise BevpoolError(_binding.BEVPOOL_ERR_INVALID_ARG, f"nz={nz} must be >= 1")
-        base = geometry_of(geometry)
-        self.nz = nz
-        self.plans = []
-        for iz in range(nz):
-            g = bevpool_geometry(*[getattr(base, f) for f in _GEOM_FIELDS])
-            g.z_min = base.z_min + iz * base.z_cell
-            self.plans.append(Plan(intrinsics, extrinsics, g, stream))
+        super().__init__(intrinsics, extrinsics, geometry, stream, nz=nz)
 
     @classmethod
     def from_rig(cls, rig, nz: int, stream=None) -> "SlabPlan":
         return cls(rig.intrinsics, rig.extrinsics, rig, nz, stream)
-
-    def forward(self, depth_prob, cam_feat, out=None, stream=None, reduce="sum"):
-        """Returns fp32 [B][ny][nx][nz * C]: channel iz * C + c is channel c
-        of slab iz."""
-        torch = _torch()
-        i = self.plans[0].info
-        B, C = depth_prob.shape[0], cam_feat.shape[-1]
-        if out is None:
-            out = torch.empty((B, i.ny, i.nx, self.nz * C), dtype=torch.float32,
-                              device=cam_feat.device)
-        elif tuple(out.shape) != (B, i.ny, i.nx, self.nz * C) or not out.is_contiguous():
-            raise BevpoolError(_binding.BEVPOOL_ERR_SHAPE_MISMATCH,
-                               "out must be a contiguous fp32 tensor [B][ny][nx][nz * C]")
-        for iz, plan in enumerate(self.plans):
-            plan.forward(depth_prob, cam_feat, out=out[..., iz * C:(iz + 1) * C], stream=stream,
-                         reduce=reduce)
-        return out
-
-    def close(self) -> None:
-        for p in self.plans:
-            p.close()
 
 
 def _autograd_function():

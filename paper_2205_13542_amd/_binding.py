@@ -25,7 +25,7 @@ EXPORTED = ("bevpool_plan", "bevpool_forward", "bevpool_forward_ex", "bevpool_fo
             "bevpool_backward", "bevpool_to_nchw", "bevpool_plan_import",
             "bevpool_plan_info_get",
             "bevpool_plan_export", "bevpool_plan_destroy", "bevpool_last_error",
-            "bevpool_version", "bevpool_associate_noalloc")
+            "bevpool_version", "bevpool_associate_noalloc", "bevpool_plan_slabs")
 
 
 class BevpoolError(RuntimeError):
@@ -58,6 +58,7 @@ class bevpool_plan_info(ctypes.Structure):
         ("n_column", ctypes.c_int32), ("n_generic", ctypes.c_int32),
         ("n_empty", ctypes.c_int32), ("n_runs", ctypes.c_int32),
         ("n_partials", ctypes.c_int32), ("n_multi", ctypes.c_int32),
+        ("nz", ctypes.c_int32),
     ]
 
 
@@ -77,6 +78,9 @@ def load(path: str = LIB_PATH):
     lib.bevpool_plan.argtypes = [dp, dp, ctypes.POINTER(bevpool_geometry), vp,
                                  ctypes.POINTER(vp)]
     lib.bevpool_plan.restype = ctypes.c_int
+    lib.bevpool_plan_slabs.argtypes = [dp, dp, ctypes.POINTER(bevpool_geometry), i32, vp,
+                                       ctypes.POINTER(vp)]
+    lib.bevpool_plan_slabs.restype = ctypes.c_int
     lib.bevpool_forward.argtypes = [vp, vp, vp, vp, i32, i32, i32, vp]
     lib.bevpool_forward.restype = ctypes.c_int
     lib.bevpool_forward_ex.argtypes = [vp, vp, vp, vp, ctypes.c_int64, i32, i32, i32, i32, vp]
@@ -131,6 +135,20 @@ def bevpool_plan(intrinsics, extrinsics, geom: bevpool_geometry, hip_stream: int
     _check(load().bevpool_plan(intr.ctypes.data_as(dp), extr.ctypes.data_as(dp),
                                ctypes.byref(geom), ctypes.c_void_p(hip_stream),
                                ctypes.byref(out)))
+    return int(out.value)
+
+
+def bevpool_plan_slabs(intrinsics, extrinsics, geom: bevpool_geometry, nz: int,
+                       hip_stream: int = 0) -> int:
+    """A plan over nz stacked z slabs; returns the plan handle."""
+    import numpy as np
+    intr = np.ascontiguousarray(intrinsics, dtype=np.float64).reshape(-1)
+    extr = np.ascontiguousarray(extrinsics, dtype=np.float64).reshape(-1)
+    out = ctypes.c_void_p()
+    dp = ctypes.POINTER(ctypes.c_double)
+    _check(load().bevpool_plan_slabs(intr.ctypes.data_as(dp), extr.ctypes.data_as(dp),
+                                     ctypes.byref(geom), int(nz), ctypes.c_void_p(hip_stream),
+                                     ctypes.byref(out)))
     return int(out.value)
 
 

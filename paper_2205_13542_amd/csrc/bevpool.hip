@@ -65,7 +65,7 @@ int32_t bevpool_version(void) { return 200; }  // 0.2.0: bevpool_forward_ex
 
 namespace {
 // Sizes and parameters of a geometry (both plan constructors).
-int check_geometry(const bevpool_geometry &g) {
+int check_geometry(const bevpool_geometry &g, int32_t nz = 1) {
     if (g.n_cams < 1 || g.feat_h < 1 || g.feat_w < 1 || g.n_depth < 1 || g.nx < 1 || g.ny < 1)
         return bevpool_fail(BEVPOOL_ERR_INVALID_ARG,
                             "sizes must be >= 1 (n_cams=%d feat_h=%d feat_w=%d n_depth=%d nx=%d ny=%d)",
@@ -81,14 +81,14 @@ int check_geometry(const bevpool_geometry &g) {
     if (np > int64_t(INT32_MAX))
         return bevpool_fail(BEVPOOL_ERR_OVERFLOW, "N*D*H*W = %lld points exceeds int32",
                             (long long)np);
-    if (int64_t(g.nx) * g.ny + 1 > int64_t(INT32_MAX))
-        return bevpool_fail(BEVPOOL_ERR_OVERFLOW, "nx*ny = %lld cells exceeds int32",
-                            (long long)(int64_t(g.nx) * g.ny));
+    if (int64_t(g.nx) * g.ny * nz + 1 > int64_t(INT32_MAX))
+        return bevpool_fail(BEVPOOL_ERR_OVERFLOW, "nx*ny*nz = %lld cells exceeds int32",
+                            (long long)(int64_t(g.nx) * g.ny * nz));
     return BEVPOOL_OK;
 }
 
 int make_plan(const double *intrinsics, const double *extrinsics, const int32_t *host_cells,
-              const bevpool_geometry &g, void *hip_stream, bevpool_plan_t **out_plan) {
+              const bevpool_geometry &g, int32_t nz, void *hip_stream, bevpool_plan_t **out_plan) {
     bevpool_plan_s *plan = new (std::nothrow) bevpool_plan_s();
     if (!plan) return bevpool_fail(BEVPOOL_ERR_OOM, "host allocation of the plan failed");
     memset(plan, 0, sizeof(*plan));
@@ -99,7 +99,8 @@ int make_plan(const double *intrinsics, const double *extrinsics, const int32_t 
         delete plan;
         return bevpool_hip_fail(e, "hipGetDevice");
     }
-    const int rc = bevpool_build_plan(intrinsics, extrinsics, host_cells, g,
+    plan->nz = nz;
+    const int rc = bevpool_build_plan(intrinsics, extrinsics, host_cells, g, nz,
                                       hipStream_t(hip_stream), plan);
     if (rc != BEVPOOL_OK) {
         free_plan(plan);
@@ -110,22 +111,29 @@ int make_plan(const double *intrinsics, const double *extrinsics, const int32_t 
 }
 }  // namespace
 
-int bevpool_plan(const double *intrinsics, const double *extrinsics, const bevpool_geometry *geom,
-                 void *hip_stream, bevpool_plan_t **out_plan) {
+int bevpool_plan_slabs(const double *intrinsics, const double *extrinsics,
+                       const bevpool_geometry *geom, int32_t nz, void *hip_stream,
+                       bevpool_plan_t **out_plan) {
     g_last_error[0] = '\0';
     if (!out_plan) return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "out_plan is NULL");
     *out_plan = nullptr;
     if (!intrinsics || !extrinsics || !geom)
         return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "intrinsics, extrinsics and geom must be non-NULL");
+    if (nz < 1) return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "nz=%d must be >= 1", nz);
     const bevpool_geometry &g = *geom;
-    int rc = check_geometry(g);
+    int rc = check_geometry(g, nz);
     if (rc != BEVPOOL_OK) return rc;
     if (!finite_all(intrinsics, size_t(4) * g.n_cams) || !finite_all(extrinsics, size_t(12) * g.n_cams))
         return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "calibration values must be finite");
     for (int n = 0; n < g.n_cams; ++n)
         if (intrinsics[4 * n] == 0.0 || intrinsics[4 * n + 1] == 0.0)
             return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "camera %d has a zero focal length", n);
-    return make_plan(intrinsics, extrinsics, nullptr, g, hip_stream, out_plan);
+    return make_plan(intrinsics, extrinsics, nullptr, g, nz, hip_stream, out_plan);
+}
+
+int bevpool_plan(const double *intrinsics, const double *extrinsics, const bevpool_geometry *geom,
+                 void *hip_stream, bevpool_plan_t **out_plan) {
+    return bevpool_plan_slabs(intrinsics, extrinsics, geom, 1, hip_stream, out_plan);
 }
 
 int bevpool_associate_noalloc(const double *intrinsics, const double *extrinsics,
@@ -164,7 +172,7 @@ int bevpool_plan_import(const int32_t *cell_of_point, const bevpool_geometry *ge
             return bevpool_fail(BEVPOOL_ERR_INVALID_ARG,
                                 "cell_of_point[%lld] = %d is neither -1 nor a cell below %d",
                                 (long long)p, cell_of_point[p], n_cells);
-    return make_plan(nullptr, nullptr, cell_of_point, g, hip_stream, out_plan);
+    return make_plan(nullptr, nullptr, cell_of_point, g, 1, hip_stream, out_plan);
 }
 
 namespace {
@@ -282,6 +290,7 @@ int bevpool_plan_info_get(const bevpool_plan_t *plan, bevpool_plan_info *info) {
     info->feat_w = plan->geom.feat_w;
     info->nx = plan->geom.nx;
     info->ny = plan->geom.ny;
+    info->nz = plan->nz;
     return BEVPOOL_OK;
 }
 

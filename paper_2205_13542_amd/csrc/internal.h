@@ -76,6 +76,7 @@ struct bevpool_plan_s {
     uint32_t magic;
     int device;
     bevpool_geometry geom;
+    int32_t nz;              // stacked z slabs; cell id (iy * nx + ix) * nz + iz
     int64_t n_points, n_kept;
     int32_t n_cells, n_nonempty, max_per_cell;
     int32_t n_column, n_generic, n_generic_heavy, n_runs, n_empty;
@@ -112,7 +113,7 @@ int bevpool_hip_fail(hipError_t err, const char *what);
 // Plan building (plan.hip): from the calibration, or, when host_cells is
 // not null, from a stored cell map (validated by the caller).
 int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
-                       const int32_t *host_cells, const bevpool_geometry &g,
+                       const int32_t *host_cells, const bevpool_geometry &g, int32_t nz,
                        hipStream_t stream, bevpool_plan_s *plan);
 int bevpool_launch_backward(const float *G, const void *P, const void *F,
                             const bevpool_plan_s *plan, float *dP, float *dF, int32_t batch,

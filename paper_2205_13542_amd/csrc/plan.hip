@@ -46,15 +46,16 @@ struct ProjectArgs {
     const double *extr;  // [N][12]
     bevpool_geometry g;
     FastDiv div_w, div_h, div_d;
-    int32_t n_points, n_cells;
+    int32_t n_points, n_cells, nz;
     int32_t *cell_of_point;
     uint32_t *keys;
     int32_t *vals;
 };
 
 // Sec. III-B, first paragraph: the pixel's ray at depth bin d, in the ego
-// frame, quantised at the cell size; points outside the grid or the z slab
-// are dropped. Sort key = cell id, or n_cells for a dropped point (last).
+// frame, quantised at the cell size, z like x and y; points outside the grid
+// or the nz stacked z slabs are dropped. Cell id (iy * nx + ix) * nz + iz.
+// Sort key = cell id, or n_cells for a dropped point (last).
 __global__ __launch_bounds__(kBlock) void k_project(ProjectArgs a) {
     const int32_t p = blockIdx.x * kBlock + threadIdx.x;
     if (p >= a.n_points) return;
@@ -82,8 +83,9 @@ __global__ __launch_bounds__(kBlock) void k_project(ProjectArgs a) {
     const double qy = floor((Y - g.y_min) / g.cell_y);
     const double qz = floor((Z - g.z_min) / g.z_cell);
     int32_t cell = -1;
-    if (qx >= 0.0 && qx < double(g.nx) && qy >= 0.0 && qy < double(g.ny) && qz == 0.0)
-        cell = int32_t(qy) * g.nx + int32_t(qx);
+    if (qx >= 0.0 && qx < double(g.nx) && qy >= 0.0 && qy < double(g.ny) && qz >= 0.0 &&
+        qz < double(a.nz))
+        cell = (int32_t(qy) * g.nx + int32_t(qx)) * a.nz + int32_t(qz);
     a.cell_of_point[p] = cell;
     a.keys[p] = cell >= 0 ? uint32_t(cell) : uint32_t(a.n_cells);
     a.vals[p] = p;
@@ -630,11 +632,11 @@ void device_scan(int32_t *data, int64_t n, int32_t *total, int32_t *sums, hipStr
 using namespace bevpool;
 
 int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
-                       const int32_t *host_cells, const bevpool_geometry &g, hipStream_t stream,
-                       bevpool_plan_s *plan) {
+                       const int32_t *host_cells, const bevpool_geometry &g, int32_t nz,
+                       hipStream_t stream, bevpool_plan_s *plan) {
     const int64_t np64 = int64_t(g.n_cams) * g.n_depth * g.feat_h * g.feat_w;
     const int32_t np = int32_t(np64);
-    const int32_t n_cells = g.nx * g.ny;
+    const int32_t n_cells = g.nx * g.ny * nz;
     const int32_t N = g.n_cams, D = g.n_depth, H = g.feat_h, W = g.feat_w;
     const int32_t HW = H * W;
     const int64_t n_combo = int64_t(N) * D * W;
@@ -645,6 +647,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
     int64_t n_seg_act = n_seg;                          // entries of the planes in use
     plan->n_points = np64;
     plan->n_cells = n_cells;
+    plan->nz = nz;
 
     int rc;
     if ((rc = dev_alloc(&plan->cell_of_point, size_t(np), "cell_of_point"))) return rc;
@@ -767,6 +770,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
             pa.div_d = make_fastdiv(uint32_t(D));
             pa.n_points = np;
             pa.n_cells = n_cells;
+            pa.nz = nz;
             pa.cell_of_point = plan->cell_of_point;
             pa.keys = keys_a;
             pa.vals = plan->sorted_point;
@@ -1059,6 +1063,7 @@ int bevpool_associate_into(const double *intrinsics, const double *extrinsics,
     pa.div_d = make_fastdiv(uint32_t(g.n_depth));
     pa.n_points = np;
     pa.n_cells = n_cells;
+    pa.nz = 1;
     pa.cell_of_point = cell_of_point;
     pa.keys = keys_a;
     pa.vals = sorted_point;

@@ -27,11 +27,11 @@ const char *hipGetErrorString(hipError_t) { return "stub error"; }
 }
 
 int bevpool_build_plan(const double *, const double *, const int32_t *, const bevpool_geometry &g,
-                       hipStream_t, bevpool_plan_s *plan) {
+                       int32_t nz, hipStream_t, bevpool_plan_s *plan) {
     if (g_build_rc != BEVPOOL_OK) return bevpool_fail(g_build_rc, "stub build failure");
     plan->n_points = int64_t(g.n_cams) * g.n_depth * g.feat_h * g.feat_w;
     plan->n_kept = plan->n_points / 2;
-    plan->n_cells = g.nx * g.ny;
+    plan->n_cells = g.nx * g.ny * nz;
     return BEVPOOL_OK;
 }
 int bevpool_launch_forward(const void *, const void *, const bevpool_plan_s *, float *, int64_t,
@@ -107,6 +107,18 @@ int main() {
     g_build_rc = BEVPOOL_OK;
     EXPECT(bevpool_plan(intr, extr, &g, nullptr, &plan), BEVPOOL_OK);
 
+    // stacked z slabs: nz is checked, and the cell count includes it
+    {
+        bevpool_plan_t *sl = nullptr;
+        EXPECT(bevpool_plan_slabs(intr, extr, &g, 0, nullptr, &sl), BEVPOOL_ERR_INVALID_ARG);
+        EXPECT(bevpool_plan_slabs(intr, extr, &g, 1 << 24, nullptr, &sl), BEVPOOL_ERR_OVERFLOW);
+        EXPECT(bevpool_plan_slabs(intr, extr, &g, 4, nullptr, &sl), BEVPOOL_OK);
+        bevpool_plan_info si;
+        EXPECT(bevpool_plan_info_get(sl, &si), BEVPOOL_OK);
+        if (si.nz != 4 || si.n_cells != 16 * 16 * 4) { printf("FAIL slab info\n"); return 1; }
+        bevpool_plan_destroy(sl);
+    }
+
     // import: every entry is validated on the host
     {
         const int64_t np = 1 * 8 * 4 * 8;
@@ -125,7 +137,7 @@ int main() {
     // info and export
     bevpool_plan_info info;
     EXPECT(bevpool_plan_info_get(plan, &info), BEVPOOL_OK);
-    if (info.n_points != 256 || info.n_cells != 256) { printf("FAIL info\n"); return 1; }
+    if (info.n_points != 256 || info.n_cells != 256 || info.nz != 1) { printf("FAIL info\n"); return 1; }
     EXPECT(bevpool_plan_info_get(plan, nullptr), BEVPOOL_ERR_INVALID_ARG);
     EXPECT(bevpool_plan_info_get(nullptr, &info), BEVPOOL_ERR_INVALID_ARG);
     {

@@ -238,3 +238,65 @@ def test_reduce_argument_errors(torch_cuda, pkg):
                                                    torch.cuda.Event(enable_timing=True)))
     torch.cuda.synchronize()
     plan.close()
+
+
+@pytest.mark.parametrize("name,nz", [("nuscenes", 4), ("nuscenes_tilted", 3), ("tiny", 2)])
+def test_slab_plan_bit_exact(pkg, oracle_lib, name, nz):
+    """One plan over nz stacked slabs (bevpool_plan_slabs): cell map, sorted
+    points and interval table equal to the oracle's bit for bit, and every
+    cell with points is served by columns or gathered."""
+    _say(f"[slab plan] {name} nz={nz}")
+    base = RIGS[name]()
+    rig = dataclasses.replace(base, z_cell=base.z_cell / nz)
+    plan = pkg.SlabPlan.from_rig(rig, nz)
+    cop, sp, cs = plan.export()
+    rcop, rsp, rcs = oracle_lib.plan_slabs(rig, nz)
+    assert np.array_equal(cop, rcop) and np.array_equal(sp, rsp) and np.array_equal(cs, rcs)
+    info = plan.info
+    counts = np.diff(rcs)
+    assert info.nz == nz and info.n_cells == rig.n_cells * nz
+    assert info.n_column + info.n_generic == int((counts > 0).sum())
+    assert info.n_empty == int((counts == 0).sum())
+    plan.close()
+
+
+@pytest.mark.parametrize("name", ["nuscenes", "nuscenes_tilted"])
+def test_slab_forward_bf16_and_batch(torch_cuda, pkg, oracle_lib, name):
+    """Four slabs, bf16 inputs, two frames in one call, against the oracle
+    (reduced-precision bound of the forward: 2e-2 of the sum of |terms|)."""
+    _say(f"[slab bf16 batch] {name}")
+    torch = torch_cuda
+    rig = dataclasses.replace(RIGS[name](), z_min=-8.0, z_cell=4.0)
+    C, nz = 24, 4
+    Pd, Fd, Ph, Fh = _inputs(torch, rig, C, seed=53, dtype="bf16", batch=2)
+    sp = pkg.SlabPlan.from_rig(rig, nz)
+    got = sp.forward(Pd, Fd).cpu().numpy().astype(np.float64)
+    grid = oracle_lib.slab_grid(rig, nz)
+    cop = oracle_lib.cell_map(rig, nz)
+    _, ref, scale = oracle_lib.pool(grid, cop, Ph, Fh, want_f64=True, want_abs=True)
+    ref = ref.reshape(got.shape)
+    scale = scale.reshape(got.shape)
+    assert (np.abs(got - ref) <= 2e-2 * scale + 1e-6).all()
+    sp.close()
+
+
+def test_slab_backward(torch_cuda, pkg, oracle_lib):
+    """Gradients through a plan of three slabs against the oracle's, on the
+    widened grid (|dP - ref| <= 1e-4 sqrt(C), |dF - ref| <= 1e-4 sqrt(k))."""
+    _say("[slab backward]")
+    torch = torch_cuda
+    rig = dataclasses.replace(RIGS["nuscenes"](), z_min=-6.0, z_cell=4.0)
+    C, nz = 16, 3
+    Pd, Fd, Ph, Fh = _inputs(torch, rig, C, seed=57)
+    G = np.random.default_rng(58).standard_normal((1, rig.ny, rig.nx, nz * C)).astype(np.float32)
+    sp = pkg.SlabPlan.from_rig(rig, nz)
+    gd, gf = sp.backward(torch.from_numpy(G).cuda(), Pd, Fd)
+    grid = oracle_lib.slab_grid(rig, nz)
+    cop = oracle_lib.cell_map(rig, nz)
+    refP, refF = oracle_lib.backward(grid, cop, Ph, Fh, G.reshape(1, rig.ny, rig.nx * nz, C))
+    errP = np.abs(gd.cpu().numpy().reshape(-1).astype(np.float64) - refP.reshape(-1))
+    assert (errP <= 1e-4 * np.sqrt(C)).all(), errP.max()
+    k = (cop >= 0).reshape(rig.n_cams, rig.n_depth, -1).sum(axis=1).reshape(-1)
+    errF = np.abs(gf.cpu().numpy().reshape(rig.n_pixels, C).astype(np.float64) - refF.reshape(rig.n_pixels, C))
+    assert (errF <= 1e-4 * np.sqrt(np.maximum(k, 1))[:, None]).all(), errF.max()
+    sp.close()
