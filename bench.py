@@ -753,7 +753,8 @@ def main():
                        "outer_events_mean": round(float(np.mean(outer_ms)) * 1e3, 2),
                        "warm_mean": round(warm_ms * 1e3, 2)},
         "algorithmic_bytes": nbytes,
-        "plan_bytes_read": 8 * info.n_cams * info.n_depth * info.feat_w + 16 * info.n_generic
+        "plan_bytes_read": 8 * info.n_planes * info.n_cams * info.n_depth * info.feat_w
+                           + 16 * info.n_generic
                            + 16 * info.n_runs + 4 * info.n_empty
                            + 4 * (info.n_multi * (10 + 8) + 1),
         "frames_per_s": round(w.batch / (mean_ms * 1e-3), 1),

@@ -274,6 +274,8 @@ typedef struct {
     int32_t n_partials;   /* partial-sum slots of cells fed by several combos */
     int32_t n_multi;      /* cells with partial-sum slots */
     int32_t nz;           /* stacked z slabs (n_cells = nx * ny * nz) */
+    int32_t n_planes;     /* column-table planes in use: the most row segments a
+                             column-served combo has (1 for a level rig, one slab) */
 } bevpool_plan_info;
 
 /* Fill *info: the sizes of the association ("Precomputation" paragraph of

@@ -58,7 +58,7 @@ class bevpool_plan_info(ctypes.Structure):
         ("n_column", ctypes.c_int32), ("n_generic", ctypes.c_int32),
         ("n_empty", ctypes.c_int32), ("n_runs", ctypes.c_int32),
         ("n_partials", ctypes.c_int32), ("n_multi", ctypes.c_int32),
-        ("nz", ctypes.c_int32),
+        ("nz", ctypes.c_int32), ("n_planes", ctypes.c_int32),
     ]
 
 

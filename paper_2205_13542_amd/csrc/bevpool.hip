@@ -291,6 +291,7 @@ int bevpool_plan_info_get(const bevpool_plan_t *plan, bevpool_plan_info *info) {
     info->nx = plan->geom.nx;
     info->ny = plan->geom.ny;
     info->nz = plan->nz;
+    info->n_planes = plan->n_planes;
     return BEVPOOL_OK;
 }
 

@@ -64,6 +64,8 @@
 
 #include <hip/hip_ext.h>
 
+#include <type_traits>
+
 #include "device.h"
 #include "internal.h"
 
@@ -223,6 +225,16 @@ __device__ void zero_rows(const ZeroArgs &z, int zb, int b, int *s_cell) {
     }
 }
 
+// fn(integral_constant<int, I>) for I = B .. E-1, each I a constant
+// expression (for the DPP lane selects).
+template <int B, int E, typename Fn>
+__device__ __forceinline__ void static_for(Fn &&fn) {
+    if constexpr (B < E) {
+        fn(std::integral_constant<int, B>());
+        static_for<B + 1, E>(fn);
+    }
+}
+
 // Zeroing workgroups of BS threads needed for the entries of z.
 template <int BS>
 int zero_blocks(const ZeroArgs &z) { return (z.zero_end - z.zero_begin + BS - 1) / BS; }
@@ -287,11 +299,60 @@ __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0,
                 warm ^= a.warm[q][i];
     }
 
-    for (int pass = 0;;) {
-    const bool act = e.x >= 0;
-    const uint32_t ey = uint32_t(e.y);
-    const int hlo = act ? int(ey & 0xFFFFu) : 0x7FFFFFFF;
-    const int hhi = act ? int((ey >> 16) & 0x3FFFu) : 0;
+    // Row segments (SEG): a combo whose kept rows fall into several cells
+    // has one segment per cell, ascending and disjoint, segment s in plane s
+    // of the table. One sweep over the rows serves them all: a lane masks
+    // its probability to the segment that holds its row, and when the rows
+    // pass the end of a segment that is not its combo's last, the depth
+    // bin's sums go to that segment's row and start again from zero. The
+    // last segment is emitted after the loop like a whole combo.
+    // A segment whose cell is gathered (demoted to a generic cell) has no
+    // entry: the list is compacted to the served segments, whose rows the
+    // sweep masks and flushes; rows of the others stay masked.
+    int2 seg[SEG ? kMaxSeg : 1];
+    int nseg = e.x >= 0 ? 1 : 0;
+    seg[0] = e;
+    if constexpr (SEG) {
+#pragma unroll
+        for (int q = 1; q < kMaxSeg; ++q) seg[q] = make_int2(-1, 0);
+#pragma unroll
+        for (int q = 1; q < kMaxSeg; ++q) {
+            const int2 eq = (dw_ok && q < a.n_planes) ? a.table[int64_t(q) * a.plane + tab0]
+                                                      : make_int2(-1, 0);
+            if (eq.x >= 0) {
+#pragma unroll
+                for (int i = 0; i < kMaxSeg; ++i) seg[i] = i == nseg ? eq : seg[i];
+                ++nseg;
+            }
+        }
+    }
+    // the lane's current segment for masking, and the next segment to flush
+    int cur = 0, fl = 0;
+    auto seg_lo = [&](int q) {
+        int v = 0;
+#pragma unroll
+        for (int i = 0; i < (SEG ? kMaxSeg : 1); ++i) v = i == q ? int(uint32_t(seg[i].y) & 0xFFFFu) : v;
+        return v;
+    };
+    auto seg_hi = [&](int q) {
+        int v = 0;
+#pragma unroll
+        for (int i = 0; i < (SEG ? kMaxSeg : 1); ++i) v = i == q ? int((uint32_t(seg[i].y) >> 16) & 0x3FFFu) : v;
+        return v;
+    };
+    auto seg_entry = [&](int q) {
+        int2 v = make_int2(-1, 0);
+#pragma unroll
+        for (int i = 0; i < (SEG ? kMaxSeg : 1); ++i) v = i == q ? seg[i] : v;
+        return v;
+    };
+    // row after which segment fl ends, if it is not the last one
+    auto flush_row = [&]() { return fl + 1 < nseg ? seg_hi(fl) - 1 : 0x7FFFFFFF; };
+    const bool act = nseg > 0;
+    // the whole combo's rows (one plane)
+    const uint32_t ey0 = uint32_t(e.y);
+    const int hlo = act ? int(ey0 & 0xFFFFu) : 0x7FFFFFFF;
+    const int hhi = act ? int((ey0 >> 16) & 0x3FFFu) : 0;
     // depth bins present in the wave (a wave without any skips the loop)
     const uint64_t bal = __ballot(act);
     const uint32_t dm = uint32_t((bal | (bal >> 16) | (bal >> 32) | (bal >> 48)) & 0xFFu);
@@ -302,6 +363,34 @@ __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0,
 #pragma unroll
         for (int k = 0; k < NCH; ++k) acc[q][k] = MAXR ? -INFINITY : 0.f;
     const float masked = MAXR ? __builtin_nanf("") : 0.f;   // probability of a row outside the combo
+    const bool mean = !MAXR && a.mean != 0;
+
+    // depth bin J's sums to the row of its segment that ends at row r, if
+    // one does (lane J of the group knows), then from zero again
+    auto flush = [&](int r) {
+        const int my = flush_row();
+        static_for<0, kColDepth>([&](auto Jc) {
+            constexpr int J = decltype(Jc)::value;
+            if (row_bcast<J>(my) == r) {
+                const int2 fe = seg_entry(fl);
+                const int x = row_bcast<J>(fe.x);
+                const uint32_t y = uint32_t(row_bcast<J>(fe.y));
+                float v[NCH];
+#pragma unroll
+                for (int k = 0; k < NCH; ++k) v[k] = acc[J][k];
+                if (mean && !(y & kComboMulti)) {
+                    const float cnt = float(int((y >> 16) & 0x3FFFu) - int(y & 0xFFFFu));
+#pragma unroll
+                    for (int k = 0; k < NCH; ++k) v[k] = v[k] / cnt;
+                }
+                store_row<NCH, VEC>(fr.O, x >= 0 ? uint32_t(x) * uint32_t(a.ldo) * 4u + uint32_t(c0) * 4u : kOff,
+                                    v, tail_ok);
+#pragma unroll
+                for (int k = 0; k < NCH; ++k) acc[J][k] = MAXR ? -INFINITY : 0.f;
+            }
+        });
+        if (my == r) ++fl;
+    };
 
     if (dm != 0) {
         // A ring of kStages stages of two rows: while one stage is applied,
@@ -317,41 +406,37 @@ __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0,
             for (int u = 0; u < kStages; ++u) {
                 const int hs = h + 2 * u;
                 const int hp = hs + hsel;
-                pq[j] = (hp >= hlo && hp < hhi) ? st[u].pv : masked;
+                bool keep;
+                if constexpr (SEG) {
+                    while (cur + 1 < nseg && hp >= seg_hi(cur)) ++cur;
+                    keep = hp >= seg_lo(cur) && hp < seg_hi(cur);
+                } else {
+                    keep = hp >= hlo && hp < hhi;
+                }
+                pq[j] = keep ? st[u].pv : masked;
                 __builtin_amdgcn_wave_barrier();
                 const float4 r0a = *reinterpret_cast<const float4 *>(pq);
                 const float4 r0b = *reinterpret_cast<const float4 *>(pq + 4);
                 const float4 r1a = *reinterpret_cast<const float4 *>(pq + 8);
                 const float4 r1b = *reinterpret_cast<const float4 *>(pq + 12);
                 __builtin_amdgcn_wave_barrier();
+                // a segment of some lane's combo ends in this stage
+                const bool split = SEG && __ballot(flush_row() <= hs + 1) != 0;
                 apply_row<NCH, MAXR>(acc, r0a, r0b, st[u].f0);
+                if (split) flush(hs);
                 apply_row<NCH, MAXR>(acc, r1a, r1b, st[u].f1);
+                if (split) flush(hs + 1);
                 load_stage(st[u], hs + 2 * kStages);
             }
         }
     }
 
-    Emit<0, NCH, VEC>::run(acc, e.x, e.y, dm, fr.O, uint32_t(c0) * 4u, a.ldo, !MAXR && a.mean != 0,
-                           tail_ok);
-    // the next plane with an entry in this wave, if any: its rows again
-    // (only in the SEG instantiation, launched for plans with several
-    // planes: the loop costs registers that the generic roles, which share
-    // the kernel, would lose in occupancy)
-    if constexpr (!SEG) break;
-    bool more = false;
-    while (++pass < a.n_planes) {
-        e = dw_ok ? a.table[int64_t(pass) * a.plane + tab0] : make_int2(-1, 0);
-        if (__ballot(e.x >= 0) != 0) {
-            more = true;
-            break;
-        }
-    }
-    if (!more) break;
-#pragma unroll
-    for (int u = 0; u < kStages; ++u) {
-        load_stage(st[u], 2 * u);
-        __builtin_amdgcn_sched_barrier(0);
-    }
+    // the combo's last segment (the whole combo when it has one)
+    if constexpr (SEG) {
+        const int2 el = seg_entry(nseg > 0 ? nseg - 1 : 0);
+        Emit<0, NCH, VEC>::run(acc, el.x, el.y, dm, fr.O, uint32_t(c0) * 4u, a.ldo, mean, tail_ok);
+    } else {
+        Emit<0, NCH, VEC>::run(acc, e.x, e.y, dm, fr.O, uint32_t(c0) * 4u, a.ldo, mean, tail_ok);
     }
     asm volatile("" ::"v"(warm));   // the touched words are not needed, only loaded
 }

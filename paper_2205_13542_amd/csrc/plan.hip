@@ -433,6 +433,21 @@ __global__ __launch_bounds__(kBlock) void k_combo_table(ComboArgs a, int2 *table
     multi_flag[t] = multi ? 1 : 0;
 }
 
+// Every entry of the column table empty ({-1, 0}): planes that the final
+// partition does not use hold no stale entries.
+__global__ __launch_bounds__(kBlock) void k_clear_table(int2 *table, int64_t n) {
+    const int64_t t = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    if (t < n) table[t] = make_int2(-1, 0);
+}
+
+// Planes in use: one past the highest plane of the column table that holds
+// an entry.
+__global__ __launch_bounds__(kBlock) void k_planes_used(const int2 *table, int64_t n,
+                                                        int32_t n_combo, int32_t *planes) {
+    const int64_t t = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    if (t < n && table[t].x >= 0) atomicMax(planes, int32_t(t / n_combo) + 1);
+}
+
 // Not enough empty rows to hold the partial sums: cells fed by several
 // combos become generic.
 __global__ __launch_bounds__(kBlock) void k_demote_multi(ComboArgs a, int32_t n_cells) {
@@ -814,6 +829,8 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         ca.max_seg = small + 6;
         ca.served_pts = small + 7;
         hipLaunchKernelGGL(k_combo_walk, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream, ca);
+        hipLaunchKernelGGL(k_clear_table, dim3(blocks_for(n_seg)), dim3(kBlock), 0, stream,
+                           plan->column_table, n_seg);
         int32_t stats[4], counters[2], n_gen = 0, n_empty = 0, kept = 0, n_part = 0;
         auto classify = [&]() -> int {
             fill(flag_a, int64_t(n_cells) + 1, 0);
@@ -853,6 +870,8 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
             // partition is rebuilt with whole combos only
             ca.planes = 1;
             n_seg_act = n_combo;
+            hipLaunchKernelGGL(k_clear_table, dim3(blocks_for(n_seg)), dim3(kBlock), 0, stream,
+                               plan->column_table, n_seg);
             fill(cell_generic, n_cells, 0);
             fill(cell_ncombo, n_cells, 0);
             fill(small + 6, 2, 0);
@@ -872,7 +891,11 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         plan->n_generic = n_gen;
         plan->n_empty = n_empty;
         plan->n_partials = n_part;
-        plan->n_planes = stats[2] > 0 ? stats[2] : 1;
+        // planes in use, from the final table (cells demoted to generic leave
+        // their segments' planes empty)
+        fill(small + 2, 1, 0);
+        hipLaunchKernelGGL(k_planes_used, dim3(blocks_for(n_seg_act)), dim3(kBlock), 0, stream,
+                           plan->column_table, n_seg_act, int32_t(n_combo), small + 2);
 
         // cells without points, ascending
         if ((rc2 = dev_alloc(&plan->empty_cells, size_t(n_empty), "empty_cells"))) return rc2;
@@ -893,10 +916,12 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         }
         device_scan(head_scan, int64_t(n_part) + 1, small + 3, scan_sums, stream);
         BEVPOOL_HIP(hipGetLastError());
-        int32_t n_multi;
+        int32_t n_multi, n_planes;
         if ((rc2 = to_host(&n_multi, head_scan + n_part))) return rc2;
+        if ((rc2 = to_host(&n_planes, small + 2))) return rc2;
         BEVPOOL_HIP(hipStreamSynchronize(stream));
         plan->n_multi = n_multi;
+        plan->n_planes = n_planes > 0 ? n_planes : 1;
         if ((rc2 = dev_alloc(&plan->multi_begin, size_t(n_multi) + 1, "multi_begin"))) return rc2;
         if ((rc2 = dev_alloc(&plan->multi_cell, size_t(n_multi), "multi_cell"))) return rc2;
         hipLaunchKernelGGL(k_multi_cells, dim3(blocks_for(int64_t(n_part) + 1)), dim3(kBlock), 0,

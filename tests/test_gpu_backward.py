@@ -80,7 +80,7 @@ def _grad(w, seed):
 
 
 @pytest.mark.parametrize("name,seed", [("tiny", 0), ("tiny_identity", 1), ("nuscenes", 2),
-                                       ("nuscenes_tilted", 3)])
+                                       ("nuscenes_tilted", 3), ("nuscenes_tilt1", 5)])
 def test_backward_matches_oracle(torch_cuda, pkg, oracle_lib, name, seed):
     """Level rig: every combo clean (one gradient row per combo); tilted rig:
     mostly rows with cells of their own."""

@@ -166,11 +166,17 @@ def test_forward_fp32(torch_cuda, pkg, oracle_lib, oracle_plans, name, seed):
     _say(f"  worst err/bound {worst:.3g}")
 
 
-@pytest.mark.parametrize("name", ["nuscenes_bf16", "nuscenes_f16"])
-def test_forward_reduced_precision(torch_cuda, pkg, oracle_lib, oracle_plans, name):
-    _say(f"[forward {name}]")
+@pytest.mark.parametrize("name,rig_name", [("nuscenes_bf16", "nuscenes"), ("nuscenes_f16", "nuscenes"),
+                                           ("nuscenes_bf16", "nuscenes_tilt1"),
+                                           ("nuscenes_f16", "nuscenes_tilt1")])
+def test_forward_reduced_precision(torch_cuda, pkg, oracle_lib, oracle_plans, name, rig_name):
+    """bf16 / fp16 inputs, fp32 accumulation, on the level rig and on the
+    slightly tilted one (row segments)."""
+    _say(f"[forward {name} on {rig_name}]")
     w = wl.make(name, seed=0)
-    cop, _, cs = oracle_plans("nuscenes")
+    if rig_name != "nuscenes":
+        w = dataclasses.replace(w, rig=RIGS[rig_name]())
+    cop, _, cs = oracle_plans(rig_name)
     ref, ref64, abs64 = oracle_lib.pool(w.rig, cop, w.P, w.F, want_f64=True, want_abs=True)
     plan = pkg.Plan.from_rig(w.rig)
     got = _run(torch_cuda, pkg, plan, w)
@@ -181,11 +187,14 @@ def test_forward_reduced_precision(torch_cuda, pkg, oracle_lib, oracle_plans, na
     _say(f"  global relative L2 error {rel:.3g}")
 
 
-def test_forward_batched_matches_single_frames(torch_cuda, pkg, oracle_lib, oracle_plans):
-    _say("[forward batched] nuscenes_b8")
+@pytest.mark.parametrize("rig_name", ["nuscenes", "nuscenes_tilt1"])
+def test_forward_batched_matches_single_frames(torch_cuda, pkg, oracle_lib, oracle_plans, rig_name):
+    _say(f"[forward batched] 8 frames on {rig_name}")
     torch = torch_cuda
     w = wl.make("nuscenes_b8", seed=0)
-    cop, _, cs = oracle_plans("nuscenes")
+    if rig_name != "nuscenes":
+        w = dataclasses.replace(w, rig=RIGS[rig_name]())
+    cop, _, cs = oracle_plans(rig_name)
     plan = pkg.Plan.from_rig(w.rig)
     P = _to_device(torch, w.P, "f32")
     F = _to_device(torch, w.F, "f32")
@@ -297,7 +306,8 @@ def test_deterministic(torch_cuda, pkg):
     assert np.array_equal(a, b)
 
 
-@pytest.mark.parametrize("name", ["tiny", "nuscenes", "nuscenes_tilted", "coarse", "empty"])
+@pytest.mark.parametrize("name", ["tiny", "nuscenes", "nuscenes_tilted", "nuscenes_tilt1", "coarse",
+                                  "empty"])
 def test_plan_import_round_trip(torch_cuda, pkg, name):
     """A plan rebuilt from its exported cell map (bevpool_plan_import) has
     the same association, the same partition and the same pooled map, bit
@@ -319,12 +329,16 @@ def test_plan_import_round_trip(torch_cuda, pkg, name):
     b.close()
 
 
-def test_one_plan_on_two_streams(torch_cuda, pkg):
+@pytest.mark.parametrize("rig_name", ["nuscenes", "nuscenes_tilt1"])
+def test_one_plan_on_two_streams(torch_cuda, pkg, rig_name):
     """The plan is read-only during a forward: two streams pool different
     frames with it at once (each into its own map), several times over, and
     every map equals the one pooled alone."""
     torch = torch_cuda
+    _say(f"[two streams] {rig_name}")
     w = wl.make("nuscenes", seed=12, batch=2)
+    if rig_name != "nuscenes":
+        w = dataclasses.replace(w, rig=RIGS[rig_name]())
     plan = pkg.Plan.from_rig(w.rig)
     P = _to_device(torch, w.P, "f32")
     F = _to_device(torch, w.F, "f32")
