@@ -278,7 +278,7 @@ def backward_bench(args):
     of the BEV map resident in HBM; each timed call after a cache-evicting
     read, timed by events recorded as stream entries around the call.
     Algorithmic bytes: P, F and the gradient rows of the non-empty cells
-    read, dP and dF written (the plan's cell map is reported beside them)."""
+    read, dP and dF written (the plan's combo table is reported beside them)."""
     import numpy as np
     import torch
     import workloads as wl
@@ -333,7 +333,9 @@ def backward_bench(args):
                         "median": round(float(np.median(ms)) * 1e3, 2),
                         "min": round(float(ms.min()) * 1e3, 2)},
         "algorithmic_bytes": nbytes,
-        "plan_bytes_read": w.rig.n_points * 4 + w.rig.n_cams * w.rig.n_depth * w.rig.feat_w * 4,
+        # the combo table by column (8 bytes per combo) and the block flags
+        "plan_bytes_read": 8 * w.rig.n_cams * w.rig.n_depth * w.rig.feat_w
+                           + 4 * w.rig.n_cams * -(-w.rig.feat_w // 8),
         "kernel_sha256_16": kernel_hash([BWD_SOURCE]),
     }
     if not args.no_cpu_baseline:

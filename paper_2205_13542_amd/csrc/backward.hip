@@ -4,23 +4,45 @@
 //   dP[b][p]      = F[b][pixel(p)] . G[b][cell(p)]   for a kept point p, else 0
 //   dF[b][pixel]  = sum over the kept points p of the pixel of P[b][p] G[b][cell(p)]
 //
-// Pixel-stationary work: a workgroup owns kBCols pixel columns x kBRows rows
-// of one camera, and its kBWaves waves take consecutive parts of the depth
-// bins. A group of 16 lanes owns one column; lane j holds the row slice
-// channels (the forward's lane layout) of the kBRows feature rows, read
-// once, and the kBRows rows' dF sums. For each depth bin the group reads one
-// gradient row when the combo (camera, depth bin, column) is clean — all its
-// kept points in one cell, which the plan records — or one per kept row
-// otherwise. dF gets P x G; dP gets the dot product F . G, reduced across the
-// 16 lanes by a transpose-reduce (8 shuffles for the 8 rows' sums). A
-// wave parks the dP values of a chunk of depth bins in LDS and writes them
-// after the chunk (vector loads and stores share one in-order counter, so a
-// store inside the loop would hold up the waits for the next loads). The
-// waves' dF sums are added in LDS in wave order and stored once; every dP
-// element is written by the one wave that owns its depth bin, so nothing is
-// accumulated with atomics and repeated calls give bitwise equal results.
-// Channel slices run as successive launches; slices after the first add
-// their dot products to dP.
+// Two kernels share the work by blocks of kBwdBlockCols pixel columns of one
+// camera (the plan flags the blocks that hold a combo that is not clean).
+//
+// Clean blocks (every combo's kept rows in one cell, one row range): per
+// pixel column w the gradients are two small matrix products over the
+// column's gradient rows G_w[d] = G[cell(n, d, w)],
+//   dF_w[h][c] = sum_d M[d][h] P[d][h] G_w[d][c]
+//   dP_w[d][h] = M[d][h] (sum_c G_w[d][c] F_w[h][c])
+// with M the kept-row mask of the combos. k_backward_mma runs both on the
+// matrix cores (v_mfma_f32_16x16x4f32, fp32 in and out): a workgroup owns
+// two adjacent columns and 16 rows of one camera, its four waves take
+// consecutive parts of the depth bins, 16 bins per step. The second product
+// takes the channels as its K dimension in the order 16t + 4q + e (t the
+// step group, q the lane quarter, e the element), so that F and G arrive as
+// 16-byte quads; the first takes the depth bins as K and reads the step's
+// gradient rows back transposed from the wave's own LDS copy. The waves' dF
+// sums are added in LDS in wave order; every dP element comes from one wave.
+// The combos come from the plan's table by column (consecutive depth bins
+// adjacent: one 8-byte read per lane covers 64 bins), and P and dP of the
+// column pair move as 8-byte pieces (W even; odd widths take the per-row
+// kernel).
+//
+// Other blocks (k_backward): pixel-stationary work on the vector ALUs. A
+// workgroup owns kBCols pixel columns x kBRows rows of one camera, and its
+// kBWaves waves take consecutive parts of the depth bins. A group of 16
+// lanes owns one column; lane j holds the row slice channels (the forward's
+// lane layout) of the kBRows feature rows, read once, and the kBRows rows'
+// dF sums. For each depth bin the group reads one gradient row when the
+// combo (camera, depth bin, column) is clean, or one per kept row otherwise.
+// dF gets P x G; dP gets the dot product F . G, reduced across the 16 lanes
+// by a transpose-reduce (8 shuffles for the 8 rows' sums). A wave parks the
+// dP values of a chunk of depth bins in LDS and writes them after the chunk
+// (vector loads and stores share one in-order counter, so a store inside the
+// loop would hold up the waits for the next loads). The waves' dF sums are
+// added in LDS in wave order and stored once.
+//
+// Nothing is accumulated with atomics, so repeated calls give bitwise equal
+// results. Channel slices run as successive launches; slices after the first
+// add their dot products to dP.
 #include <stdint.h>
 
 #include <algorithm>
@@ -33,6 +55,7 @@ namespace {
 
 constexpr int kBRows = 8;                      // pixel rows per lane group
 constexpr int kBCols = 4;                      // pixel columns per workgroup (lane groups of a wave)
+static_assert(kBwdBlockCols % kBCols == 0, "a workgroup's columns lie in one backward block");
 constexpr int kBWaves = 4;                     // depth parts per workgroup
 constexpr int kBBlock = kBWaves * kWaveSize;
 constexpr int kBStages = 4;                    // depth bins in flight per wave
@@ -49,6 +72,9 @@ struct BwdArgs {
     int32_t items_w, items_h;                  // column blocks and row blocks per camera
     int32_t part;                              // depth bins per wave
     int32_t accumulate_dp, want_dp, want_df;
+    const int32_t *mixed;                      // per backward block: 1 if a combo is not clean
+    int32_t skip_clean;                        // 1: blocks without such combos are left to k_backward_mma
+    int32_t blocks_w8;                         // backward blocks per camera
 };
 
 // One depth bin of a lane group: its combo's cell, each row's cell (lane j:
@@ -148,6 +174,7 @@ __global__ __launch_bounds__(kBBlock) void k_backward(BwdArgs a) {
     const int rb = item % a.items_h;
     const int t = item / a.items_h;
     const int cb = t % a.items_w, n = t / a.items_w;
+    if (a.skip_clean && a.mixed[n * a.blocks_w8 + cb * kBCols / kBwdBlockCols] == 0) return;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int j = lane & 15, grp = lane >> 4;
     const int w = cb * kBCols + grp;
@@ -277,6 +304,284 @@ __global__ __launch_bounds__(kBBlock) void k_backward(BwdArgs a) {
         store_row<NCH, VEC>(dF, h0 + r < a.H ? df_col + uint32_t(r) * df_row : kOff, acc[r], tail_ok);
 }
 
+
+// ---------------------------------------------------------------- matrix cores
+
+constexpr int kMWaves = 4;                     // depth parts per workgroup
+constexpr int kMCols = 2;                      // adjacent pixel columns per workgroup
+constexpr int kMRows = 16;                     // pixel rows per workgroup (M of the instruction)
+constexpr int kMChunk = 16;                    // depth bins per step (N of the dP product)
+constexpr int kMBlock = kMWaves * kWaveSize;
+constexpr int kMSlice = 80;                    // channels per launch (a multiple of 16)
+static_assert(kBwdBlockCols % kMCols == 0, "a column pair lies in one backward block");
+
+typedef float f4v __attribute__((ext_vector_type(4)));
+
+struct MmaArgs {
+    const char *P, *F;
+    const float *G;
+    float *dP, *dF;
+    const int2 *combos;                        // [N][W][D]: {cell, rows} of a clean combo, else {-1, 0}
+    const int32_t *mixed;                      // [N][blocks_w]: 1 if a combo of the block is not clean
+    int32_t D, H, W, C, c0, cn;                // channel slice [c0, c0 + cn), cn a multiple of 4; W even
+    uint32_t p_bytes, f_bytes, g_bytes, dp_bytes, df_bytes, cb_bytes;
+    int32_t pairs_w, blocks_h, blocks_w;       // column pairs, row blocks, backward blocks per camera
+    int32_t part;                              // depth bins per wave, a multiple of kMChunk
+    int32_t accumulate_dp, want_dp, want_df;
+};
+
+// LDS row stride (floats) of a step's gradient rows: an odd multiple of 16,
+// so that the four rows one transposed read touches fall in distinct banks.
+template <int T>
+constexpr int mma_stride() { return 16 * (T | 1); }
+
+// Two consecutive elements as fp32.
+template <int DT>
+__device__ __forceinline__ void load_pair(Rsrc r, uint32_t off, float &x, float &y) {
+    if constexpr (DT == BEVPOOL_F32) {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, int(off), 0, 0);
+        x = __uint_as_float(v[0]);
+        y = __uint_as_float(v[1]);
+    } else {
+        const uint32_t v = __builtin_amdgcn_raw_buffer_load_b32(r, int(off), 0, 0);
+        if constexpr (DT == BEVPOOL_BF16) {
+            x = __uint_as_float(v << 16);
+            y = __uint_as_float(v & 0xFFFF0000u);
+        } else {
+            x = float(__builtin_bit_cast(_Float16, uint16_t(v & 0xFFFFu)));
+            y = float(__builtin_bit_cast(_Float16, uint16_t(v >> 16)));
+        }
+    }
+}
+
+__device__ __forceinline__ bool row_kept(int h, int rg) {
+    const int lo = rg & 0xFFFF, hi = rg >> 16;
+    return uint32_t(h - lo) < uint32_t(hi - lo);
+}
+
+template <int DT, int T>
+__global__ __launch_bounds__(kMBlock) __attribute__((amdgpu_waves_per_eu(3)))
+void k_backward_mma(MmaArgs a) {
+    constexpr int S = mma_stride<T>();
+    constexpr int kLds = kMWaves * kMCols * kMChunk * S;
+    static_assert((kMWaves - 1) * kMCols * T * 4 * kWaveSize <= kLds, "dF exchange fits the step buffers");
+    constexpr int kFq = 4 * T + 1;             // quads per feature row in LDS (odd: no bank conflicts)
+    __shared__ __attribute__((aligned(16))) float s_g[kLds];
+    __shared__ f4v s_f[kMCols * kMRows * kFq];
+    constexpr uint32_t ES = Elem<DT>::kBytes;
+    const int b = blockIdx.y;
+    // the two row blocks of a column pair share its gradient rows: placed on
+    // one CU; neighbouring pairs share P lines: placed on one XCD
+    const int item = xcd_cu_remap<2>(blockIdx.x, gridDim.x);
+    const int rb = item % a.blocks_h;
+    const int tt = item / a.blocks_h;
+    const int cp = tt % a.pairs_w, n = tt / a.pairs_w;
+    const int w0 = cp * kMCols;
+    if (a.mixed[n * a.blocks_w + w0 / kBwdBlockCols] != 0) return;   // left to k_backward
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int q = lane >> 4, j = lane & 15;
+    const int h0 = rb * kMRows;
+    const int hj = h0 + j;
+    const bool hj_ok = hj < a.H;
+
+    const Rsrc P = make_rsrc(a.P + int64_t(b) * a.p_bytes, a.p_bytes);
+    const Rsrc F = make_rsrc(a.F + int64_t(b) * a.f_bytes, a.f_bytes);
+    const Rsrc G = make_rsrc(reinterpret_cast<const char *>(a.G) + int64_t(b) * a.g_bytes, a.g_bytes);
+    const Rsrc dP = make_rsrc(reinterpret_cast<const char *>(a.dP) + int64_t(b) * a.dp_bytes, a.dp_bytes);
+    const Rsrc dF = make_rsrc(reinterpret_cast<const char *>(a.dF) + int64_t(b) * a.df_bytes, a.df_bytes);
+    const Rsrc CB = make_rsrc(a.combos, a.cb_bytes);
+    const uint32_t HW = uint32_t(a.H) * uint32_t(a.W);
+    const int d_lo = min(a.D, wave * a.part), d_hi = min(a.D, d_lo + a.part);
+
+    // combos of up to 64 depth bins, lane l: bin dsup + l (one 8-byte entry
+    // per column, consecutive bins adjacent), issued before everything else
+    int ccv[kMCols], rgv[kMCols];
+    auto load_combos = [&](int dsup) {
+#pragma unroll
+        for (int i = 0; i < kMCols; ++i) {
+            const int d = dsup + lane;
+            const bool ok = d < d_hi;
+            const uint32_t addr = (uint32_t(n * a.W + w0 + i) * uint32_t(a.D) + uint32_t(d)) * 8u;
+            const auto v = __builtin_amdgcn_raw_buffer_load_b64(CB, int(ok ? addr : kOff), 0, 0);
+            ccv[i] = ok ? int(v[0]) : -1;
+            rgv[i] = ok ? int(v[1]) : 0;
+        }
+    };
+    load_combos(d_lo);
+
+    // the feature rows of the workgroup's two columns and 16 rows, in LDS:
+    // quad 4t + q of row (i, r) holds channels c0 + 16t + 4q .. + 3
+    for (int x = threadIdx.x; x < kMCols * kMRows * 4 * T; x += kMBlock) {
+        const int qd = x % (4 * T), r = (x / (4 * T)) % kMRows, i = x / (4 * T * kMRows);
+        const int h = h0 + r;
+        const bool ok = (h < a.H) & (4 * qd < a.cn);
+        const uint32_t addr = ((uint32_t(n) * HW + uint32_t(h) * uint32_t(a.W) + uint32_t(w0 + i)) * uint32_t(a.C) +
+                               uint32_t(a.c0 + 4 * qd)) * ES;
+        float v[4];
+        Elem<DT>::load4(F, ok ? addr : kOff, v);
+        s_f[(i * kMRows + r) * kFq + qd] = f4v{v[0], v[1], v[2], v[3]};
+    }
+
+    // dF sums: lane (q, j), value r holds row h0 + 4q + r, channel c0 + 16t + j
+    f4v accf[kMCols][T];
+#pragma unroll
+    for (int i = 0; i < kMCols; ++i)
+#pragma unroll
+        for (int t = 0; t < T; ++t) accf[i][t] = f4v{0.f, 0.f, 0.f, 0.f};
+
+    float *sg = s_g + wave * (kMCols * kMChunk * S);
+
+    // Loads of one step (16 depth bins from d0 = dsup + k): the gradient rows
+    // of bins d0 + j as 16-byte quads in the channel order of the dP product,
+    // and P of bins d0 + 4s + q, row h0 + j (operand A of the dF product).
+    struct StepIn {
+        f4v g[kMCols][T];
+        float p[kMCols][4];
+    };
+    auto load_step = [&](StepIn &in, int dsup, int k) {
+        const int d0 = dsup + k;
+#pragma unroll
+        for (int i = 0; i < kMCols; ++i) {
+            const int cc = __shfl(ccv[i], k + j, kWaveSize);
+            const uint32_t row = uint32_t(max(cc, 0)) * uint32_t(a.C) + uint32_t(a.c0 + 4 * q);
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+                const bool ok = (cc >= 0) & (16 * t + 4 * q < a.cn);
+                const uint32_t addr = (row + uint32_t(16 * t)) * 4u;
+                const auto v = __builtin_amdgcn_raw_buffer_load_b128(G, int(ok ? addr : kOff), 0, 0);
+                in.g[i][t] = f4v{__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]),
+                                 __uint_as_float(v[3])};
+            }
+        }
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            const int d = d0 + 4 * s + q;
+            const bool ok = (d < d_hi) & hj_ok;
+            const uint32_t pt = uint32_t(n * a.D + d) * HW + uint32_t(hj) * uint32_t(a.W) + uint32_t(w0);
+            load_pair<DT>(P, ok ? pt * ES : kOff, in.p[0][s], in.p[1][s]);
+        }
+    };
+
+    auto run_step = [&](const StepIn &in, int dsup, int k) {
+        const int d0 = dsup + k;
+        // dP product: lane (q, j), value r is row h0 + 4q + r, bin d0 + j
+        f4v accp[kMCols];
+#pragma unroll
+        for (int i = 0; i < kMCols; ++i) {
+            accp[i] = f4v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+                const f4v f = s_f[(i * kMRows + j) * kFq + 4 * t + q];
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    accp[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(f[e], in.g[i][t][e], accp[i], 0, 0, 0);
+            }
+        }
+        // the step's gradient rows into this wave's LDS rows, row j = bin d0 + j
+#pragma unroll
+        for (int i = 0; i < kMCols; ++i)
+#pragma unroll
+            for (int t = 0; t < T; ++t)
+                *reinterpret_cast<f4v *>(&sg[(i * kMChunk + j) * S + 16 * t + 4 * q]) = in.g[i][t];
+        // dF product: operand A masked to the combos' kept rows, operand B
+        // (K = bin, N = channel) read back transposed
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int i = 0; i < kMCols; ++i) {
+                const int rg = __shfl(rgv[i], k + 4 * s + q, kWaveSize);
+                const float pm = row_kept(hj, rg) ? in.p[i][s] : 0.f;
+#pragma unroll
+                for (int t = 0; t < T; ++t) {
+                    const float g = sg[(i * kMChunk + 4 * s + q) * S + 16 * t + j];
+                    accf[i][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(pm, g, accf[i][t], 0, 0, 0);
+                }
+            }
+        if (a.want_dp) {
+            const int d = d0 + j;
+            int rgj[kMCols];
+#pragma unroll
+            for (int i = 0; i < kMCols; ++i) rgj[i] = __shfl(rgv[i], k + j, kWaveSize);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int h = h0 + 4 * q + r;
+                const bool ok = (d < d_hi) & (h < a.H);
+                const uint32_t off = ok ? (uint32_t(n * a.D + d) * HW + uint32_t(h) * uint32_t(a.W) + uint32_t(w0)) * 4u
+                                        : kOff;
+                float v0 = row_kept(h, rgj[0]) ? accp[0][r] : 0.f;
+                float v1 = row_kept(h, rgj[1]) ? accp[1][r] : 0.f;
+                if (a.accumulate_dp) {
+                    const auto o = __builtin_amdgcn_raw_buffer_load_b64(dP, int(off), 0, 0);
+                    v0 += __uint_as_float(o[0]);
+                    v1 += __uint_as_float(o[1]);
+                }
+                __builtin_amdgcn_raw_buffer_store_b64(
+                    (__attribute__((ext_vector_type(2))) uint32_t){__float_as_uint(v0), __float_as_uint(v1)}, dP,
+                    int(off), 0, 0);
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+    };
+
+    __syncthreads();   // the feature rows are in LDS
+    // steps of 16 bins
+    StepIn in0;
+    for (int dsup = d_lo; dsup < d_hi; dsup += kWaveSize) {
+        if (dsup > d_lo) load_combos(dsup);
+        const int dn = min(kWaveSize, d_hi - dsup);
+        for (int k = 0; k < dn; k += kMChunk) {
+            load_step(in0, dsup, k);
+            run_step(in0, dsup, k);
+        }
+    }
+
+    if (!a.want_df) return;
+    // waves 1.. park their sums in LDS; wave 0 adds them in wave order
+    __syncthreads();
+    if (wave > 0) {
+#pragma unroll
+        for (int i = 0; i < kMCols; ++i)
+#pragma unroll
+            for (int t = 0; t < T; ++t)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    s_g[((((wave - 1) * kMCols + i) * T + t) * 4 + r) * kWaveSize + lane] = accf[i][t][r];
+    }
+    __syncthreads();
+    if (wave > 0) return;
+    for (int v = 1; v < kMWaves; ++v)
+#pragma unroll
+        for (int i = 0; i < kMCols; ++i)
+#pragma unroll
+            for (int t = 0; t < T; ++t)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    accf[i][t][r] += s_g[((((v - 1) * kMCols + i) * T + t) * 4 + r) * kWaveSize + lane];
+#pragma unroll
+    for (int i = 0; i < kMCols; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int h = h0 + 4 * q + r;
+            const uint32_t row = (uint32_t(n) * HW + uint32_t(h) * uint32_t(a.W) + uint32_t(w0 + i)) * uint32_t(a.C);
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+                const bool ok = (h < a.H) & (16 * t + j < a.cn);
+                store_f32(dF, ok ? (row + uint32_t(a.c0 + 16 * t + j)) * 4u : kOff, accf[i][t][r]);
+            }
+        }
+}
+
+template <int DT>
+void launch_mma(const MmaArgs &a, dim3 grid, int tiles, hipStream_t s) {
+    switch (tiles) {
+        case 1: hipLaunchKernelGGL((k_backward_mma<DT, 1>), grid, dim3(kMBlock), 0, s, a); break;
+        case 2: hipLaunchKernelGGL((k_backward_mma<DT, 2>), grid, dim3(kMBlock), 0, s, a); break;
+        case 3: hipLaunchKernelGGL((k_backward_mma<DT, 3>), grid, dim3(kMBlock), 0, s, a); break;
+        case 4: hipLaunchKernelGGL((k_backward_mma<DT, 4>), grid, dim3(kMBlock), 0, s, a); break;
+        default: hipLaunchKernelGGL((k_backward_mma<DT, 5>), grid, dim3(kMBlock), 0, s, a); break;
+    }
+}
+
 template <int DT>
 void launch_bwd(const BwdArgs &a, dim3 grid, int nch, bool vec, hipStream_t s) {
     switch (nch) {
@@ -316,6 +621,56 @@ int bevpool_launch_backward(const float *G, const void *P, const void *F,
     if (batch > 65535)
         return bevpool_fail(BEVPOOL_ERR_INVALID_ARG, "batch=%d exceeds 65535 frames per call", batch);
 
+    // Matrix-core kernel for the blocks whose combos are all clean: feature
+    // and gradient rows move as 4-element quads, so channels % 4 == 0 and
+    // aligned rows; the per-row kernel takes the other blocks (or all blocks).
+    const bool quads = channels % 4 == 0 && reinterpret_cast<uintptr_t>(F) % (4 * esize) == 0 &&
+                       reinterpret_cast<uintptr_t>(G) % 16 == 0;
+    // (a column pair is read and written as one 8-byte piece: W even)
+    const bool run_mma = quads && g.feat_w % 2 == 0 && plan->n_bwd_mixed < plan->n_bwd_blocks;
+    const bool run_rows = !run_mma || plan->n_bwd_mixed > 0;
+    if (run_mma) {
+        MmaArgs m;
+        m.P = static_cast<const char *>(P);
+        m.F = static_cast<const char *>(F);
+        m.G = G;
+        m.dP = dP;
+        m.dF = dF;
+        m.combos = plan->combo_cols;
+        m.mixed = plan->bwd_mixed;
+        m.D = g.n_depth;
+        m.H = g.feat_h;
+        m.W = g.feat_w;
+        m.C = channels;
+        m.p_bytes = uint32_t(p_bytes);
+        m.f_bytes = uint32_t(f_bytes);
+        m.g_bytes = uint32_t(g_bytes);
+        m.dp_bytes = dP ? uint32_t(dp_bytes) : 0u;
+        m.df_bytes = dF ? uint32_t(df_bytes) : 0u;
+        m.cb_bytes = uint32_t(int64_t(g.n_cams) * g.n_depth * g.feat_w * 8);
+        m.pairs_w = g.feat_w / kMCols;
+        m.blocks_h = (g.feat_h + kMRows - 1) / kMRows;
+        m.blocks_w = (g.feat_w + kBwdBlockCols - 1) / kBwdBlockCols;
+        const int part = (g.n_depth + kMWaves - 1) / kMWaves;
+        m.part = (part + kMChunk - 1) / kMChunk * kMChunk;
+        m.want_dp = dP != nullptr;
+        m.want_df = dF != nullptr;
+        const dim3 grid(g.n_cams * m.pairs_w * m.blocks_h, batch);
+        for (int c0 = 0; c0 < channels; c0 += kMSlice) {
+            m.c0 = c0;
+            m.cn = std::min(kMSlice, channels - c0);
+            m.accumulate_dp = c0 > 0;
+            const int tiles = (m.cn + 15) / 16;
+            switch (dtype) {
+                case BEVPOOL_F32: launch_mma<BEVPOOL_F32>(m, grid, tiles, stream); break;
+                case BEVPOOL_BF16: launch_mma<BEVPOOL_BF16>(m, grid, tiles, stream); break;
+                default: launch_mma<BEVPOOL_F16>(m, grid, tiles, stream); break;
+            }
+            BEVPOOL_HIP(hipGetLastError());
+        }
+    }
+    if (!run_rows) return BEVPOOL_OK;
+
     const int n_slices = (channels + kBwdSliceChannels - 1) / kBwdSliceChannels;
     const int slice_c = (channels + n_slices - 1) / n_slices;
     const int nch = (slice_c + 15) / 16;
@@ -350,6 +705,9 @@ int bevpool_launch_backward(const float *G, const void *P, const void *F,
     a.part = (g.n_depth + kBWaves - 1) / kBWaves;
     a.want_dp = dP != nullptr;
     a.want_df = dF != nullptr;
+    a.mixed = plan->bwd_mixed;
+    a.skip_clean = run_mma ? 1 : 0;
+    a.blocks_w8 = (g.feat_w + kBwdBlockCols - 1) / kBwdBlockCols;
     const dim3 grid(g.n_cams * a.items_w * a.items_h, batch);
     for (int s = 0; s < n_slices; ++s) {
         a.c0 = s * slice_c;

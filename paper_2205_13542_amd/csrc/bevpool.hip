@@ -38,6 +38,8 @@ void free_plan(bevpool_plan_s *plan) {
     (void)hipFree(plan->multi_cell);
     (void)hipFree(plan->multi_rows);
     (void)hipFree(plan->combo_cells);
+    (void)hipFree(plan->combo_cols);
+    (void)hipFree(plan->bwd_mixed);
     if (prev >= 0 && prev != plan->device) (void)hipSetDevice(prev);
     plan->magic = 0;
     delete plan;

@@ -42,6 +42,7 @@ constexpr int kColWidth = kFwdBlock / kGroupLanes;  // 8 columns per item
 constexpr int kGenHeavy = 256;
 constexpr int kSliceChannels = 128;             // channels per forward pass, at most
 constexpr int kBwdSliceChannels = 80;           // channels per backward pass
+constexpr int kBwdBlockCols = 8;                // pixel columns of a backward block
 constexpr int kCombineInline = 8;               // borrowed rows listed with each multi-combo cell
 
 // Column-table entry: {cell (single-combo cell) or borrowed row of its
@@ -88,6 +89,12 @@ struct bevpool_plan_s {
     // forward work partition
     int2 *column_table;      // [N][D][W]: {cell or borrowed row or -1, h_lo | h_hi << 16 | flags}
     int32_t *combo_cells;    // [N][D][W]: cell of a clean combo, -1 none kept, -2 not clean
+    int2 *combo_cols;        // [N][W][D]: {cell, kept rows h_lo | h_hi << 16} of a clean combo, else {-1, 0}
+    // backward work split: per camera and block of kBwdBlockCols pixel
+    // columns, 1 when a combo of the block is not clean (such blocks take
+    // the per-row kernel, the others the matrix-core kernel)
+    int32_t *bwd_mixed;      // [N][ceil(W / kBwdBlockCols)]
+    int32_t n_bwd_blocks, n_bwd_mixed;
     int32_t *multi_begin;    // [n_multi + 1]: first partial slot of each multi-combo cell
     int32_t *multi_cell;     // [n_multi]
     int32_t *multi_rows;     // [n_multi][kCombineInline]: borrowed rows of the first slots, or -1

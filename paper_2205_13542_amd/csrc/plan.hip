@@ -448,6 +448,39 @@ __global__ __launch_bounds__(kBlock) void k_planes_used(const int2 *table, int64
     if (t < n && table[t].x >= 0) atomicMax(planes, int32_t(t / n_combo) + 1);
 }
 
+// Clean combos by pixel column: entry (n, w, d) = {cell, rows} of combo
+// (n, d, w) when it is clean and its backward block holds no combo that is
+// not clean, else {-1, 0} (such blocks are left to the per-row kernel).
+__global__ __launch_bounds__(kBlock) void k_combo_cols(const int32_t *combo_cell,
+                                                       const int32_t *combo_range,
+                                                       const int32_t *mixed, int32_t n_combo,
+                                                       int32_t W, int32_t D, int32_t blocks_w,
+                                                       int2 *cols) {
+    const int32_t x = blockIdx.x * kBlock + threadIdx.x;
+    if (x >= n_combo) return;
+    const int32_t w = x % W, nd = x / W, d = nd % D, n = nd / D;
+    const int32_t c = combo_cell[x];
+    const bool clean = c >= 0 && mixed[n * blocks_w + w / kBwdBlockCols] == 0;
+    cols[(int64_t(n) * W + w) * D + d] = clean ? make_int2(c, combo_range[x]) : make_int2(-1, 0);
+}
+
+// Backward blocks (kBwdBlockCols pixel columns of one camera) that hold a
+// combo that is not clean: flagged 1 (every writer stores the same value).
+__global__ __launch_bounds__(kBlock) void k_bwd_flags(const int32_t *combo_cell, int32_t n_combo,
+                                                      int32_t W, int32_t D, int32_t blocks_w,
+                                                      int32_t *flags) {
+    const int32_t x = blockIdx.x * kBlock + threadIdx.x;
+    if (x >= n_combo || combo_cell[x] != -2) return;
+    const int32_t w = x % W, n = x / W / D;
+    flags[n * blocks_w + w / kBwdBlockCols] = 1;
+}
+
+__global__ __launch_bounds__(kBlock) void k_count_flags(const int32_t *flags, int32_t n,
+                                                        int32_t *count) {
+    const int32_t x = blockIdx.x * kBlock + threadIdx.x;
+    if (x < n && flags[x] != 0) atomicAdd(count, 1);
+}
+
 // Not enough empty rows to hold the partial sums: cells fed by several
 // combos become generic.
 __global__ __launch_bounds__(kBlock) void k_demote_multi(ComboArgs a, int32_t n_cells) {
@@ -734,7 +767,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
             const size_t cells1_b = Arena::piece((size_t(n_cells) + 1) * i4);
             const size_t combo1_b = Arena::piece((size_t(n_seg) + 1) * i4);
             arena.cap = Arena::piece(size_t(g.n_cams) * 16 * sizeof(double)) + 4 * sort_b +
-                        Arena::piece(size_t(sort_tiles_cap) * 256 * i4) + Arena::piece(12 * i4) +
+                        Arena::piece(size_t(sort_tiles_cap) * 256 * i4) + Arena::piece(16 * i4) +
                         Arena::piece(size_t(scan_sums_needed(sort_cap + 1)) * i4) +
                         5 * cells1_b +                 // flag_a, flag_b, cell_generic, cell_ncombo, run_begin
                         Arena::piece(size_t(n_cells) * i4) +          // pos_of_cell
@@ -752,8 +785,9 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         if ((rc2 = arena.take(&vals_b, size_t(sort_cap), "sort values"))) return rc2;
         if ((rc2 = arena.take(&hist, size_t(sort_tiles_cap) * 256, "radix histogram"))) return rc2;
         // [0..1] cell stats, [3] scan totals, [4..5] class counters, [6] most
-        // segments of a combo, [7] their kept points, [8..11] gathered counts
-        if ((rc2 = arena.take(&small, 12, "plan counters"))) return rc2;
+        // segments of a combo, [7] their kept points, [8..11] gathered counts,
+        // [12] backward blocks with a combo that is not clean
+        if ((rc2 = arena.take(&small, 16, "plan counters"))) return rc2;
         // the longest scan is over sort_cap + 1 elements (radix histograms
         // are shorter)
         if ((rc2 = arena.take(&scan_sums, size_t(scan_sums_needed(sort_cap + 1)), "scan chunk sums")))
@@ -761,7 +795,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         if ((rc2 = arena.take(&flag_a, size_t(n_cells) + 1, "flags"))) return rc2;
         if ((rc2 = arena.take(&flag_b, size_t(n_cells) + 1, "flags"))) return rc2;
 
-        fill(small, 12, 0);
+        fill(small, 16, 0);
         if (host_cells) {
             // a stored association: the cell map as exported, checked by the caller
             BEVPOOL_HIP(hipMemcpyAsync(plan->cell_of_point, host_cells, sizeof(int32_t) * size_t(np),
@@ -800,7 +834,8 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         BEVPOOL_HIP(hipGetLastError());
 
         // combos, cell classes and the column table
-        // the combo cells stay with the plan (the backward pass reads them)
+        // the combo cells and rows stay with the plan (the backward pass
+        // reads them)
         if ((rc2 = dev_alloc(&plan->combo_cells, size_t(n_combo), "combo cells"))) return rc2;
         combo_cell = plan->combo_cells;
         if ((rc2 = arena.take(&combo_range, size_t(n_combo), "combo ranges"))) return rc2;
@@ -897,6 +932,24 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         hipLaunchKernelGGL(k_planes_used, dim3(blocks_for(n_seg_act)), dim3(kBlock), 0, stream,
                            plan->column_table, n_seg_act, int32_t(n_combo), small + 2);
 
+        // the backward blocks holding a combo that is not clean, and the clean
+        // combos of the other blocks by pixel column
+        const int32_t bwd_bw = (W + kBwdBlockCols - 1) / kBwdBlockCols;
+        plan->n_bwd_blocks = N * bwd_bw;
+        if ((rc2 = dev_alloc(&plan->bwd_mixed, size_t(plan->n_bwd_blocks), "backward blocks")))
+            return rc2;
+        fill(plan->bwd_mixed, plan->n_bwd_blocks, 0);
+        hipLaunchKernelGGL(k_bwd_flags, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream,
+                           combo_cell, int32_t(n_combo), W, D, bwd_bw, plan->bwd_mixed);
+        fill(small + 12, 1, 0);
+        hipLaunchKernelGGL(k_count_flags, dim3(blocks_for(plan->n_bwd_blocks)), dim3(kBlock), 0,
+                           stream, plan->bwd_mixed, plan->n_bwd_blocks, small + 12);
+        if ((rc2 = dev_alloc(&plan->combo_cols, size_t(n_combo), "combos by column"))) return rc2;
+        hipLaunchKernelGGL(k_combo_cols, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream,
+                           combo_cell, combo_range, plan->bwd_mixed, int32_t(n_combo), W, D, bwd_bw,
+                           plan->combo_cols);
+        BEVPOOL_HIP(hipGetLastError());
+
         // cells without points, ascending
         if ((rc2 = dev_alloc(&plan->empty_cells, size_t(n_empty), "empty_cells"))) return rc2;
         hipLaunchKernelGGL(k_empty_list, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream, flag_b,
@@ -916,10 +969,12 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         }
         device_scan(head_scan, int64_t(n_part) + 1, small + 3, scan_sums, stream);
         BEVPOOL_HIP(hipGetLastError());
-        int32_t n_multi, n_planes;
+        int32_t n_multi, n_planes, n_mixed;
         if ((rc2 = to_host(&n_multi, head_scan + n_part))) return rc2;
         if ((rc2 = to_host(&n_planes, small + 2))) return rc2;
+        if ((rc2 = to_host(&n_mixed, small + 12))) return rc2;
         BEVPOOL_HIP(hipStreamSynchronize(stream));
+        plan->n_bwd_mixed = n_mixed;
         plan->n_multi = n_multi;
         plan->n_planes = n_planes > 0 ? n_planes : 1;
         if ((rc2 = dev_alloc(&plan->multi_begin, size_t(n_multi) + 1, "multi_begin"))) return rc2;

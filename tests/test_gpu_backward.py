@@ -2,6 +2,8 @@
 association). Bounds, per element: |dP - ref| <= 1e-4 sqrt(C) (a dot product
 of C terms of order one) and |dF - ref| <= 1e-4 sqrt(k), k the pixel's kept
 depth bins; dropped points and pixels without kept points exactly 0."""
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -168,4 +170,101 @@ def test_autograd_function_matches_oracle(torch_cuda, pkg, oracle_lib):
     bound = 1e-4 * np.sqrt(np.maximum(k, 1))[None, :, None]
     got = F.grad.cpu().numpy().reshape(w.batch, w.rig.n_pixels, w.channels)
     assert (np.abs(got - refF.reshape(got.shape)) <= bound).all()
+    plan.close()
+
+
+# ------------------------------------------------------------ matrix-core path
+#
+# Level rigs send every block to the matrix-core kernel when the channel count
+# is a multiple of 4 and the rows are aligned; otherwise, and for blocks with a
+# combo that is not clean, the per-row kernel runs.
+
+from test_gpu_parity import RIGS  # noqa: E402
+
+
+def _rig_workload(rig, channels, seed, batch=1, dtype="f32"):
+    P, F = wl.frames(rig, channels, batch, "peaked", seed=seed, dtype=dtype)
+    return wl.Workload("c", rig, channels, batch, dtype, P, F)
+
+
+@pytest.mark.parametrize("channels", [4, 16, 48, 64, 80, 84, 160, 200, 5, 17, 81])
+def test_backward_level_channel_counts(torch_cuda, pkg, oracle_lib, channels):
+    """Matrix-core launches of 1..5 channel tiles, a ragged last tile (84,
+    200: slices of 80 then 4 or 40), several slices adding into dP (160,
+    200); 5, 17 and 81 channels take the per-row kernel."""
+    _say(f"[backward level] nuscenes C={channels}")
+    w = _rig_workload(wl.ring_rig(), channels, seed=channels)
+    _check(torch_cuda, pkg, oracle_lib, w, _grad(w, channels + 1))
+
+
+@pytest.mark.parametrize("name", ["odd", "odd_tilted", "anisotropic", "coarse", "coarse_tilted",
+                                  "one_cell", "empty", "tiny_identity"])
+@pytest.mark.parametrize("channels", [8, 20])
+def test_backward_edge_rigs(torch_cuda, pkg, oracle_lib, name, channels):
+    """Odd sizes (27 columns: the last column pair has one column; 13 rows: a
+    partial row block; 37 bins: partial depth steps), an empty grid, one
+    cell, and cells fed by many combos."""
+    _say(f"[backward edge] {name} C={channels}")
+    w = _rig_workload(RIGS[name](), channels, seed=channels + 3)
+    _check(torch_cuda, pkg, oracle_lib, w, _grad(w, channels + 7))
+
+
+def _one_tilted_camera_rig():
+    """The ring rig with camera 0 pitched 5 degrees: its blocks hold combos
+    that are not clean, the other cameras' blocks are all clean."""
+    base = wl.ring_rig()
+    tilted = wl.tilt_rig(base, 5.0, 2.0)
+    E = base.extrinsics.copy()
+    E[0] = tilted.extrinsics[0]
+    return dataclasses.replace(base, extrinsics=E)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_backward_mixed_blocks(torch_cuda, pkg, oracle_lib, dtype):
+    """One call runs both kernels on disjoint blocks."""
+    _say(f"[backward mixed] one tilted camera {dtype}")
+    w = _rig_workload(_one_tilted_camera_rig(), 80, seed=21, batch=2, dtype=dtype)
+    _check(torch_cuda, pkg, oracle_lib, w, _grad(w, 22), dtype=dtype)
+
+
+def test_backward_highres(torch_cuda, pkg, oracle_lib):
+    """6 x 236 bins x 64 x 176, C = 128 (slices of 80 and 48 channels)."""
+    _say("[backward highres] C=128")
+    w = wl.make("highres", seed=3)
+    _check(torch_cuda, pkg, oracle_lib, w, _grad(w, 23))
+
+
+def test_backward_unaligned_features(torch_cuda, pkg, oracle_lib):
+    """F one element past a 16-byte boundary: the per-row kernel takes every
+    block; the result matches the aligned call within the bounds."""
+    torch = torch_cuda
+    _say("[backward] unaligned F")
+    w = _rig_workload(wl.ring_rig(), 80, seed=24)
+    plan = pkg.Plan.from_rig(w.rig)
+    P = _dev(torch, w.P, "f32")
+    buf = torch.empty(w.F.size + 1, dtype=torch.float32, device="cuda")
+    buf[1:] = torch.from_numpy(w.F.reshape(-1)).cuda()
+    F_un = buf[1:].view(w.F.shape)
+    G = torch.from_numpy(_grad(w, 25)).cuda()
+    gd, gf = plan.backward(G, P, F_un)
+    torch.cuda.synchronize()
+    cop = oracle_lib.cell_map(w.rig)
+    refP, refF = oracle_lib.backward(w.rig, cop, w.P, w.F, _grad(w, 25))
+    assert (np.abs(gd.cpu().numpy().astype(np.float64) - refP) <= 1e-4 * np.sqrt(80)).all()
+    k = (cop >= 0).reshape(w.rig.n_cams, w.rig.n_depth, -1).sum(axis=1).reshape(-1)
+    bound = 1e-4 * np.sqrt(np.maximum(k, 1))[None, :, None]
+    got = gf.cpu().numpy().reshape(1, w.rig.n_pixels, 80)
+    assert (np.abs(got - refF.reshape(got.shape)) <= bound).all()
+    plan.close()
+
+
+def test_backward_level_deterministic(torch_cuda, pkg):
+    torch = torch_cuda
+    w = wl.make("nuscenes", seed=26)
+    plan = pkg.Plan.from_rig(w.rig)
+    P, F = _dev(torch, w.P, "f32"), _dev(torch, w.F, "f32")
+    G = torch.from_numpy(_grad(w, 27)).cuda()
+    a = plan.backward(G, P, F)
+    b = plan.backward(G, P, F)
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
     plan.close()
