@@ -290,13 +290,24 @@ __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0,
     // Touch the second launch's plan arrays (after this item's own loads):
     // item i reads words i * kFwdBlock + t, i * kFwdBlock + t + kFwdBlock *
     // n_items, ... of each. The values are only kept live until the end.
+    // The first word of each array is loaded without a wait (an offset past
+    // the array reads 0) and consumed only at the end; further words (grids
+    // with more plan entries than threads) are read in a loop.
     int warm = 0;
+    int wfirst[kWarmArrays];
+#pragma unroll
+    for (int q = 0; q < kWarmArrays; ++q) wfirst[q] = 0;
     if (blockIdx.y == 0 && blockIdx.z == 0) {
         const int stride = a.n_items * kFwdBlock;
+        const int i0 = item * kFwdBlock + int(threadIdx.x);
+#pragma unroll
+        for (int q = 0; q < kWarmArrays; ++q) {
+            const Rsrc wr = make_rsrc(a.warm[q], uint32_t(a.warm_n[q]) * 4u);
+            wfirst[q] = int(__builtin_amdgcn_raw_buffer_load_b32(wr, i0 < a.warm_n[q] ? i0 * 4 : int(kOff), 0, 0));
+        }
 #pragma unroll
         for (int q = 0; q < kWarmArrays; ++q)
-            for (int i = item * kFwdBlock + int(threadIdx.x); i < a.warm_n[q]; i += stride)
-                warm ^= a.warm[q][i];
+            for (int i = i0 + stride; i < a.warm_n[q]; i += stride) warm ^= a.warm[q][i];
     }
 
     // Row segments (SEG): a combo whose kept rows fall into several cells
@@ -438,7 +449,7 @@ __device__ void column_item(const FwdArgs &a, const Frame &fr, int item, int c0,
     } else {
         Emit<0, NCH, VEC>::run(acc, e.x, e.y, dm, fr.O, uint32_t(c0) * 4u, a.ldo, mean, tail_ok);
     }
-    asm volatile("" ::"v"(warm));   // the touched words are not needed, only loaded
+    asm volatile("" ::"v"(warm ^ wfirst[0] ^ wfirst[1] ^ wfirst[2] ^ wfirst[3]));   // only loaded, not needed
 }
 
 // A generic cell's runs in chunks of 64: lane i loads run i of the chunk and
