@@ -755,6 +755,11 @@ def main():
                        "outer_events_mean": round(float(np.mean(outer_ms)) * 1e3, 2),
                        "warm_mean": round(warm_ms * 1e3, 2)},
         "algorithmic_bytes": nbytes,
+        # the HBM bytes the counters measured for these kernel sources, per
+        # unit time and against the algorithmic bytes
+        "counter_traffic": None if traffic is None else {
+            "bytes": traffic, "GBps": round(traffic / (mean_ms * 1e-3) / 1e9, 2),
+            "vs_algorithmic": round(traffic / nbytes, 3)},
         "plan_bytes_read": 8 * info.n_planes * info.n_cams * info.n_depth * info.feat_w
                            + 16 * info.n_generic
                            + 16 * info.n_runs + 4 * info.n_empty
