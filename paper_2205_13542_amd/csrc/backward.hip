@@ -131,32 +131,48 @@ struct RowTerms<kBRows, NCH> {
 };
 
 // The same for a combo that is not clean: row R reads the gradient row of
-// its own cell (lane R's cell of the group), if it has one.
-template <int R, int NCH, bool VEC>
-struct RowTermsEach {
-    static __device__ __forceinline__ void run(float (&acc)[kBRows][NCH], float (&dot)[kBRows],
-                                               const Row<NCH> (&f)[kBRows], Rsrc G, uint32_t g_ch,
-                                               int C, int cell, float pv) {
-        const int c = row_bcast<R>(cell);
-        Row<NCH> g;
-        load_row<BEVPOOL_F32, NCH, VEC>(g, G, c >= 0 ? uint32_t(c) * uint32_t(C) * 4u + g_ch : kOff);
+// its own cell (lane R's cell of the group), if it has one. The rows' loads
+// are issued kBEach at a time before their terms, so that one round trip
+// serves them (loading and using each row in turn made every row wait for
+// all loads in flight).
+constexpr int kBEach = 4;
+template <int R0, int U, int NCH, bool VEC>
+__device__ __forceinline__ void each_loads(Row<NCH> (&g)[kBEach], Rsrc G, uint32_t g_ch, int C, int cell) {
+    if constexpr (U < kBEach) {
+        const int c = row_bcast<R0 + U>(cell);
+        const uint32_t addr = uint32_t(max(c, 0)) * uint32_t(C) * 4u + g_ch;
+        load_row<BEVPOOL_F32, NCH, VEC>(g[U], G, c >= 0 ? addr : kOff);
+        each_loads<R0, U + 1, NCH, VEC>(g, G, g_ch, C, cell);
+    }
+}
+template <int R0, int U, int NCH>
+__device__ __forceinline__ void each_terms(float (&acc)[kBRows][NCH], float (&dot)[kBRows],
+                                           const Row<NCH> (&f)[kBRows], const Row<NCH> (&g)[kBEach],
+                                           float pv) {
+    if constexpr (U < kBEach) {
+        constexpr int R = R0 + U;
         const float p = row_bcast<R>(pv);
         float s = 0.f;
 #pragma unroll
         for (int k = 0; k < NCH; ++k) {
-            acc[R][k] = __builtin_fmaf(p, g.v[k], acc[R][k]);
-            s = __builtin_fmaf(f[R].v[k], g.v[k], s);
+            acc[R][k] = __builtin_fmaf(p, g[U].v[k], acc[R][k]);
+            s = __builtin_fmaf(f[R].v[k], g[U].v[k], s);
         }
         dot[R] = s;
-        RowTermsEach<R + 1, NCH, VEC>::run(acc, dot, f, G, g_ch, C, cell, pv);
+        each_terms<R0, U + 1, NCH>(acc, dot, f, g, pv);
     }
-};
-template <int NCH, bool VEC>
-struct RowTermsEach<kBRows, NCH, VEC> {
-    static __device__ __forceinline__ void run(float (&)[kBRows][NCH], float (&)[kBRows],
-                                               const Row<NCH> (&)[kBRows], Rsrc, uint32_t, int, int,
-                                               float) {}
-};
+}
+template <int R0, int NCH, bool VEC>
+__device__ __forceinline__ void row_terms_each(float (&acc)[kBRows][NCH], float (&dot)[kBRows],
+                                               const Row<NCH> (&f)[kBRows], Rsrc G, uint32_t g_ch,
+                                               int C, int cell, float pv) {
+    if constexpr (R0 < kBRows) {
+        Row<NCH> g[kBEach];
+        each_loads<R0, 0, NCH, VEC>(g, G, g_ch, C, cell);
+        each_terms<R0, 0, NCH>(acc, dot, f, g, pv);
+        row_terms_each<R0 + kBEach, NCH, VEC>(acc, dot, f, G, g_ch, C, cell, pv);
+    }
+}
 
 template <int NCH>
 constexpr int bwd_stride() { return kBRows * NCH * 16 + 16; }   // one lane group's dF sums in LDS
@@ -248,7 +264,7 @@ __global__ __launch_bounds__(kBBlock) void k_backward(BwdArgs a) {
                 if (st[u].cc >= 0) {
                     RowTerms<0, NCH>::run(acc, dot, f, st[u].g, pv);
                 } else if (st[u].cc == -2) {
-                    RowTermsEach<0, NCH, VEC>::run(acc, dot, f, G, g_ch, a.C, st[u].cell, pv);
+                    row_terms_each<0, NCH, VEC>(acc, dot, f, G, g_ch, a.C, st[u].cell, pv);
                 } else {
 #pragma unroll
                     for (int r = 0; r < kBRows; ++r) dot[r] = 0.f;
