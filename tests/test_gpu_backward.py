@@ -198,12 +198,12 @@ def test_backward_level_channel_counts(torch_cuda, pkg, oracle_lib, channels):
 
 
 @pytest.mark.parametrize("name", ["odd", "odd_tilted", "anisotropic", "coarse", "coarse_tilted",
-                                  "one_cell", "empty", "tiny_identity"])
+                                  "one_cell", "empty", "tiny_identity", "tall"])
 @pytest.mark.parametrize("channels", [8, 20])
 def test_backward_edge_rigs(torch_cuda, pkg, oracle_lib, name, channels):
     """Odd sizes (27 columns: the last column pair has one column; 13 rows: a
     partial row block; 37 bins: partial depth steps), an empty grid, one
-    cell, and cells fed by many combos."""
+    cell, cells fed by many combos, and 16,400 rows (no clean combo)."""
     _say(f"[backward edge] {name} C={channels}")
     w = _rig_workload(RIGS[name](), channels, seed=channels + 3)
     _check(torch_cuda, pkg, oracle_lib, w, _grad(w, channels + 7))

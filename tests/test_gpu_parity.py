@@ -86,6 +86,17 @@ def _one_cell_rig():
                                cell_x=16.0, cell_y=16.0)
 
 
+def _tall_rig():
+    """The tiny camera with a feature map of 16,400 rows (more than the 2^14
+    that the column table's row fields hold), 3 columns and 3 depth bins:
+    every combo is geometrically clean (a level camera), but no combo can be
+    column-served, so every cell takes the gathered path (16,400 or 32,800
+    points each)."""
+    H, W = 16400, 3
+    return dataclasses.replace(wl.tiny_rig(), feat_h=H, feat_w=W, n_depth=3,
+                               intrinsics=np.array([[1.5, H / 2.0, W / 2.0, H / 2.0]]))
+
+
 RIGS = {
     "tiny": wl.tiny_rig, "tiny_identity": wl.identity_rig, "nuscenes": wl.ring_rig,
     "nuscenes_tilted": lambda: wl.tilt_rig(wl.ring_rig()), "highres": lambda: wl.ring_rig(2),
@@ -94,7 +105,7 @@ RIGS = {
     "anisotropic": _anisotropic_rig, "coarse": _coarse_rig, "coarse_tilted": _coarse_tilted_rig,
     "empty": _empty_rig,
     "odd": lambda: _odd_rig(False), "odd_tilted": lambda: _odd_rig(True),
-    "one_cell": _one_cell_rig,
+    "one_cell": _one_cell_rig, "tall": _tall_rig,
 }
 
 
@@ -217,7 +228,7 @@ def test_forward_highres(torch_cuda, pkg, oracle_lib, oracle_plans):
 
 
 @pytest.mark.parametrize("name", ["coarse", "coarse_tilted", "anisotropic", "empty", "one_cell",
-                                  "odd", "odd_tilted"])
+                                  "odd", "odd_tilted", "tall"])
 def test_forward_edge_rigs(torch_cuda, pkg, oracle_lib, oracle_plans, name):
     _say(f"[forward edge] {name}")
     rig = RIGS[name]()
@@ -242,6 +253,10 @@ def test_forward_edge_rigs(torch_cuda, pkg, oracle_lib, oracle_plans, name):
         assert plan.info.n_kept > 0 and plan.info.n_column > 0
         if name == "odd_tilted":
             assert plan.info.n_generic > 0
+    if name == "tall":
+        counts = np.diff(cs)
+        assert plan.info.n_column == 0 and plan.info.n_generic == int((counts > 0).sum())
+        assert plan.info.max_per_cell == int(counts.max()) >= rig.feat_h
 
 
 @pytest.mark.parametrize("rig_name", ["nuscenes", "nuscenes_tilted", "nuscenes_tilt1"])
@@ -399,7 +414,7 @@ def test_plan_used_on_another_device_is_rejected(torch_cuda, pkg):
 
 
 @pytest.mark.parametrize("name", ["nuscenes", "nuscenes_tilted", "nuscenes_tilt1", "coarse",
-                                  "anisotropic", "tiny"])
+                                  "anisotropic", "tiny", "tall"])
 def test_plan_partition_counts(pkg, oracle_plans, name):
     """Every cell is column-served, generic or empty; the level rig has no
     generic cell at all."""
