@@ -296,14 +296,46 @@ __global__ __launch_bounds__(kBlock) void k_cell_start(const uint32_t *skeys, in
     for (int64_t c = prev + 1; c <= cur; ++c) cell_start[c] = int32_t(i);
 }
 
+// Counters shared by the whole grid (counts, maxima) are reduced in the
+// workgroup first and updated by one atomic per workgroup, and the kernels
+// that update them run a capped grid over their elements: atomics on one
+// address are performed one after another, so one per wave (what the
+// compiler makes of per-thread updates) would cost tens of microseconds.
+constexpr int kReduceBlocks = 256;
+
+// Workgroup sum (MAX: maximum) of one value per thread; every thread of the
+// workgroup calls it, the result is valid in thread 0. s_red holds kWaves
+// words and is not reused by another call before a barrier.
+template <bool MAX>
+__device__ __forceinline__ int32_t block_reduce(int32_t v, int32_t *s_red) {
+#pragma unroll
+    for (int o = kWaveSize / 2; o > 0; o >>= 1) {
+        const int32_t u = __shfl_xor(v, o, kWaveSize);
+        v = MAX ? max(v, u) : v + u;
+    }
+    if ((threadIdx.x & (kWaveSize - 1)) == 0) s_red[threadIdx.x / kWaveSize] = v;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) v = MAX ? max(v, s_red[w]) : v + s_red[w];
+    }
+    return v;
+}
+
 __global__ __launch_bounds__(kBlock) void k_cell_stats(const int32_t *cell_start, int32_t n_cells,
                                                        int32_t *stats /* nonempty, max */) {
-    const int32_t c = blockIdx.x * kBlock + threadIdx.x;
-    if (c >= n_cells) return;
-    const int32_t cnt = cell_start[c + 1] - cell_start[c];
-    if (cnt > 0) {
-        atomicAdd(&stats[0], 1);
-        atomicMax(&stats[1], cnt);
+    __shared__ int32_t s_n[kWaves], s_m[kWaves];
+    int32_t nonempty = 0, most = 0;
+    for (int32_t c = blockIdx.x * kBlock + threadIdx.x; c < n_cells; c += gridDim.x * kBlock) {
+        const int32_t cnt = cell_start[c + 1] - cell_start[c];
+        nonempty += cnt > 0 ? 1 : 0;
+        most = max(most, cnt);
+    }
+    nonempty = block_reduce<false>(nonempty, s_n);
+    most = block_reduce<true>(most, s_m);
+    if (threadIdx.x == 0) {
+        if (nonempty > 0) atomicAdd(&stats[0], nonempty);
+        if (most > 0) atomicMax(&stats[1], most);
     }
 }
 
@@ -347,34 +379,48 @@ struct ComboArgs {
 // segments: maximal runs of consecutive kept rows in one cell. A combo with
 // at most `planes` segments is served by the column items, one segment per
 // pass (a level camera gives every combo one segment: a clean combo);
-// otherwise its cells are generic.
-__global__ __launch_bounds__(kBlock) void k_combo_walk(ComboArgs a) {
-    const int64_t x = int64_t(blockIdx.x) * kBlock + threadIdx.x;
-    const int64_t n_combo = int64_t(a.N) * a.D * a.W;
-    if (x >= n_combo) return;
-    const int32_t X = int32_t(x);
+// otherwise its cells are generic. The rows are loaded kWalkRows at a time
+// before they are walked (rows past H read row H - 1 and count as dropped),
+// so one round trip serves kWalkRows rows.
+constexpr int kWalkRows = 16;
+
+__device__ __forceinline__ void walk_rows(const ComboArgs &a, int64_t base, int32_t h0,
+                                          int32_t (&cc)[kWalkRows]) {
+#pragma unroll
+    for (int u = 0; u < kWalkRows; ++u)
+        cc[u] = a.cell_of_point[base + int64_t(min(h0 + u, a.H - 1)) * a.W];
+}
+
+__device__ __forceinline__ void combo_walk_one(const ComboArgs &a, int32_t X, int64_t n_combo,
+                                               int32_t &max_seg, int32_t &served_pts) {
     const int32_t w = X % a.W, nd = X / a.W;
     const int64_t base = int64_t(nd) * a.H * a.W + w;
     int32_t cell[kMaxSeg], lo[kMaxSeg], hi[kMaxSeg];
     int32_t n_seg = 0, cur = -1, first = -1, last = -1, kept = 0;
-    for (int32_t h = 0; h < a.H; ++h) {
-        const int32_t c = a.cell_of_point[base + int64_t(h) * a.W];
-        if (c < 0) {
-            cur = -1;
-            continue;
-        }
-        ++kept;
-        if (first < 0) first = h;
-        last = h;
-        if (c != cur) {
-            if (n_seg < a.planes) {
-                cell[n_seg] = c;
-                lo[n_seg] = h;
+    for (int32_t h0 = 0; h0 < a.H; h0 += kWalkRows) {
+        int32_t cc[kWalkRows];
+        walk_rows(a, base, h0, cc);
+#pragma unroll
+        for (int u = 0; u < kWalkRows; ++u) {
+            const int32_t h = h0 + u;
+            const int32_t c = h < a.H ? cc[u] : -1;
+            if (c < 0) {
+                cur = -1;
+            } else {
+                ++kept;
+                if (first < 0) first = h;
+                last = h;
+                if (c != cur) {
+                    if (n_seg < a.planes) {
+                        cell[n_seg] = c;
+                        lo[n_seg] = h;
+                    }
+                    ++n_seg;
+                    cur = c;
+                }
+                if (n_seg <= a.planes) hi[n_seg - 1] = h + 1;
             }
-            ++n_seg;
-            cur = c;
         }
-        if (n_seg <= a.planes) hi[n_seg - 1] = h + 1;
     }
     for (int s = 0; s < a.planes; ++s) a.seg_cell[int64_t(s) * n_combo + X] = -1;
     if (n_seg == 0) {
@@ -388,17 +434,35 @@ __global__ __launch_bounds__(kBlock) void k_combo_walk(ComboArgs a) {
             a.seg_range[int64_t(s) * n_combo + X] = lo[s] | (hi[s] << 16);
             atomicAdd(&a.cell_ncombo[cell[s]], 1);
         }
-        atomicMax(a.max_seg, n_seg);
-        atomicAdd(a.served_pts, kept);
+        max_seg = max(max_seg, n_seg);
+        served_pts += kept;
         a.combo_cell[X] = n_seg == 1 ? cell[0] : -2;
         a.combo_range[X] = n_seg == 1 ? (lo[0] | (hi[0] << 16)) : 0;
     } else {
         a.combo_cell[X] = -2;
         a.combo_range[X] = 0;
-        for (int32_t h = first; h <= last; ++h) {
-            const int32_t c = a.cell_of_point[base + int64_t(h) * a.W];
-            if (c >= 0) atomicOr(&a.cell_generic[c], 1);
+        for (int32_t h0 = first; h0 <= last; h0 += kWalkRows) {
+            int32_t cc[kWalkRows];
+            walk_rows(a, base, h0, cc);
+#pragma unroll
+            for (int u = 0; u < kWalkRows; ++u)
+                if (h0 + u <= last && cc[u] >= 0) atomicOr(&a.cell_generic[cc[u]], 1);
         }
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void k_combo_walk(ComboArgs a) {
+    __shared__ int32_t s_m[kWaves], s_p[kWaves];
+    const int64_t n_combo = int64_t(a.N) * a.D * a.W;
+    int32_t max_seg = 0, served_pts = 0;
+    for (int64_t x = int64_t(blockIdx.x) * kBlock + threadIdx.x; x < n_combo;
+         x += int64_t(gridDim.x) * kBlock)
+        combo_walk_one(a, int32_t(x), n_combo, max_seg, served_pts);
+    max_seg = block_reduce<true>(max_seg, s_m);
+    served_pts = block_reduce<false>(served_pts, s_p);
+    if (threadIdx.x == 0) {
+        if (max_seg > 0) atomicMax(a.max_seg, max_seg);
+        if (served_pts > 0) atomicAdd(a.served_pts, served_pts);
     }
 }
 
@@ -407,14 +471,22 @@ __global__ __launch_bounds__(kBlock) void k_combo_walk(ComboArgs a) {
 __global__ __launch_bounds__(kBlock) void k_cell_class(ComboArgs a, const int32_t *cell_start,
                                                        int32_t n_cells, int32_t *generic_flag,
                                                        int32_t *empty_flag, int32_t *counters) {
-    const int32_t c = blockIdx.x * kBlock + threadIdx.x;
-    if (c >= n_cells) return;
-    const int32_t cnt = cell_start[c + 1] - cell_start[c];
-    const bool served = cnt > 0 && a.cell_generic[c] == 0;
-    generic_flag[c] = (cnt > 0 && !served) ? 1 : 0;
-    empty_flag[c] = cnt == 0 ? 1 : 0;
-    if (served) atomicAdd(&counters[0], 1);
-    if (cnt > kGenHeavy && !served) atomicAdd(&counters[1], 1);
+    __shared__ int32_t s_s[kWaves], s_h[kWaves];
+    int32_t n_served = 0, n_heavy = 0;
+    for (int32_t c = blockIdx.x * kBlock + threadIdx.x; c < n_cells; c += gridDim.x * kBlock) {
+        const int32_t cnt = cell_start[c + 1] - cell_start[c];
+        const bool served = cnt > 0 && a.cell_generic[c] == 0;
+        generic_flag[c] = (cnt > 0 && !served) ? 1 : 0;
+        empty_flag[c] = cnt == 0 ? 1 : 0;
+        n_served += served ? 1 : 0;
+        n_heavy += (cnt > kGenHeavy && !served) ? 1 : 0;
+    }
+    n_served = block_reduce<false>(n_served, s_s);
+    n_heavy = block_reduce<false>(n_heavy, s_h);
+    if (threadIdx.x == 0) {
+        if (n_served > 0) atomicAdd(&counters[0], n_served);
+        if (n_heavy > 0) atomicAdd(&counters[1], n_heavy);
+    }
 }
 
 // Column table entries, one plane per segment index, and a flag on each
@@ -444,8 +516,12 @@ __global__ __launch_bounds__(kBlock) void k_clear_table(int2 *table, int64_t n) 
 // an entry.
 __global__ __launch_bounds__(kBlock) void k_planes_used(const int2 *table, int64_t n,
                                                         int32_t n_combo, int32_t *planes) {
-    const int64_t t = int64_t(blockIdx.x) * kBlock + threadIdx.x;
-    if (t < n && table[t].x >= 0) atomicMax(planes, int32_t(t / n_combo) + 1);
+    __shared__ int32_t s_m[kWaves];
+    int32_t most = 0;
+    for (int64_t t = int64_t(blockIdx.x) * kBlock + threadIdx.x; t < n; t += int64_t(gridDim.x) * kBlock)
+        if (table[t].x >= 0) most = max(most, int32_t(t / n_combo) + 1);
+    most = block_reduce<true>(most, s_m);
+    if (threadIdx.x == 0 && most > 0) atomicMax(planes, most);
 }
 
 // Clean combos by pixel column: entry (n, w, d) = {cell, rows} of combo
@@ -621,6 +697,8 @@ __global__ __launch_bounds__(kBlock) void k_generic_runs(const int32_t *sorted_p
 }
 
 int blocks_for(int64_t n) { return int((n + kBlock - 1) / kBlock); }
+// Grid of a kernel that reduces into shared counters (at least one workgroup).
+int reduce_blocks(int64_t n) { return std::max(1, std::min(blocks_for(n), kReduceBlocks)); }
 
 template <typename T>
 int dev_alloc(T **p, size_t count, const char *what) {
@@ -829,7 +907,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         if ((rc2 = radix_sort(keys_a, plan->sorted_point, np, bits_for(n_cells)))) return rc2;
         hipLaunchKernelGGL(k_cell_start, dim3(blocks_for(int64_t(np) + 1)), dim3(kBlock), 0,
                            stream, keys_a, np, n_cells, plan->cell_start);
-        hipLaunchKernelGGL(k_cell_stats, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream,
+        hipLaunchKernelGGL(k_cell_stats, dim3(reduce_blocks(n_cells)), dim3(kBlock), 0, stream,
                            plan->cell_start, n_cells, small);
         BEVPOOL_HIP(hipGetLastError());
 
@@ -863,7 +941,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         ca.seg_range = seg_range;
         ca.max_seg = small + 6;
         ca.served_pts = small + 7;
-        hipLaunchKernelGGL(k_combo_walk, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream, ca);
+        hipLaunchKernelGGL(k_combo_walk, dim3(reduce_blocks(n_combo)), dim3(kBlock), 0, stream, ca);
         hipLaunchKernelGGL(k_clear_table, dim3(blocks_for(n_seg)), dim3(kBlock), 0, stream,
                            plan->column_table, n_seg);
         int32_t stats[4], counters[2], n_gen = 0, n_empty = 0, kept = 0, n_part = 0;
@@ -872,7 +950,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
             fill(flag_b, int64_t(n_cells) + 1, 0);
             fill(combo_flag, n_seg_act + 1, 0);
             fill(small + 4, 2, 0);
-            hipLaunchKernelGGL(k_cell_class, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream, ca,
+            hipLaunchKernelGGL(k_cell_class, dim3(reduce_blocks(n_cells)), dim3(kBlock), 0, stream, ca,
                                plan->cell_start, n_cells, flag_a, flag_b, small + 4);
             hipLaunchKernelGGL(k_combo_table, dim3(blocks_for(n_seg_act)), dim3(kBlock), 0, stream,
                                ca, plan->column_table, combo_flag);
@@ -910,7 +988,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
             fill(cell_generic, n_cells, 0);
             fill(cell_ncombo, n_cells, 0);
             fill(small + 6, 2, 0);
-            hipLaunchKernelGGL(k_combo_walk, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream, ca);
+            hipLaunchKernelGGL(k_combo_walk, dim3(reduce_blocks(n_combo)), dim3(kBlock), 0, stream, ca);
             if ((rc2 = classify())) return rc2;
         }
         if (n_part > n_empty) {
@@ -929,7 +1007,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         // planes in use, from the final table (cells demoted to generic leave
         // their segments' planes empty)
         fill(small + 2, 1, 0);
-        hipLaunchKernelGGL(k_planes_used, dim3(blocks_for(n_seg_act)), dim3(kBlock), 0, stream,
+        hipLaunchKernelGGL(k_planes_used, dim3(reduce_blocks(n_seg_act)), dim3(kBlock), 0, stream,
                            plan->column_table, n_seg_act, int32_t(n_combo), small + 2);
 
         // the backward blocks holding a combo that is not clean, and the clean
