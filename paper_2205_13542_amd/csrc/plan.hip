@@ -322,11 +322,16 @@ __device__ __forceinline__ int32_t block_reduce(int32_t v, int32_t *s_red) {
     return v;
 }
 
+// Non-empty cells and the largest interval; clears two per-cell arrays
+// (the combo walk's counters) on the way.
 __global__ __launch_bounds__(kBlock) void k_cell_stats(const int32_t *cell_start, int32_t n_cells,
-                                                       int32_t *stats /* nonempty, max */) {
+                                                       int32_t *stats /* nonempty, max */,
+                                                       int32_t *clear_a, int32_t *clear_b) {
     __shared__ int32_t s_n[kWaves], s_m[kWaves];
     int32_t nonempty = 0, most = 0;
     for (int32_t c = blockIdx.x * kBlock + threadIdx.x; c < n_cells; c += gridDim.x * kBlock) {
+        clear_a[c] = 0;
+        clear_b[c] = 0;
         const int32_t cnt = cell_start[c + 1] - cell_start[c];
         nonempty += cnt > 0 ? 1 : 0;
         most = max(most, cnt);
@@ -466,12 +471,17 @@ __global__ __launch_bounds__(kBlock) void k_combo_walk(ComboArgs a) {
     }
 }
 
-// Per cell: generic flag, empty flag; counters[0] += column-served cells,
-// counters[1] += heavy generic cells.
+// Per cell: generic flag, empty flag (both arrays n_cells + 1 long, the
+// last entry 0); counters[0] += column-served cells, counters[1] += heavy
+// generic cells.
 __global__ __launch_bounds__(kBlock) void k_cell_class(ComboArgs a, const int32_t *cell_start,
                                                        int32_t n_cells, int32_t *generic_flag,
                                                        int32_t *empty_flag, int32_t *counters) {
     __shared__ int32_t s_s[kWaves], s_h[kWaves];
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        generic_flag[n_cells] = 0;   // the flags are scanned over n_cells + 1 entries
+        empty_flag[n_cells] = 0;
+    }
     int32_t n_served = 0, n_heavy = 0;
     for (int32_t c = blockIdx.x * kBlock + threadIdx.x; c < n_cells; c += gridDim.x * kBlock) {
         const int32_t cnt = cell_start[c + 1] - cell_start[c];
@@ -490,10 +500,13 @@ __global__ __launch_bounds__(kBlock) void k_cell_class(ComboArgs a, const int32_
 }
 
 // Column table entries, one plane per segment index, and a flag on each
-// segment of a cell fed by several segments.
+// segment of a cell fed by several segments (one more entry, 0, ends the
+// flags).
 __global__ __launch_bounds__(kBlock) void k_combo_table(ComboArgs a, int2 *table, int32_t *multi_flag) {
     const int64_t t = int64_t(blockIdx.x) * kBlock + threadIdx.x;
-    if (t >= int64_t(a.planes) * a.N * a.D * a.W) return;
+    const int64_t n = int64_t(a.planes) * a.N * a.D * a.W;
+    if (t == 0) multi_flag[n] = 0;   // scanned over n + 1 entries
+    if (t >= n) return;
     const int32_t c = a.seg_cell[t];
     int2 e = make_int2(-1, 0);
     bool multi = false;
@@ -542,19 +555,24 @@ __global__ __launch_bounds__(kBlock) void k_combo_cols(const int32_t *combo_cell
 
 // Backward blocks (kBwdBlockCols pixel columns of one camera) that hold a
 // combo that is not clean: flagged 1 (every writer stores the same value).
-__global__ __launch_bounds__(kBlock) void k_bwd_flags(const int32_t *combo_cell, int32_t n_combo,
-                                                      int32_t W, int32_t D, int32_t blocks_w,
-                                                      int32_t *flags) {
-    const int32_t x = blockIdx.x * kBlock + threadIdx.x;
-    if (x >= n_combo || combo_cell[x] != -2) return;
-    const int32_t w = x % W, n = x / W / D;
-    flags[n * blocks_w + w / kBwdBlockCols] = 1;
-}
-
-__global__ __launch_bounds__(kBlock) void k_count_flags(const int32_t *flags, int32_t n,
-                                                        int32_t *count) {
-    const int32_t x = blockIdx.x * kBlock + threadIdx.x;
-    if (x < n && flags[x] != 0) atomicAdd(count, 1);
+// One workgroup per backward block (camera n, kBwdBlockCols pixel columns):
+// flags[block] = 1 when one of its combos is not clean, and *count adds the
+// flagged blocks.
+__global__ __launch_bounds__(kBlock) void k_bwd_blocks(const int32_t *combo_cell, int32_t W,
+                                                       int32_t D, int32_t blocks_w, int32_t *flags,
+                                                       int32_t *count) {
+    __shared__ int32_t s_m[kWaves];
+    const int32_t n = blockIdx.x / blocks_w, w0 = (blockIdx.x % blocks_w) * kBwdBlockCols;
+    int32_t mixed = 0;
+    for (int32_t i = threadIdx.x; i < D * kBwdBlockCols; i += kBlock) {
+        const int32_t d = i / kBwdBlockCols, w = w0 + i % kBwdBlockCols;
+        if (w < W && combo_cell[(int64_t(n) * D + d) * W + w] == -2) mixed = 1;
+    }
+    mixed = block_reduce<true>(mixed, s_m);
+    if (threadIdx.x == 0) {
+        flags[blockIdx.x] = mixed;
+        if (mixed) atomicAdd(count, 1);
+    }
 }
 
 // Not enough empty rows to hold the partial sums: cells fed by several
@@ -589,6 +607,7 @@ __global__ __launch_bounds__(kBlock) void k_multi_slots(const uint32_t *key, con
                                                         int32_t n, const int32_t *empty_cells,
                                                         int2 *table, int32_t *head_flag) {
     const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+    if (i == 0) head_flag[n] = 0;   // scanned over n + 1 entries
     if (i >= n) return;
     table[val[i]].x = empty_cells[i];
     head_flag[i] = (i == 0 || key[i] != key[i - 1]) ? 1 : 0;
@@ -611,16 +630,15 @@ __global__ __launch_bounds__(kBlock) void k_multi_cells(const uint32_t *key, con
 
 // The borrowed rows of the first kCombineInline slots of each multi-combo
 // cell, next to each other, so that the combine kernel finds them with one
-// access (slot i belongs to cell head_scan[i + 1] - 1).
-__global__ __launch_bounds__(kBlock) void k_multi_rows(const int32_t *head_scan,
-                                                       const int32_t *multi_begin, int32_t n,
+// access; -1 past the cell's last slot. One thread per entry.
+__global__ __launch_bounds__(kBlock) void k_multi_rows(const int32_t *multi_begin, int32_t n_multi,
                                                        const int32_t *empty_cells,
                                                        int32_t *multi_rows) {
-    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
-    if (i >= n) return;
-    const int32_t k = head_scan[i + 1] - 1;
-    const int32_t u = i - multi_begin[k];
-    if (u < kCombineInline) multi_rows[int64_t(k) * kCombineInline + u] = empty_cells[i];
+    const int64_t x = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    if (x >= int64_t(n_multi) * kCombineInline) return;
+    const int32_t k = int32_t(x / kCombineInline), u = int32_t(x % kCombineInline);
+    const int32_t s = multi_begin[k] + u;
+    multi_rows[x] = s < multi_begin[k + 1] ? empty_cells[s] : -1;
 }
 
 // Generic cells keyed for a descending sort by point count.
@@ -635,13 +653,15 @@ __global__ __launch_bounds__(kBlock) void k_compact_generic(const int32_t *cell_
 }
 
 // 1 where a kept point of a generic cell starts a run: its previous depth
-// bin (same pixel) is not a point of the same cell.
+// bin (same pixel) is not a point of the same cell (one more entry, 0, ends
+// the flags).
 __global__ __launch_bounds__(kBlock) void k_run_flags(const int32_t *sorted_point, int32_t n_kept,
                                                       const int32_t *cell_of_point,
                                                       const int32_t *generic_pos, int32_t HW,
                                                       FastDiv div_hw, FastDiv div_d, int32_t D,
                                                       int32_t *flag) {
     const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+    if (i == 0) flag[n_kept] = 0;   // scanned over n_kept + 1 entries
     if (i >= n_kept) return;
     const int32_t p = sorted_point[i];
     const int32_t c = cell_of_point[p];
@@ -651,12 +671,14 @@ __global__ __launch_bounds__(kBlock) void k_run_flags(const int32_t *sorted_poin
     flag[i] = (generic && (d == 0 || cell_of_point[p - HW] != c)) ? 1 : 0;
 }
 
-// Runs per listed generic cell, and each cell's list position.
+// Runs per listed generic cell (one more entry, 0, for the scan), and each
+// cell's list position.
 __global__ __launch_bounds__(kBlock) void k_generic_counts(const int32_t *gen_cell, int32_t n_gen,
                                                            const int32_t *cell_start,
                                                            const int32_t *run_scan,
                                                            int32_t *runs_of, int32_t *pos_of_cell) {
     const int32_t k = blockIdx.x * kBlock + threadIdx.x;
+    if (k == 0) runs_of[n_gen] = 0;   // scanned over n_gen + 1 entries
     if (k >= n_gen) return;
     const int32_t c = gen_cell[k];
     runs_of[k] = run_scan[cell_start[c + 1]] - run_scan[cell_start[c]];
@@ -797,12 +819,17 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
 
     // stable LSD radix sort of (keys, vals)[0, n) on the low `bits` bits; the
     // result ends in (keys, vals)
-    auto radix_sort = [&](uint32_t *keys, int32_t *vals, int32_t n, int bits) -> int {
+    // Stable LSD radix sort of n (key, value) pairs on the keys' low `bits`
+    // bits, 8 per pass, ping-ponging between keys / kalt and vals / valt;
+    // keys and vals are left pointing at the buffers that hold the result
+    // (vals ends in valt after an odd number of passes).
+    auto radix_sort = [&](uint32_t *&keys, uint32_t *kalt, int32_t *&vals, int32_t *valt, int32_t n,
+                          int bits) -> int {
         if (n <= 0) return BEVPOOL_OK;
         const int tiles = int((int64_t(n) + kSortTile - 1) / kSortTile);
         const int passes = (bits + 7) / 8;
-        uint32_t *kin = keys, *kout = keys == keys_a ? keys_b : keys_a;
-        int32_t *vin = vals, *vout = vals == vals_b ? vals_a : vals_b;
+        uint32_t *kin = keys, *kout = kalt;
+        int32_t *vin = vals, *vout = valt;
         for (int pass = 0; pass < passes; ++pass) {
             const int shift = 8 * pass;
             hipLaunchKernelGGL(k_radix_hist, dim3(tiles), dim3(kBlock), 0, stream, kin, n, shift, hist);
@@ -813,12 +840,8 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
             std::swap(kin, kout);
             std::swap(vin, vout);
         }
-        if (kin != keys)
-            BEVPOOL_HIP(hipMemcpyAsync(keys, kin, sizeof(uint32_t) * size_t(n),
-                                       hipMemcpyDeviceToDevice, stream));
-        if (vin != vals)
-            BEVPOOL_HIP(hipMemcpyAsync(vals, vin, sizeof(int32_t) * size_t(n),
-                                       hipMemcpyDeviceToDevice, stream));
+        keys = kin;
+        vals = vin;
         return BEVPOOL_OK;
     };
     auto bits_for = [](int64_t max_key) {
@@ -874,12 +897,17 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         if ((rc2 = arena.take(&flag_b, size_t(n_cells) + 1, "flags"))) return rc2;
 
         fill(small, 16, 0);
+        // the sort's point ids start in the buffer from which its passes end
+        // in sorted_point (vals_b for an odd number of passes)
+        const bool odd_passes = ((bits_for(n_cells) + 7) / 8) % 2 == 1;
+        int32_t *ids0 = odd_passes ? vals_b : plan->sorted_point;
+        int32_t *ids1 = odd_passes ? plan->sorted_point : vals_b;
         if (host_cells) {
             // a stored association: the cell map as exported, checked by the caller
             BEVPOOL_HIP(hipMemcpyAsync(plan->cell_of_point, host_cells, sizeof(int32_t) * size_t(np),
                                        hipMemcpyHostToDevice, stream));
             hipLaunchKernelGGL(k_keys_from_cells, dim3(blocks_for(np)), dim3(kBlock), 0, stream,
-                               plan->cell_of_point, np, n_cells, keys_a, plan->sorted_point);
+                               plan->cell_of_point, np, n_cells, keys_a, ids0);
         } else {
             BEVPOOL_HIP(hipMemcpyAsync(d_calib, intrinsics, sizeof(double) * 4 * g.n_cams,
                                        hipMemcpyHostToDevice, stream));
@@ -900,15 +928,23 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
             pa.nz = nz;
             pa.cell_of_point = plan->cell_of_point;
             pa.keys = keys_a;
-            pa.vals = plan->sorted_point;
+            pa.vals = ids0;
             hipLaunchKernelGGL(k_project, dim3(blocks_for(np)), dim3(kBlock), 0, stream, pa);
         }
         BEVPOOL_HIP(hipGetLastError());
-        if ((rc2 = radix_sort(keys_a, plan->sorted_point, np, bits_for(n_cells)))) return rc2;
+        uint32_t *skeys = keys_a;
+        int32_t *sids = ids0;
+        if ((rc2 = radix_sort(skeys, keys_b, sids, ids1, np, bits_for(n_cells)))) return rc2;
+        if (sids != plan->sorted_point)
+            BEVPOOL_HIP(hipMemcpyAsync(plan->sorted_point, sids, sizeof(int32_t) * size_t(np),
+                                       hipMemcpyDeviceToDevice, stream));
         hipLaunchKernelGGL(k_cell_start, dim3(blocks_for(int64_t(np) + 1)), dim3(kBlock), 0,
-                           stream, keys_a, np, n_cells, plan->cell_start);
+                           stream, skeys, np, n_cells, plan->cell_start);
+        // per-cell counters of the combo walk, cleared by k_cell_stats
+        if ((rc2 = arena.take(&cell_generic, size_t(n_cells), "cell classes"))) return rc2;
+        if ((rc2 = arena.take(&cell_ncombo, size_t(n_cells), "cell combos"))) return rc2;
         hipLaunchKernelGGL(k_cell_stats, dim3(reduce_blocks(n_cells)), dim3(kBlock), 0, stream,
-                           plan->cell_start, n_cells, small);
+                           plan->cell_start, n_cells, small, cell_generic, cell_ncombo);
         BEVPOOL_HIP(hipGetLastError());
 
         // combos, cell classes and the column table
@@ -921,10 +957,6 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         int32_t *seg_cell = nullptr, *seg_range = nullptr;
         if ((rc2 = arena.take(&seg_cell, size_t(n_seg), "segment cells"))) return rc2;
         if ((rc2 = arena.take(&seg_range, size_t(n_seg), "segment rows"))) return rc2;
-        if ((rc2 = arena.take(&cell_generic, size_t(n_cells), "cell classes"))) return rc2;
-        if ((rc2 = arena.take(&cell_ncombo, size_t(n_cells), "cell combos"))) return rc2;
-        fill(cell_generic, n_cells, 0);
-        fill(cell_ncombo, n_cells, 0);
         ComboArgs ca;
         ca.cell_of_point = plan->cell_of_point;
         ca.N = N;
@@ -946,9 +978,6 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
                            plan->column_table, n_seg);
         int32_t stats[4], counters[2], n_gen = 0, n_empty = 0, kept = 0, n_part = 0;
         auto classify = [&]() -> int {
-            fill(flag_a, int64_t(n_cells) + 1, 0);
-            fill(flag_b, int64_t(n_cells) + 1, 0);
-            fill(combo_flag, n_seg_act + 1, 0);
             fill(small + 4, 2, 0);
             hipLaunchKernelGGL(k_cell_class, dim3(reduce_blocks(n_cells)), dim3(kBlock), 0, stream, ca,
                                plan->cell_start, n_cells, flag_a, flag_b, small + 4);
@@ -1006,7 +1035,6 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         plan->n_partials = n_part;
         // planes in use, from the final table (cells demoted to generic leave
         // their segments' planes empty)
-        fill(small + 2, 1, 0);
         hipLaunchKernelGGL(k_planes_used, dim3(reduce_blocks(n_seg_act)), dim3(kBlock), 0, stream,
                            plan->column_table, n_seg_act, int32_t(n_combo), small + 2);
 
@@ -1016,12 +1044,8 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         plan->n_bwd_blocks = N * bwd_bw;
         if ((rc2 = dev_alloc(&plan->bwd_mixed, size_t(plan->n_bwd_blocks), "backward blocks")))
             return rc2;
-        fill(plan->bwd_mixed, plan->n_bwd_blocks, 0);
-        hipLaunchKernelGGL(k_bwd_flags, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream,
-                           combo_cell, int32_t(n_combo), W, D, bwd_bw, plan->bwd_mixed);
-        fill(small + 12, 1, 0);
-        hipLaunchKernelGGL(k_count_flags, dim3(blocks_for(plan->n_bwd_blocks)), dim3(kBlock), 0,
-                           stream, plan->bwd_mixed, plan->n_bwd_blocks, small + 12);
+        hipLaunchKernelGGL(k_bwd_blocks, dim3(plan->n_bwd_blocks), dim3(kBlock), 0, stream,
+                           combo_cell, W, D, bwd_bw, plan->bwd_mixed, small + 12);
         if ((rc2 = dev_alloc(&plan->combo_cols, size_t(n_combo), "combos by column"))) return rc2;
         hipLaunchKernelGGL(k_combo_cols, dim3(blocks_for(n_combo)), dim3(kBlock), 0, stream,
                            combo_cell, combo_range, plan->bwd_mixed, int32_t(n_combo), W, D, bwd_bw,
@@ -1036,55 +1060,63 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         // partial-sum slots of the multi-combo cells, kept in the first
         // n_part empty rows
         if ((rc2 = arena.take(&head_scan, size_t(n_part) + 1, "multi heads"))) return rc2;
-        fill(head_scan, int64_t(n_part) + 1, 0);
+        uint32_t *mkeys = keys_a;
+        int32_t *mvals = vals_a;
         if (n_part > 0) {
             hipLaunchKernelGGL(k_multi_compact, dim3(blocks_for(n_seg_act)), dim3(kBlock), 0, stream,
                                seg_cell, combo_flag, int32_t(n_seg_act), keys_a, vals_a);
-            if ((rc2 = radix_sort(keys_a, vals_a, n_part, bits_for(n_cells)))) return rc2;
+            if ((rc2 = radix_sort(mkeys, keys_b, mvals, vals_b, n_part, bits_for(n_cells)))) return rc2;
             hipLaunchKernelGGL(k_multi_slots, dim3(blocks_for(n_part)), dim3(kBlock), 0, stream,
-                               keys_a, vals_a, n_part, plan->empty_cells, plan->column_table,
+                               mkeys, mvals, n_part, plan->empty_cells, plan->column_table,
                                head_scan);
+            // the number of multi-combo cells lands in small[3]
+            device_scan(head_scan, int64_t(n_part) + 1, small + 3, scan_sums, stream);
+        } else {
+            fill(head_scan, 1, 0);
         }
-        device_scan(head_scan, int64_t(n_part) + 1, small + 3, scan_sums, stream);
         BEVPOOL_HIP(hipGetLastError());
-        int32_t n_multi, n_planes, n_mixed;
-        if ((rc2 = to_host(&n_multi, head_scan + n_part))) return rc2;
-        if ((rc2 = to_host(&n_planes, small + 2))) return rc2;
-        if ((rc2 = to_host(&n_mixed, small + 12))) return rc2;
+        // one read-back for the counts that size the remaining arrays
+        int32_t h[16];
+        BEVPOOL_HIP(hipMemcpyAsync(h, small, sizeof(h), hipMemcpyDeviceToHost, stream));
         BEVPOOL_HIP(hipStreamSynchronize(stream));
-        plan->n_bwd_mixed = n_mixed;
+        const int32_t n_multi = n_part > 0 ? h[3] : 0;
+        plan->n_bwd_mixed = h[12];
         plan->n_multi = n_multi;
-        plan->n_planes = n_planes > 0 ? n_planes : 1;
+        plan->n_planes = h[2] > 0 ? h[2] : 1;
         if ((rc2 = dev_alloc(&plan->multi_begin, size_t(n_multi) + 1, "multi_begin"))) return rc2;
         if ((rc2 = dev_alloc(&plan->multi_cell, size_t(n_multi), "multi_cell"))) return rc2;
-        hipLaunchKernelGGL(k_multi_cells, dim3(blocks_for(int64_t(n_part) + 1)), dim3(kBlock), 0,
-                           stream, keys_a, head_scan, n_part, plan->multi_begin, plan->multi_cell);
-        BEVPOOL_HIP(hipGetLastError());
         if ((rc2 = dev_alloc(&plan->multi_rows, size_t(n_multi) * kCombineInline, "multi_rows")))
             return rc2;
-        fill(plan->multi_rows, int64_t(n_multi) * kCombineInline, -1);
-        if (n_part > 0) {
-            hipLaunchKernelGGL(k_multi_rows, dim3(blocks_for(n_part)), dim3(kBlock), 0, stream,
-                               head_scan, plan->multi_begin, n_part, plan->empty_cells,
-                               plan->multi_rows);
-            BEVPOOL_HIP(hipGetLastError());
-        }
+        if ((rc2 = dev_alloc(&plan->generic_hdr, size_t(n_gen), "generic_hdr"))) return rc2;
+        hipLaunchKernelGGL(k_multi_cells, dim3(blocks_for(int64_t(n_part) + 1)), dim3(kBlock), 0,
+                           stream, mkeys, head_scan, n_part, plan->multi_begin, plan->multi_cell);
+        if (n_multi > 0)
+            hipLaunchKernelGGL(k_multi_rows, dim3(blocks_for(int64_t(n_multi) * kCombineInline)),
+                               dim3(kBlock), 0, stream, plan->multi_begin, n_multi,
+                               plan->empty_cells, plan->multi_rows);
+        BEVPOOL_HIP(hipGetLastError());
 
         // generic cells by descending point count
-        if ((rc2 = dev_alloc(&plan->generic_hdr, size_t(n_gen), "generic_hdr"))) return rc2;
-        uint32_t *gen_key = keys_a;   // free again after k_multi_cells
+        if (n_gen == 0) {
+            // every cell with points is column-served (a level rig): no runs
+            plan->n_runs = 0;
+            if ((rc2 = dev_alloc(&plan->generic_runs, 0, "generic_runs"))) return rc2;
+            BEVPOOL_HIP(hipGetLastError());
+            BEVPOOL_HIP(hipStreamSynchronize(stream));
+            return BEVPOOL_OK;
+        }
+        uint32_t *gen_key = keys_a;   // the sort buffers are free again after k_multi_cells
         int32_t *gen_cell = vals_a;
         hipLaunchKernelGGL(k_compact_generic, dim3(blocks_for(n_cells)), dim3(kBlock), 0, stream,
                            plan->cell_start, n_cells, flag_a, plan->max_per_cell, gen_key, gen_cell);
         BEVPOOL_HIP(hipGetLastError());
-        if ((rc2 = radix_sort(gen_key, gen_cell, n_gen, bits_for(plan->max_per_cell)))) return rc2;
+        if ((rc2 = radix_sort(gen_key, keys_b, gen_cell, vals_b, n_gen, bits_for(plan->max_per_cell))))
+            return rc2;
 
         // runs of the generic cells, in list order
         if ((rc2 = arena.take(&run_scan, size_t(kept) + 1, "run flags"))) return rc2;
         if ((rc2 = arena.take(&run_begin, size_t(n_gen) + 1, "run offsets"))) return rc2;
         if ((rc2 = arena.take(&pos_of_cell, size_t(n_cells), "cell positions"))) return rc2;
-        fill(run_scan, int64_t(kept) + 1, 0);
-        fill(run_begin, int64_t(n_gen) + 1, 0);
         const FastDiv div_hw = make_fastdiv(uint32_t(HW)), div_d = make_fastdiv(uint32_t(D));
         if (kept > 0)
             hipLaunchKernelGGL(k_run_flags, dim3(blocks_for(kept)), dim3(kBlock), 0, stream,
@@ -1222,18 +1254,21 @@ int bevpool_associate_into(const double *intrinsics, const double *extrinsics,
     pa.n_points = np;
     pa.n_cells = n_cells;
     pa.nz = 1;
+    // stable LSD radix sort of (cell, point id) on the cell's bits, 8 per
+    // pass; the ids start in the buffer from which the passes end in
+    // sorted_point
+    int bits = 1;
+    while ((int64_t(1) << bits) <= int64_t(n_cells)) ++bits;
+    const bool odd_passes = ((bits + 7) / 8) % 2 == 1;
     pa.cell_of_point = cell_of_point;
     pa.keys = keys_a;
-    pa.vals = sorted_point;
+    pa.vals = odd_passes ? vals_b : sorted_point;
     hipLaunchKernelGGL(k_project, dim3(blocks_for(np)), dim3(kBlock), 0, stream, pa);
     BEVPOOL_HIP(hipGetLastError());
 
-    // stable LSD radix sort of (cell, point id) on the cell's bits, 8 per pass
-    int bits = 1;
-    while ((int64_t(1) << bits) <= int64_t(n_cells)) ++bits;
     const int tiles = int((int64_t(np) + kSortTile - 1) / kSortTile);
     uint32_t *kin = keys_a, *kout = keys_b;
-    int32_t *vin = sorted_point, *vout = vals_b;
+    int32_t *vin = pa.vals, *vout = odd_passes ? sorted_point : vals_b;
     for (int shift = 0; shift < bits; shift += 8) {
         hipLaunchKernelGGL(k_radix_hist, dim3(tiles), dim3(kBlock), 0, stream, kin, np, shift, hist);
         device_scan(hist, int64_t(tiles) * 256, small + 3, sums, stream);
