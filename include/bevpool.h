@@ -329,7 +329,7 @@ BEVPOOL_API int bevpool_plan_import(const int32_t *cell_of_point, const bevpool_
  *              is the kept count.
  * The results equal bevpool_plan's bit for bit. Limits: at most 2^22
  * points and 16 cameras. The temporaries live in one fixed device array of
- * 50 MiB per device, held while the library is loaded and shared by every
+ * 52 MiB per device, held while the library is loaded and shared by every
  * call on that device: calls that overlap on one device (two streams, or two
  * host threads) race and must be serialised by the caller. Asynchronous and
  * stream-ordered on hip_stream: no host synchronisation, no allocation, no

@@ -131,7 +131,7 @@ int bevpool_launch_to_nchw(const float *in, int64_t in_row_stride, float *out, i
 // temporaries in a fixed device array of kAssocScratchTotal bytes per device.
 constexpr int64_t kAssocMaxPoints = int64_t(1) << 22;
 constexpr int kAssocMaxCams = 16;
-constexpr size_t kAssocScratchTotal = 52431616;   // 50 MiB
+constexpr size_t kAssocScratchTotal = 54529280;   // 52 MiB
 int bevpool_associate_into(const double *intrinsics, const double *extrinsics,
                            const bevpool_geometry &g, int32_t *cell_of_point,
                            int32_t *sorted_point, int32_t *cell_start, hipStream_t stream);

@@ -5,7 +5,8 @@
 //
 // Kernels, in launch order:
 //   k_project      one thread per point: camera ray -> ego frame -> cell id
-//   k_radix_hist   } stable LSD radix sort of (cell, point id), 8-bit digits;
+//   k_radix_hist   } stable LSD radix sort of (cell, point id), digits of
+//                  } at most 9 bits;
 //   k_scan...      } input in id order, so ties stay in id order (scans:
 //   k_radix_scatter} one workgroup for a short array, else chunk sums,
 //                    their scan and per-chunk scans from the offsets)
@@ -36,10 +37,20 @@ namespace {
 constexpr int kSortItems = 8;                       // keys per thread per tile
 constexpr int kSortTile = kBlock * kSortItems;      // 2048 keys per workgroup
 constexpr int kWaveItems = kWaveSize * kSortItems;  // 512 keys per wave
+constexpr int kRadixBits = 9;                       // digit bits per pass, at most
+constexpr int kRadixBins = 1 << kRadixBits;         // 512 digits, at most two per thread
+
+// A sort on `bits` key bits takes the fewest passes of at most kRadixBits
+// bits, with the bits split evenly over them (17-bit cell ids: two passes of
+// 9; 19 bits: three of 7, whose 128-digit histograms are cheaper than 512).
+constexpr int radix_passes(int bits) { return (bits + kRadixBits - 1) / kRadixBits; }
+constexpr int radix_digit_bits(int bits) {
+    return (bits + radix_passes(bits) - 1) / radix_passes(bits);
+}
 constexpr int kScanBlock = 1024;
 constexpr int kScanItems = 4;
 constexpr int kScanChunk = kScanBlock * kScanItems;  // elements per workgroup of a multi-block scan
-static_assert(kBlock == 256, "one radix digit per thread");
+static_assert(kBlock == 256, "a sort tile is four waves of 512 keys");
 
 struct ProjectArgs {
     const double *intr;  // [N][4]
@@ -197,38 +208,48 @@ __global__ __launch_bounds__(kScanBlock) void k_scan_apply(int32_t *data, int64_
 // Digit histogram of each 2048-key tile, stored digit-major:
 // hist[digit * n_tiles + tile], so an exclusive scan of the whole array
 // gives every (digit, tile) its first output slot in stable order.
+// Digit counts of one tile: hist[digit * tiles + tile], digits of dbits
+// bits (dbits <= kRadixBits) from bit `shift` on.
 __global__ __launch_bounds__(kBlock) void k_radix_hist(const uint32_t *keys, int32_t n,
-                                                       int shift, int32_t *hist) {
-    __shared__ int cnt[256];
-    cnt[threadIdx.x] = 0;
+                                                       int shift, int dbits, int32_t *hist) {
+    __shared__ int cnt[kRadixBins];
+    const int bins = 1 << dbits;
+    const uint32_t mask = uint32_t(bins) - 1u;
+    for (int d = threadIdx.x; d < bins; d += kBlock) cnt[d] = 0;
     __syncthreads();
     const int64_t base = int64_t(blockIdx.x) * kSortTile;
 #pragma unroll
     for (int k = 0; k < kSortItems; ++k) {
         const int64_t i = base + int64_t(k) * kBlock + threadIdx.x;
-        if (i < n) atomicAdd(&cnt[(keys[i] >> shift) & 255u], 1);
+        if (i < n) atomicAdd(&cnt[(keys[i] >> shift) & mask], 1);
     }
     __syncthreads();
-    hist[int64_t(threadIdx.x) * gridDim.x + blockIdx.x] = cnt[threadIdx.x];
+    for (int d = threadIdx.x; d < bins; d += kBlock)
+        hist[int64_t(d) * gridDim.x + blockIdx.x] = cnt[d];
 }
 
 // Stable scatter. Wave w of a tile owns keys [w*512, (w+1)*512) of the tile
 // and walks them 64 at a time in order. Within a step, a key's rank among
-// equal digits comes from eight ballots (one per digit bit): lanes whose
-// ballots agree on every bit hold the same digit. A per-wave LDS counter per
+// equal digits comes from one ballot per digit bit: lanes whose ballots
+// agree on every bit hold the same digit. A per-wave LDS counter per
 // digit carries ranks across steps. Per-wave counts are then prefixed across
 // the waves and added to the scanned global offsets.
 __global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t *keys_in,
                                                           const int32_t *vals_in, int32_t n,
-                                                          int shift, const int32_t *hist_scan,
+                                                          int shift, int dbits,
+                                                          const int32_t *hist_scan,
                                                           uint32_t *keys_out, int32_t *vals_out) {
-    __shared__ int wcount[kWaves][256];
-    __shared__ int gbase[256];
+    __shared__ int wcount[kWaves][kRadixBins];
+    __shared__ int gbase[kRadixBins];
+    const int bins = 1 << dbits;
+    const uint32_t mask = uint32_t(bins) - 1u;
     const int lane = threadIdx.x & (kWaveSize - 1);
     const int wave = threadIdx.x / kWaveSize;
+    for (int d = threadIdx.x; d < bins; d += kBlock) {
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) wcount[w][threadIdx.x] = 0;
-    gbase[threadIdx.x] = hist_scan[int64_t(threadIdx.x) * gridDim.x + blockIdx.x];
+        for (int w = 0; w < kWaves; ++w) wcount[w][d] = 0;
+        gbase[d] = hist_scan[int64_t(d) * gridDim.x + blockIdx.x];
+    }
     __syncthreads();
 
     const int64_t base = int64_t(blockIdx.x) * kSortTile + int64_t(wave) * kWaveItems;
@@ -242,13 +263,15 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t *keys_i
         const bool valid = i < n;
         key[k] = valid ? keys_in[i] : 0u;
         val[k] = valid ? vals_in[i] : 0;
-        const uint32_t digit = (key[k] >> shift) & 255u;
+        const uint32_t digit = (key[k] >> shift) & mask;
         uint64_t same = __ballot(valid);
 #pragma unroll
-        for (int b = 0; b < 8; ++b) {
-            const bool bit = (digit >> b) & 1u;
-            const uint64_t ones = __ballot(bit);
-            same &= bit ? ones : ~ones;
+        for (int b = 0; b < kRadixBits; ++b) {
+            if (b < dbits) {   // uniform over the workgroup
+                const bool bit = (digit >> b) & 1u;
+                const uint64_t ones = __ballot(bit);
+                same &= bit ? ones : ~ones;
+            }
         }
         const int before = __popcll(same & lanes_below);
         const int prior = wcount[wave][digit];
@@ -259,12 +282,12 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t *keys_i
         __builtin_amdgcn_wave_barrier();
     }
     __syncthreads();
-    {
+    for (int d = threadIdx.x; d < bins; d += kBlock) {
         int run = 0;
 #pragma unroll
         for (int w = 0; w < kWaves; ++w) {
-            const int c = wcount[w][threadIdx.x];
-            wcount[w][threadIdx.x] = run;
+            const int c = wcount[w][d];
+            wcount[w][d] = run;
             run += c;
         }
     }
@@ -273,7 +296,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t *keys_i
     for (int k = 0; k < kSortItems; ++k) {
         const int64_t i = base + int64_t(k) * kWaveSize + lane;
         if (i < n) {
-            const uint32_t digit = (key[k] >> shift) & 255u;
+            const uint32_t digit = (key[k] >> shift) & mask;
             const int64_t pos = int64_t(gbase[digit]) + wcount[wave][digit] + rank[k];
             keys_out[pos] = key[k];
             vals_out[pos] = val[k];
@@ -817,25 +840,25 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
     int32_t *run_scan = nullptr, *run_begin = nullptr, *pos_of_cell = nullptr;
     auto cleanup = [&]() { (void)hipFree(arena.base); };
 
-    // stable LSD radix sort of (keys, vals)[0, n) on the low `bits` bits; the
-    // result ends in (keys, vals)
     // Stable LSD radix sort of n (key, value) pairs on the keys' low `bits`
-    // bits, 8 per pass, ping-ponging between keys / kalt and vals / valt;
-    // keys and vals are left pointing at the buffers that hold the result
-    // (vals ends in valt after an odd number of passes).
+    // bits (radix_passes passes of radix_digit_bits bits), ping-ponging
+    // between keys / kalt and vals / valt; keys and vals are left pointing at
+    // the buffers that hold the result (vals ends in valt after an odd number
+    // of passes).
     auto radix_sort = [&](uint32_t *&keys, uint32_t *kalt, int32_t *&vals, int32_t *valt, int32_t n,
                           int bits) -> int {
         if (n <= 0) return BEVPOOL_OK;
         const int tiles = int((int64_t(n) + kSortTile - 1) / kSortTile);
-        const int passes = (bits + 7) / 8;
+        const int passes = radix_passes(bits), dbits = radix_digit_bits(bits);
         uint32_t *kin = keys, *kout = kalt;
         int32_t *vin = vals, *vout = valt;
         for (int pass = 0; pass < passes; ++pass) {
-            const int shift = 8 * pass;
-            hipLaunchKernelGGL(k_radix_hist, dim3(tiles), dim3(kBlock), 0, stream, kin, n, shift, hist);
-            device_scan(hist, int64_t(tiles) * 256, small + 3, scan_sums, stream);
+            const int shift = dbits * pass;
+            hipLaunchKernelGGL(k_radix_hist, dim3(tiles), dim3(kBlock), 0, stream, kin, n, shift,
+                               dbits, hist);
+            device_scan(hist, int64_t(tiles) << dbits, small + 3, scan_sums, stream);
             hipLaunchKernelGGL(k_radix_scatter, dim3(tiles), dim3(kBlock), 0, stream, kin, vin, n,
-                               shift, hist, kout, vout);
+                               shift, dbits, hist, kout, vout);
             BEVPOOL_HIP(hipGetLastError());
             std::swap(kin, kout);
             std::swap(vin, vout);
@@ -868,7 +891,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
             const size_t cells1_b = Arena::piece((size_t(n_cells) + 1) * i4);
             const size_t combo1_b = Arena::piece((size_t(n_seg) + 1) * i4);
             arena.cap = Arena::piece(size_t(g.n_cams) * 16 * sizeof(double)) + 4 * sort_b +
-                        Arena::piece(size_t(sort_tiles_cap) * 256 * i4) + Arena::piece(16 * i4) +
+                        Arena::piece(size_t(sort_tiles_cap) * kRadixBins * i4) + Arena::piece(16 * i4) +
                         Arena::piece(size_t(scan_sums_needed(sort_cap + 1)) * i4) +
                         5 * cells1_b +                 // flag_a, flag_b, cell_generic, cell_ncombo, run_begin
                         Arena::piece(size_t(n_cells) * i4) +          // pos_of_cell
@@ -884,7 +907,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         if ((rc2 = arena.take(&keys_b, size_t(sort_cap), "sort keys"))) return rc2;
         if ((rc2 = arena.take(&vals_a, size_t(sort_cap), "sort values"))) return rc2;
         if ((rc2 = arena.take(&vals_b, size_t(sort_cap), "sort values"))) return rc2;
-        if ((rc2 = arena.take(&hist, size_t(sort_tiles_cap) * 256, "radix histogram"))) return rc2;
+        if ((rc2 = arena.take(&hist, size_t(sort_tiles_cap) * kRadixBins, "radix histogram"))) return rc2;
         // [0..1] cell stats, [3] scan totals, [4..5] class counters, [6] most
         // segments of a combo, [7] their kept points, [8..11] gathered counts,
         // [12] backward blocks with a combo that is not clean
@@ -899,7 +922,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         fill(small, 16, 0);
         // the sort's point ids start in the buffer from which its passes end
         // in sorted_point (vals_b for an odd number of passes)
-        const bool odd_passes = ((bits_for(n_cells) + 7) / 8) % 2 == 1;
+        const bool odd_passes = radix_passes(bits_for(n_cells)) % 2 == 1;
         int32_t *ids0 = odd_passes ? vals_b : plan->sorted_point;
         int32_t *ids1 = odd_passes ? plan->sorted_point : vals_b;
         if (host_cells) {
@@ -1166,13 +1189,13 @@ namespace {
 
 constexpr size_t scratch_piece(size_t b) { return (b + 255) & ~size_t(255); }
 constexpr int64_t kAssocTiles = (kAssocMaxPoints + kSortTile - 1) / kSortTile;
-constexpr int64_t kAssocSums = (kAssocTiles * 256 + kScanChunk - 1) / kScanChunk;
+constexpr int64_t kAssocSums = (kAssocTiles * kRadixBins + kScanChunk - 1) / kScanChunk;
 constexpr size_t kOffCalib = 0;
 constexpr size_t kOffKeysA = kOffCalib + scratch_piece(size_t(kAssocMaxCams) * 16 * sizeof(double));
 constexpr size_t kOffKeysB = kOffKeysA + scratch_piece(size_t(kAssocMaxPoints) * 4);
 constexpr size_t kOffValsB = kOffKeysB + scratch_piece(size_t(kAssocMaxPoints) * 4);
 constexpr size_t kOffHist = kOffValsB + scratch_piece(size_t(kAssocMaxPoints) * 4);
-constexpr size_t kOffSmall = kOffHist + scratch_piece(size_t(kAssocTiles) * 256 * 4);
+constexpr size_t kOffSmall = kOffHist + scratch_piece(size_t(kAssocTiles) * kRadixBins * 4);
 constexpr size_t kOffSums = kOffSmall + scratch_piece(16 * 4);
 constexpr size_t kAssocScratchBytes = kOffSums + scratch_piece(size_t(kAssocSums) * 4);
 static_assert(kAssocScratchBytes == kAssocScratchTotal, "scratch size stated in internal.h");
@@ -1254,12 +1277,12 @@ int bevpool_associate_into(const double *intrinsics, const double *extrinsics,
     pa.n_points = np;
     pa.n_cells = n_cells;
     pa.nz = 1;
-    // stable LSD radix sort of (cell, point id) on the cell's bits, 8 per
-    // pass; the ids start in the buffer from which the passes end in
-    // sorted_point
+    // stable LSD radix sort of (cell, point id) on the cell's bits
+    // (radix_passes passes); the ids start in the buffer from which the
+    // passes end in sorted_point
     int bits = 1;
     while ((int64_t(1) << bits) <= int64_t(n_cells)) ++bits;
-    const bool odd_passes = ((bits + 7) / 8) % 2 == 1;
+    const bool odd_passes = radix_passes(bits) % 2 == 1;
     pa.cell_of_point = cell_of_point;
     pa.keys = keys_a;
     pa.vals = odd_passes ? vals_b : sorted_point;
@@ -1269,11 +1292,13 @@ int bevpool_associate_into(const double *intrinsics, const double *extrinsics,
     const int tiles = int((int64_t(np) + kSortTile - 1) / kSortTile);
     uint32_t *kin = keys_a, *kout = keys_b;
     int32_t *vin = pa.vals, *vout = odd_passes ? sorted_point : vals_b;
-    for (int shift = 0; shift < bits; shift += 8) {
-        hipLaunchKernelGGL(k_radix_hist, dim3(tiles), dim3(kBlock), 0, stream, kin, np, shift, hist);
-        device_scan(hist, int64_t(tiles) * 256, small + 3, sums, stream);
+    const int dbits = radix_digit_bits(bits);
+    for (int shift = 0; shift < bits; shift += dbits) {
+        hipLaunchKernelGGL(k_radix_hist, dim3(tiles), dim3(kBlock), 0, stream, kin, np, shift, dbits,
+                           hist);
+        device_scan(hist, int64_t(tiles) << dbits, small + 3, sums, stream);
         hipLaunchKernelGGL(k_radix_scatter, dim3(tiles), dim3(kBlock), 0, stream, kin, vin, np, shift,
-                           hist, kout, vout);
+                           dbits, hist, kout, vout);
         BEVPOOL_HIP(hipGetLastError());
         std::swap(kin, kout);
         std::swap(vin, vout);
