@@ -50,11 +50,15 @@ constexpr int radix_digit_bits(int bits) {
 constexpr int kScanBlock = 1024;
 constexpr int kScanItems = 4;
 constexpr int kScanChunk = kScanBlock * kScanItems;  // elements per workgroup of a multi-block scan
+constexpr int kScanOneBlockChunks = 8;               // scans of up to 8 chunks take one workgroup
 static_assert(kBlock == 256, "a sort tile is four waves of 512 keys");
 
+constexpr int kArgCams = 16;   // cameras whose calibration travels in the kernel arguments
+
 struct ProjectArgs {
-    const double *intr;  // [N][4]
+    const double *intr;  // [N][4] in device memory, or null: the calibration is in cal
     const double *extr;  // [N][12]
+    double cal[kArgCams * 16];   // [N][4] intrinsics, then [N][12] extrinsics (intr null)
     bevpool_geometry g;
     FastDiv div_w, div_h, div_d;
     int32_t n_points, n_cells, nz;
@@ -78,9 +82,9 @@ __global__ __launch_bounds__(kBlock) void k_project(ProjectArgs a) {
     const int n = int(fdiv(q_h, a.div_d));
     const int d = int(q_h) - n * g.n_depth;
 
-    const double fx = a.intr[4 * n + 0], fy = a.intr[4 * n + 1];
-    const double cx = a.intr[4 * n + 2], cy = a.intr[4 * n + 3];
-    const double *E = a.extr + 12 * n;
+    const double *I = a.intr ? a.intr + 4 * n : a.cal + 4 * n;
+    const double *E = a.intr ? a.extr + 12 * n : a.cal + 4 * g.n_cams + 12 * n;
+    const double fx = I[0], fy = I[1], cx = I[2], cy = I[3];
     const double depth = g.depth_min + double(d) * g.depth_step;
     const double u = double(w) + g.pixel_offset;
     const double v = double(h) + g.pixel_offset;
@@ -345,12 +349,14 @@ __device__ __forceinline__ int32_t block_reduce(int32_t v, int32_t *s_red) {
     return v;
 }
 
-// Non-empty cells and the largest interval; clears two per-cell arrays
+// Non-empty cells and the largest interval into stats[0..1], the kept
+// count (cell_start[n_cells]) into stats[10]; clears two per-cell arrays
 // (the combo walk's counters) on the way.
 __global__ __launch_bounds__(kBlock) void k_cell_stats(const int32_t *cell_start, int32_t n_cells,
                                                        int32_t *stats /* nonempty, max */,
                                                        int32_t *clear_a, int32_t *clear_b) {
     __shared__ int32_t s_n[kWaves], s_m[kWaves];
+    if (blockIdx.x == 0 && threadIdx.x == 0) stats[10] = cell_start[n_cells];
     int32_t nonempty = 0, most = 0;
     for (int32_t c = blockIdx.x * kBlock + threadIdx.x; c < n_cells; c += gridDim.x * kBlock) {
         clear_a[c] = 0;
@@ -367,15 +373,6 @@ __global__ __launch_bounds__(kBlock) void k_cell_stats(const int32_t *cell_start
     }
 }
 
-// Four single counts next to each other, so that one copy brings them to
-// the host.
-__global__ void k_gather4(int32_t *dst, const int32_t *a, const int32_t *b, const int32_t *c,
-                          const int32_t *d) {
-    dst[0] = *a;
-    dst[1] = *b;
-    dst[2] = *c;
-    dst[3] = *d;
-}
 
 // ---------------------------------------------------------------- work partition
 //
@@ -401,6 +398,7 @@ struct ComboArgs {
     int32_t *seg_range;         // [planes][N*D*W]: its rows h_lo | h_hi << 16
     int32_t *max_seg;           // most segments of a column-served combo
     int32_t *served_pts;        // kept points of column-served combos
+    int32_t *class_counters;    // [2]: k_cell_class's counters, cleared here for it
 };
 
 // One thread per combo walks its H rows and splits the kept ones into
@@ -481,6 +479,7 @@ __device__ __forceinline__ void combo_walk_one(const ComboArgs &a, int32_t X, in
 
 __global__ __launch_bounds__(kBlock) void k_combo_walk(ComboArgs a) {
     __shared__ int32_t s_m[kWaves], s_p[kWaves];
+    if (blockIdx.x == 0 && threadIdx.x < 2) a.class_counters[threadIdx.x] = 0;
     const int64_t n_combo = int64_t(a.N) * a.D * a.W;
     int32_t max_seg = 0, served_pts = 0;
     for (int64_t x = int64_t(blockIdx.x) * kBlock + threadIdx.x; x < n_combo;
@@ -602,6 +601,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_blocks(const int32_t *combo_cell
 // combos become generic.
 __global__ __launch_bounds__(kBlock) void k_demote_multi(ComboArgs a, int32_t n_cells) {
     const int32_t c = blockIdx.x * kBlock + threadIdx.x;
+    if (c < 2) a.class_counters[c] = 0;
     if (c < n_cells && a.cell_generic[c] == 0 && a.cell_ncombo[c] > 1) a.cell_generic[c] = 1;
 }
 
@@ -788,7 +788,7 @@ int64_t scan_sums_needed(int64_t n) { return (n + kScanChunk - 1) / kScanChunk; 
 // scratch of scan_sums_needed(n) ints (unused for a single chunk).
 void device_scan(int32_t *data, int64_t n, int32_t *total, int32_t *sums, hipStream_t stream) {
     const int64_t nb = scan_sums_needed(n);
-    if (nb <= 1) {
+    if (nb <= kScanOneBlockChunks) {   // one launch: the workgroup walks the chunks
         hipLaunchKernelGGL(k_scan, dim3(1), dim3(kScanBlock), 0, stream, data, n, total);
         return;
     }
@@ -901,7 +901,9 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
                         Arena::piece((size_t(np) + 1) * i4);          // run_scan
             if ((rc2 = dev_alloc(&arena.base, arena.cap, "plan temporaries"))) return rc2;
         }
-        if (!host_cells && (rc2 = arena.take(&d_calib, size_t(g.n_cams) * 16, "calibration")))
+        const bool cal_in_args = g.n_cams <= kArgCams;
+        if (!host_cells && !cal_in_args &&
+            (rc2 = arena.take(&d_calib, size_t(g.n_cams) * 16, "calibration")))
             return rc2;
         if ((rc2 = arena.take(&keys_a, size_t(sort_cap), "sort keys"))) return rc2;
         if ((rc2 = arena.take(&keys_b, size_t(sort_cap), "sort keys"))) return rc2;
@@ -909,7 +911,8 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         if ((rc2 = arena.take(&vals_b, size_t(sort_cap), "sort values"))) return rc2;
         if ((rc2 = arena.take(&hist, size_t(sort_tiles_cap) * kRadixBins, "radix histogram"))) return rc2;
         // [0..1] cell stats, [3] scan totals, [4..5] class counters, [6] most
-        // segments of a combo, [7] their kept points, [8..11] gathered counts,
+        // segments of a combo, [7] their kept points, [8] generic cells, [9]
+        // empty cells, [10] kept points, [11] segments of multi-combo cells,
         // [12] backward blocks with a combo that is not clean
         if ((rc2 = arena.take(&small, 16, "plan counters"))) return rc2;
         // the longest scan is over sort_cap + 1 elements (radix histograms
@@ -932,16 +935,24 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
             hipLaunchKernelGGL(k_keys_from_cells, dim3(blocks_for(np)), dim3(kBlock), 0, stream,
                                plan->cell_of_point, np, n_cells, keys_a, ids0);
         } else {
-            BEVPOOL_HIP(hipMemcpyAsync(d_calib, intrinsics, sizeof(double) * 4 * g.n_cams,
-                                       hipMemcpyHostToDevice, stream));
-            BEVPOOL_HIP(hipMemcpyAsync(d_calib + 4 * g.n_cams, extrinsics,
-                                       sizeof(double) * 12 * g.n_cams, hipMemcpyHostToDevice, stream));
+            ProjectArgs pa;
+            if (cal_in_args) {
+                // up to kArgCams cameras: no host-to-device copy
+                pa.intr = pa.extr = nullptr;
+                memcpy(pa.cal, intrinsics, sizeof(double) * 4 * g.n_cams);
+                memcpy(pa.cal + 4 * g.n_cams, extrinsics, sizeof(double) * 12 * g.n_cams);
+            } else {
+                BEVPOOL_HIP(hipMemcpyAsync(d_calib, intrinsics, sizeof(double) * 4 * g.n_cams,
+                                           hipMemcpyHostToDevice, stream));
+                BEVPOOL_HIP(hipMemcpyAsync(d_calib + 4 * g.n_cams, extrinsics,
+                                           sizeof(double) * 12 * g.n_cams, hipMemcpyHostToDevice,
+                                           stream));
+                pa.intr = d_calib;
+                pa.extr = d_calib + 4 * g.n_cams;
+            }
 
             // Sec. III-B, precomputation: cell of every point, then the points
             // sorted by (cell, id) and the interval table.
-            ProjectArgs pa;
-            pa.intr = d_calib;
-            pa.extr = d_calib + 4 * g.n_cams;
             pa.g = g;
             pa.div_w = make_fastdiv(uint32_t(W));
             pa.div_h = make_fastdiv(uint32_t(H));
@@ -996,22 +1007,20 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
         ca.seg_range = seg_range;
         ca.max_seg = small + 6;
         ca.served_pts = small + 7;
+        ca.class_counters = small + 4;
+        // (k_combo_table writes every entry of every plane: no clearing first)
         hipLaunchKernelGGL(k_combo_walk, dim3(reduce_blocks(n_combo)), dim3(kBlock), 0, stream, ca);
-        hipLaunchKernelGGL(k_clear_table, dim3(blocks_for(n_seg)), dim3(kBlock), 0, stream,
-                           plan->column_table, n_seg);
         int32_t stats[4], counters[2], n_gen = 0, n_empty = 0, kept = 0, n_part = 0;
+        // (the class counters small[4..5] are cleared by k_combo_walk or
+        // k_demote_multi, which run before each classification)
         auto classify = [&]() -> int {
-            fill(small + 4, 2, 0);
             hipLaunchKernelGGL(k_cell_class, dim3(reduce_blocks(n_cells)), dim3(kBlock), 0, stream, ca,
                                plan->cell_start, n_cells, flag_a, flag_b, small + 4);
             hipLaunchKernelGGL(k_combo_table, dim3(blocks_for(n_seg_act)), dim3(kBlock), 0, stream,
                                ca, plan->column_table, combo_flag);
-            device_scan(flag_a, int64_t(n_cells) + 1, small + 3, scan_sums, stream);       // generic cells
-            device_scan(flag_b, int64_t(n_cells) + 1, small + 3, scan_sums, stream);       // empty cells
-            device_scan(combo_flag, n_seg_act + 1, small + 3, scan_sums, stream);   // segments of multi cells
-            BEVPOOL_HIP(hipGetLastError());
-            hipLaunchKernelGGL(k_gather4, dim3(1), dim3(1), 0, stream, small + 8, flag_a + n_cells,
-                               flag_b + n_cells, plan->cell_start + n_cells, combo_flag + n_seg_act);
+            device_scan(flag_a, int64_t(n_cells) + 1, small + 8, scan_sums, stream);       // generic cells
+            device_scan(flag_b, int64_t(n_cells) + 1, small + 9, scan_sums, stream);       // empty cells
+            device_scan(combo_flag, n_seg_act + 1, small + 11, scan_sums, stream);  // segments of multi cells
             BEVPOOL_HIP(hipGetLastError());
             int32_t h[12];
             BEVPOOL_HIP(hipMemcpyAsync(h, small, sizeof(h), hipMemcpyDeviceToHost, stream));
@@ -1024,7 +1033,7 @@ int bevpool_build_plan(const double *intrinsics, const double *extrinsics,
             counters[1] = h[5];
             n_gen = h[8];          // generic cells
             n_empty = h[9];        // empty cells
-            kept = h[10];          // kept points
+            kept = h[10];          // kept points (k_cell_stats)
             n_part = h[11];        // combos of multi-combo cells (partial slots)
             return BEVPOOL_OK;
         };
