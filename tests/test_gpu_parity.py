@@ -86,6 +86,18 @@ def _one_cell_rig():
                                cell_x=16.0, cell_y=16.0)
 
 
+def _ring20_rig():
+    """Twenty level cameras on the ring (more than the 16 whose calibration
+    the plan build passes in kernel arguments, so it is copied to the device
+    instead), 8x16 features, 24 depth bins, a 120 x 120 grid at 0.9 m."""
+    H, W, N = 8, 16, 20
+    intr = np.tile(np.array([[14.0, 14.0, W / 2.0, H / 2.0]]), (N, 1))
+    return dataclasses.replace(wl.ring_rig(), n_cams=N, feat_h=H, feat_w=W, n_depth=24,
+                               depth_min=1.0, depth_step=2.0, nx=120, ny=120, cell_x=0.9,
+                               cell_y=0.9, intrinsics=intr,
+                               extrinsics=wl._ring_extrinsics(N, 1.0, 1.5))
+
+
 def _tall_rig():
     """The tiny camera with a feature map of 16,400 rows (more than the 2^14
     that the column table's row fields hold), 3 columns and 3 depth bins:
@@ -105,7 +117,7 @@ RIGS = {
     "anisotropic": _anisotropic_rig, "coarse": _coarse_rig, "coarse_tilted": _coarse_tilted_rig,
     "empty": _empty_rig,
     "odd": lambda: _odd_rig(False), "odd_tilted": lambda: _odd_rig(True),
-    "one_cell": _one_cell_rig, "tall": _tall_rig,
+    "one_cell": _one_cell_rig, "tall": _tall_rig, "ring20": _ring20_rig,
 }
 
 
@@ -228,7 +240,7 @@ def test_forward_highres(torch_cuda, pkg, oracle_lib, oracle_plans):
 
 
 @pytest.mark.parametrize("name", ["coarse", "coarse_tilted", "anisotropic", "empty", "one_cell",
-                                  "odd", "odd_tilted", "tall"])
+                                  "odd", "odd_tilted", "tall", "ring20"])
 def test_forward_edge_rigs(torch_cuda, pkg, oracle_lib, oracle_plans, name):
     _say(f"[forward edge] {name}")
     rig = RIGS[name]()
@@ -253,6 +265,8 @@ def test_forward_edge_rigs(torch_cuda, pkg, oracle_lib, oracle_plans, name):
         assert plan.info.n_kept > 0 and plan.info.n_column > 0
         if name == "odd_tilted":
             assert plan.info.n_generic > 0
+    if name == "ring20":
+        assert plan.info.n_kept > 0 and plan.info.n_column > 0
     if name == "tall":
         counts = np.diff(cs)
         assert plan.info.n_column == 0 and plan.info.n_generic == int((counts > 0).sum())
